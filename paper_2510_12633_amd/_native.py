@@ -1,0 +1,213 @@
+"""ctypes binding of the C ABI in include/laminar_decode_attn.h.
+
+Argument marshalling only: every step of the computation runs in the HIP
+library. Importing this module does not touch the GPU; loading fails loudly
+when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import (POINTER, c_float, c_int32, c_size_t, c_void_p)
+
+import numpy as np
+
+from .build import LIB_PATH
+
+LAMINAR_OK = 0
+LAMINAR_ERR_INVALID_ARG = 1
+LAMINAR_ERR_UNSUPPORTED = 2
+LAMINAR_ERR_WORKSPACE = 3
+LAMINAR_ERR_HIP = 4
+
+LAMINAR_KV_BF16 = 0
+LAMINAR_KV_FP8_E4M3FN = 1
+
+
+class LaminarAttnDesc(ctypes.Structure):
+    _fields_ = [
+        ("batch", c_int32),
+        ("num_q_heads", c_int32),
+        ("num_kv_heads", c_int32),
+        ("head_dim", c_int32),
+        ("page_size", c_int32),
+        ("num_pages", c_int32),
+        ("max_blocks_per_seq", c_int32),
+        ("kv_dtype", c_int32),
+        ("softmax_scale", c_float),
+        ("k_scale", c_void_p),
+        ("v_scale", c_void_p),
+        ("pages_per_item", c_int32),
+        ("waves_per_item", c_int32),
+    ]
+
+
+class LaminarError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = int(status)
+        super().__init__(f"{where}: {laminar_status_string(status)} "
+                         f"(status {status})")
+
+
+_LIB = None
+
+# name -> (restype, argtypes)
+_SIGNATURES = {
+    "laminar_plan_create": (c_int32, [POINTER(LaminarAttnDesc), POINTER(c_int32),
+                                      c_int32, POINTER(c_void_p)]),
+    "laminar_plan_workspace_bytes": (c_size_t, [c_void_p]),
+    "laminar_plan_bind_workspace": (c_int32, [c_void_p, c_void_p, c_size_t,
+                                              c_void_p]),
+    "laminar_decode_attn": (c_int32, [c_void_p] + [c_void_p] * 7 + [c_void_p]),
+    "laminar_decode_attn_partial": (c_int32, [c_void_p] + [c_void_p] * 7
+                                    + [c_void_p]),
+    "laminar_decode_attn_merge": (c_int32, [c_void_p, c_void_p, c_void_p,
+                                            c_void_p]),
+    "laminar_plan_num_items": (c_int32, [c_void_p]),
+    "laminar_plan_num_merges": (c_int32, [c_void_p]),
+    "laminar_plan_pages_per_item": (c_int32, [c_void_p]),
+    "laminar_plan_waves_per_item": (c_int32, [c_void_p]),
+    "laminar_plan_items_copy": (c_int32, [c_void_p, POINTER(c_int32), c_int32]),
+    "laminar_plan_merges_copy": (c_int32, [c_void_p, POINTER(c_int32), c_int32]),
+    "laminar_plan_destroy": (None, [c_void_p]),
+    "laminar_status_string": (ctypes.c_char_p, [c_int32]),
+    "laminar_hbm_read_sink_floats": (c_int32, []),
+    "laminar_hbm_read": (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p]),
+    "laminar_hbm_copy": (c_int32, [c_void_p, c_void_p, c_size_t, c_void_p]),
+}
+
+
+def library_path() -> str:
+    return os.environ.get("LAMINAR_LIB", LIB_PATH)
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library; raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise RuntimeError(
+                f"HIP library {path} is missing: build it with "
+                "`python -m paper_2510_12633_amd.build` (no CPU fallback)")
+        handle = ctypes.CDLL(path)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = handle
+    return _LIB
+
+
+def _ptr(x):
+    """Device or host address of a tensor / integer / None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    raise TypeError(f"cannot take the address of {type(x).__name__}")
+
+
+def _check(status: int, where: str):
+    if status != LAMINAR_OK:
+        raise LaminarError(status, where)
+
+
+def laminar_status_string(status: int) -> str:
+    return lib().laminar_status_string(int(status)).decode()
+
+
+def laminar_plan_create(desc: LaminarAttnDesc, seq_lens_host, num_cus: int):
+    lens = np.ascontiguousarray(seq_lens_host, dtype=np.int32)
+    out = c_void_p()
+    st = lib().laminar_plan_create(
+        ctypes.byref(desc), lens.ctypes.data_as(POINTER(c_int32)),
+        int(num_cus), ctypes.byref(out))
+    _check(st, "laminar_plan_create")
+    return out.value
+
+
+def laminar_plan_workspace_bytes(plan) -> int:
+    return int(lib().laminar_plan_workspace_bytes(plan))
+
+
+def laminar_plan_bind_workspace(plan, workspace, nbytes: int, stream):
+    _check(lib().laminar_plan_bind_workspace(plan, _ptr(workspace), int(nbytes),
+                                             _ptr(stream)),
+           "laminar_plan_bind_workspace")
+
+
+def laminar_decode_attn(plan, q, k_pages, v_pages, block_table, seq_lens, out,
+                        lse, stream):
+    _check(lib().laminar_decode_attn(
+        plan, _ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table),
+        _ptr(seq_lens), _ptr(out), _ptr(lse), _ptr(stream)),
+        "laminar_decode_attn")
+
+
+def laminar_decode_attn_partial(plan, q, k_pages, v_pages, block_table,
+                                seq_lens, out, lse, stream):
+    _check(lib().laminar_decode_attn_partial(
+        plan, _ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table),
+        _ptr(seq_lens), _ptr(out), _ptr(lse), _ptr(stream)),
+        "laminar_decode_attn_partial")
+
+
+def laminar_decode_attn_merge(plan, out, lse, stream):
+    _check(lib().laminar_decode_attn_merge(plan, _ptr(out), _ptr(lse),
+                                           _ptr(stream)),
+           "laminar_decode_attn_merge")
+
+
+def laminar_plan_num_items(plan) -> int:
+    return int(lib().laminar_plan_num_items(plan))
+
+
+def laminar_plan_num_merges(plan) -> int:
+    return int(lib().laminar_plan_num_merges(plan))
+
+
+def laminar_plan_pages_per_item(plan) -> int:
+    return int(lib().laminar_plan_pages_per_item(plan))
+
+
+def laminar_plan_waves_per_item(plan) -> int:
+    return int(lib().laminar_plan_waves_per_item(plan))
+
+
+def laminar_plan_items_copy(plan) -> np.ndarray:
+    n = laminar_plan_num_items(plan)
+    buf = np.zeros((max(n, 0), 4), dtype=np.int32)
+    got = lib().laminar_plan_items_copy(
+        plan, buf.ctypes.data_as(POINTER(c_int32)), n)
+    assert got == n
+    return buf
+
+
+def laminar_plan_merges_copy(plan) -> np.ndarray:
+    n = laminar_plan_num_merges(plan)
+    buf = np.zeros((max(n, 0), 4), dtype=np.int32)
+    got = lib().laminar_plan_merges_copy(
+        plan, buf.ctypes.data_as(POINTER(c_int32)), n)
+    assert got == n
+    return buf
+
+
+def laminar_plan_destroy(plan):
+    lib().laminar_plan_destroy(plan)
+
+
+def laminar_hbm_read_sink_floats() -> int:
+    return int(lib().laminar_hbm_read_sink_floats())
+
+
+def laminar_hbm_read(src, nbytes: int, sink, stream):
+    _check(lib().laminar_hbm_read(_ptr(src), int(nbytes), _ptr(sink),
+                                  _ptr(stream)), "laminar_hbm_read")
+
+
+def laminar_hbm_copy(dst, src, nbytes: int, stream):
+    _check(lib().laminar_hbm_copy(_ptr(dst), _ptr(src), int(nbytes),
+                                  _ptr(stream)), "laminar_hbm_copy")

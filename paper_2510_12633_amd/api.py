@@ -1,0 +1,132 @@
+"""Owner object for one decode step's plan and workspace.
+
+Holds the plan handle and a torch-allocated device workspace and forwards
+calls to the C ABI. Argument marshalling and resource ownership only.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import _native as N
+
+KV_DTYPES = {"bf16": N.LAMINAR_KV_BF16, "fp8_e4m3fn": N.LAMINAR_KV_FP8_E4M3FN}
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def num_cus(device=None) -> int:
+    return torch.cuda.get_device_properties(
+        device if device is not None else torch.cuda.current_device()
+    ).multi_processor_count
+
+
+class PagedDecodeAttention:
+    """Plan + bound workspace for a batch with fixed trajectory lengths.
+
+    ``seq_lens_host`` are the lengths the next calls will see. The plan is
+    reusable by every layer of the decode step.
+    """
+
+    def __init__(self, *, batch: int, num_q_heads: int, num_kv_heads: int,
+                 head_dim: int, num_pages: int, max_blocks_per_seq: int,
+                 seq_lens_host, softmax_scale: float, kv_dtype: str = "bf16",
+                 k_scale: Optional[torch.Tensor] = None,
+                 v_scale: Optional[torch.Tensor] = None,
+                 pages_per_item: int = 0, waves_per_item: int = 0,
+                 cus: Optional[int] = None, device="cuda", stream=None):
+        self.desc = N.LaminarAttnDesc(
+            batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
+            head_dim=head_dim, page_size=16, num_pages=num_pages,
+            max_blocks_per_seq=max_blocks_per_seq,
+            kv_dtype=KV_DTYPES[kv_dtype], softmax_scale=softmax_scale,
+            k_scale=None if k_scale is None else k_scale.data_ptr(),
+            v_scale=None if v_scale is None else v_scale.data_ptr(),
+            pages_per_item=pages_per_item, waves_per_item=waves_per_item)
+        self.device = torch.device(device)
+        self._scales = (k_scale, v_scale)        # keep alive
+        if cus is None:
+            cus = num_cus(self.device) if self.device.type == "cuda" else 256
+        self.plan = N.laminar_plan_create(self.desc,
+                                          np.asarray(seq_lens_host), cus)
+        self.workspace_bytes = N.laminar_plan_workspace_bytes(self.plan)
+        self.workspace = None
+        if self.device.type == "cuda":
+            self.bind(stream)
+
+    def bind(self, stream=None):
+        nbytes = max(self.workspace_bytes, 256)
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8,
+                                     device=self.device)
+        self._bind_stream = stream
+        N.laminar_plan_bind_workspace(self.plan, self.workspace,
+                                      self.workspace_bytes,
+                                      _stream_handle(stream))
+
+    def outputs(self):
+        d = self.desc
+        out = torch.empty((d.batch, d.num_q_heads, d.head_dim),
+                          dtype=torch.float32, device=self.device)
+        lse = torch.empty((d.batch, d.num_q_heads), dtype=torch.float32,
+                          device=self.device)
+        return out, lse
+
+    def __call__(self, q, k_pages, v_pages, block_table, seq_lens, out=None,
+                 lse=None, stream=None):
+        if out is None or lse is None:
+            out, lse = self.outputs()
+        N.laminar_decode_attn(self.plan, q, k_pages, v_pages, block_table,
+                              seq_lens, out, lse, _stream_handle(stream))
+        return out, lse
+
+    def partial(self, q, k_pages, v_pages, block_table, seq_lens, out, lse,
+                stream=None):
+        N.laminar_decode_attn_partial(self.plan, q, k_pages, v_pages,
+                                      block_table, seq_lens, out, lse,
+                                      _stream_handle(stream))
+
+    def merge(self, out, lse, stream=None):
+        N.laminar_decode_attn_merge(self.plan, out, lse, _stream_handle(stream))
+
+    @property
+    def num_items(self) -> int:
+        return N.laminar_plan_num_items(self.plan)
+
+    @property
+    def num_merges(self) -> int:
+        return N.laminar_plan_num_merges(self.plan)
+
+    @property
+    def pages_per_item(self) -> int:
+        return N.laminar_plan_pages_per_item(self.plan)
+
+    @property
+    def waves_per_item(self) -> int:
+        return N.laminar_plan_waves_per_item(self.plan)
+
+    def items(self) -> np.ndarray:
+        return N.laminar_plan_items_copy(self.plan)
+
+    def merges(self) -> np.ndarray:
+        return N.laminar_plan_merges_copy(self.plan)
+
+    def close(self):
+        """Destroy the plan once the stream has passed the table upload."""
+        if getattr(self, "plan", None):
+            if self.workspace is not None:
+                torch.cuda.current_stream(self.device).synchronize() \
+                    if self._bind_stream is None else self._bind_stream.synchronize()
+            N.laminar_plan_destroy(self.plan)
+            self.plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,721 @@
+// Paged grouped-query decode attention for MI355X (gfx950, CDNA4).
+//
+// Rollout decoding is memory-bound (§2.4 of the paper) and its KV-cache reads
+// dominate each decode step (§5.2), so the kernels below are organised around
+// streaming 16-token KV pages from HBM once:
+//
+//  * decode_partial: one workgroup per work item (trajectory, kv-head, page
+//    range) from the host plan. Each wavefront takes pairs of pages in turn
+//    and keeps the next pair's loads in flight while it computes the current
+//    one. Per pair it forms the scores of all g query heads of the GQA group
+//    with bf16 matrix-core products (v_mfma_f32_16x16x32_bf16: 16 tokens x
+//    16 head slots, head_dim as the reduction), updates an online softmax in
+//    fp32, and accumulates P*V on the matrix cores with P split into a bf16
+//    high part and a bf16 low part, so P keeps about 16 bits of precision.
+//    The page layouts put every operand fragment in 16-byte runs, so no LDS
+//    staging or lane shuffles are needed; LDS is only used to combine the
+//    wavefronts of one item.
+//  * decode_merge: log-sum-exp merge of the partial (out, lse) records of
+//    trajectories whose pages were split over several items.
+//  * hbm_read / hbm_copy: bandwidth calibration.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "laminar_decode_attn.h"
+#include "plan_internal.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+struct DecodeArgs {
+  const uint16_t* q;
+  const uint8_t* k_pages;
+  const uint8_t* v_pages;
+  const float* k_scale;
+  const float* v_scale;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  float* out;
+  float* lse;
+  float* o_part;
+  float* lse_part;
+  const int4* items;
+  const int4* merges;
+  int32_t hq, hkv, group, max_blocks, num_pages;
+  float scale_log2;  // softmax_scale * log2(e)
+  float scale;       // softmax_scale
+};
+
+// Fragment geometry for one (page, kv-head) tile of 16 tokens x D dims.
+template <int D, bool FP8>
+struct Geo {
+  static constexpr int KK = D / 32;             // QK^T matrix-core steps
+  static constexpr int NT = D / 16;             // 16-dim tiles of P*V
+  static constexpr int EB = FP8 ? 1 : 2;        // bytes per element
+  static constexpr int TILE = 16 * D * EB;      // bytes per tile
+  static constexpr int KL = 8 * KK * EB / 16;   // 16-byte K loads per lane
+  static constexpr int VL = 4 * NT * EB / 16;   // 16-byte V loads per lane
+};
+
+template <int D, bool FP8>
+struct PairRegs {
+  using G = Geo<D, FP8>;
+  u32x4 ka[G::KL], kb[G::KL];
+  u32x4 va[G::VL], vb[G::VL];
+  int nva, nvb;          // valid tokens in page A / B (0..16)
+  float ksa, ksb, vsa, vsb;
+};
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  bf16x2 v;
+  v[0] = (__bf16)lo;     // round to nearest even (v_cvt_pk_bf16_f32)
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Two OCP e4m3fn codes (bytes 0,1 or, with HIGH, 2,3 of w) to a packed bf16
+// pair; exact.
+template <bool HIGH>
+__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w) {
+  return __builtin_bit_cast(
+      uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HIGH));
+}
+
+__device__ __forceinline__ float bf16_lo_f(uint32_t w) {
+  return __uint_as_float(w << 16);
+}
+__device__ __forceinline__ float bf16_hi_f(uint32_t w) {
+  return __uint_as_float(w & 0xFFFF0000u);
+}
+
+__device__ __forceinline__ u32x4 u4(uint32_t a, uint32_t b, uint32_t c,
+                                    uint32_t d) {
+  u32x4 r;
+  r[0] = a; r[1] = b; r[2] = c; r[3] = d;
+  return r;
+}
+
+__device__ __forceinline__ s16x4 s4(uint32_t a, uint32_t b) {
+  u32x2 r;
+  r[0] = a; r[1] = b;
+  return __builtin_bit_cast(s16x4, r);
+}
+
+__device__ __forceinline__ uint32_t word(const u32x4* v, int k) {
+  return v[k >> 2][k & 3];
+}
+
+// A-operand fragment of K for matrix-core step kk: lane (token t = lane%16,
+// group gq = lane/16) holds dims (gq*KK + kk)*8 .. +7 of token t.
+template <int D, bool FP8>
+__device__ __forceinline__ bf16x8 k_frag(const u32x4 (&k)[Geo<D, FP8>::KL],
+                                         int kk) {
+  if constexpr (!FP8) {
+    return __builtin_bit_cast(bf16x8, k[kk]);
+  } else {
+    const u32x4 src = k[kk >> 1];
+    const uint32_t w0 = src[(kk & 1) * 2], w1 = src[(kk & 1) * 2 + 1];
+    return __builtin_bit_cast(
+        bf16x8, u4(fp8x2_to_bf16x2<false>(w0), fp8x2_to_bf16x2<true>(w0),
+                   fp8x2_to_bf16x2<false>(w1), fp8x2_to_bf16x2<true>(w1)));
+  }
+}
+
+// A-operand fragment of V^T for dim tile n: lane (row m = lane%16, group gq)
+// holds dim m*NT + n of tokens 4gq..4gq+3 of page A (items 0-3) and of
+// page B (items 4-7).
+template <int D, bool FP8>
+__device__ __forceinline__ bf16x8 v_frag(const u32x4 (&va)[Geo<D, FP8>::VL],
+                                         const u32x4 (&vb)[Geo<D, FP8>::VL],
+                                         int n) {
+  if constexpr (!FP8) {
+    return __builtin_bit_cast(
+        bf16x8, u4(word(va, 2 * n), word(va, 2 * n + 1), word(vb, 2 * n),
+                   word(vb, 2 * n + 1)));
+  } else {
+    const uint32_t wa = word(va, n), wb = word(vb, n);
+    return __builtin_bit_cast(
+        bf16x8, u4(fp8x2_to_bf16x2<false>(wa), fp8x2_to_bf16x2<true>(wa),
+                   fp8x2_to_bf16x2<false>(wb), fp8x2_to_bf16x2<true>(wb)));
+  }
+}
+
+// Zero the V elements of tokens at or beyond `nv` held by this lane
+// (tokens 4gq..4gq+3 of the page), so that P = 0 never meets NaN poison.
+template <int D, bool FP8>
+__device__ __forceinline__ void zero_tail_v(u32x4* v, int nv, int gq) {
+  const int t0 = 4 * gq;
+  if constexpr (!FP8) {
+    const uint32_t m0 = (t0 + 0 < nv ? 0x0000FFFFu : 0u) |
+                        (t0 + 1 < nv ? 0xFFFF0000u : 0u);
+    const uint32_t m1 = (t0 + 2 < nv ? 0x0000FFFFu : 0u) |
+                        (t0 + 3 < nv ? 0xFFFF0000u : 0u);
+#pragma unroll
+    for (int j = 0; j < Geo<D, FP8>::VL; ++j) {
+      v[j][0] &= m0; v[j][1] &= m1; v[j][2] &= m0; v[j][3] &= m1;
+    }
+  } else {
+    const uint32_t m = (t0 + 0 < nv ? 0x000000FFu : 0u) |
+                       (t0 + 1 < nv ? 0x0000FF00u : 0u) |
+                       (t0 + 2 < nv ? 0x00FF0000u : 0u) |
+                       (t0 + 3 < nv ? 0xFF000000u : 0u);
+#pragma unroll
+    for (int j = 0; j < Geo<D, FP8>::VL; ++j) {
+      v[j][0] &= m; v[j][1] &= m; v[j][2] &= m; v[j][3] &= m;
+    }
+  }
+}
+
+template <int D, bool FP8, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
+__attribute__((amdgpu_waves_per_eu(2)))
+decode_partial(const DecodeArgs a) {
+  using G = Geo<D, FP8>;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, gq = lane >> 4;
+
+  const int4 it = a.items[blockIdx.x];
+  const int unit = it.x;
+  const int b = unit / a.hkv;
+  const int kvh = unit - b * a.hkv;
+  const int len = a.seq_lens[b];
+  const int p0 = it.y;
+  const int p1 = min(it.z, (len + 15) >> 4);
+  const int npages = max(p1 - p0, 0);
+  const int npairs = (npages + 1) >> 1;
+
+  // Query fragment (B operand of QK^T): lane holds head r16 of the group,
+  // dims (gq*KK + kk)*8 .. +7 for each step kk. Heads beyond the group are 0.
+  const bool head_ok = r16 < a.group;
+  const int h = kvh * a.group + r16;
+  bf16x8 qf[G::KK];
+  {
+    const u32x4* qp = reinterpret_cast<const u32x4*>(
+        a.q + (size_t(b) * a.hq + (head_ok ? h : 0)) * D) + gq * G::KK;
+#pragma unroll
+    for (int kk = 0; kk < G::KK; ++kk) {
+      const u32x4 v = head_ok ? qp[kk] : u4(0, 0, 0, 0);
+      qf[kk] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  f32x4 acc[G::NT];
+#pragma unroll
+  for (int n = 0; n < G::NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;   // running max of raw scores, per head r16
+  float l_run = 0.f;         // this lane's share of the softmax denominator
+
+  const size_t page_stride = size_t(a.hkv) * G::TILE;
+  const uint8_t* kbase = a.k_pages + size_t(kvh) * G::TILE;
+  const uint8_t* vbase = a.v_pages + size_t(kvh) * G::TILE;
+  const int32_t* bt = a.block_table + size_t(b) * a.max_blocks + p0;
+  const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
+  const int voff = (gq * D + r16 * G::NT) * G::EB / 4;       // u32x4 units
+
+  // Block-table entries of this item, 64 pages per window, one per lane.
+  int win = -1;
+  int btv = -1;
+
+  auto load_pair = [&](PairRegs<D, FP8>& pr, int jp) {
+    const int ja = 2 * jp;                       // page index within item
+    const int w = ja >> 6;
+    if (w != win) {
+      const int j = w * 64 + lane;
+      btv = j < npages ? bt[j] : -1;
+      win = w;
+    }
+    const bool has_b = ja + 1 < npages;
+    int ppa = __builtin_amdgcn_readlane(btv, ja & 63);
+    int ppb = has_b ? __builtin_amdgcn_readlane(btv, (ja + 1) & 63) : ppa;
+    const int base_tok = (p0 + ja) * 16;
+    int nva = min(16, len - base_tok);
+    int nvb = has_b ? min(16, len - base_tok - 16) : 0;
+    if (ppa < 0 || ppa >= a.num_pages) { ppa = 0; nva = 0; }
+    if (ppb < 0 || ppb >= a.num_pages) { ppb = 0; nvb = 0; }
+    pr.nva = nva;
+    pr.nvb = nvb;
+    const u32x4* ka = reinterpret_cast<const u32x4*>(kbase + size_t(ppa) * page_stride);
+    const u32x4* kb = reinterpret_cast<const u32x4*>(kbase + size_t(ppb) * page_stride);
+    const u32x4* va = reinterpret_cast<const u32x4*>(vbase + size_t(ppa) * page_stride);
+    const u32x4* vb = reinterpret_cast<const u32x4*>(vbase + size_t(ppb) * page_stride);
+#pragma unroll
+    for (int j = 0; j < G::KL; ++j) pr.ka[j] = ka[koff + j * 16];
+#pragma unroll
+    for (int j = 0; j < G::KL; ++j) pr.kb[j] = kb[koff + j * 16];
+#pragma unroll
+    for (int j = 0; j < G::VL; ++j) pr.va[j] = va[voff + j];
+#pragma unroll
+    for (int j = 0; j < G::VL; ++j) pr.vb[j] = vb[voff + j];
+    if constexpr (FP8) {
+      pr.ksa = a.k_scale[size_t(ppa) * a.hkv + kvh];
+      pr.ksb = a.k_scale[size_t(ppb) * a.hkv + kvh];
+      pr.vsa = a.v_scale[size_t(ppa) * a.hkv + kvh];
+      pr.vsb = a.v_scale[size_t(ppb) * a.hkv + kvh];
+    }
+  };
+
+  auto compute_pair = [&](PairRegs<D, FP8>& pr) {
+    // Scores S^T[token][head] of both pages: lane holds head r16, tokens
+    // 4gq..4gq+3 of page A (sa) and of page B (sb).
+    f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < G::KK; ++kk) {
+      sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_frag<D, FP8>(pr.ka, kk),
+                                                   qf[kk], sa, 0, 0, 0);
+      sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_frag<D, FP8>(pr.kb, kk),
+                                                   qf[kk], sb, 0, 0, 0);
+    }
+    if constexpr (FP8) {
+      sa *= pr.ksa;
+      sb *= pr.ksb;
+    }
+    if (pr.nva < 16 || pr.nvb < 16) {          // uniform: only at the tail
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        sa[r] = (4 * gq + r < pr.nva) ? sa[r] : -INFINITY;
+        sb[r] = (4 * gq + r < pr.nvb) ? sb[r] : -INFINITY;
+      }
+      zero_tail_v<D, FP8>(pr.va, pr.nva, gq);
+      zero_tail_v<D, FP8>(pr.vb, pr.nvb, gq);
+    }
+    float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])),
+                     fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float mc = (m_new == -INFINITY) ? 0.f : m_new * a.scale_log2;
+    const float alpha = __builtin_amdgcn_exp2f(m_run * a.scale_log2 - mc);
+    m_run = m_new;
+    float pa[4], pb[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      pa[r] = __builtin_amdgcn_exp2f(fmaf(sa[r], a.scale_log2, -mc));
+      pb[r] = __builtin_amdgcn_exp2f(fmaf(sb[r], a.scale_log2, -mc));
+    }
+    l_run = fmaf(l_run, alpha, ((pa[0] + pa[1]) + (pa[2] + pa[3])) +
+                                   ((pb[0] + pb[1]) + (pb[2] + pb[3])));
+#pragma unroll
+    for (int n = 0; n < G::NT; ++n) acc[n] *= alpha;
+    if constexpr (FP8) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pa[r] *= pr.vsa;
+        pb[r] *= pr.vsb;
+      }
+    }
+    // P^T as B operand: lane holds head r16, slots 8gq+e = token 4gq+e of
+    // page A (e < 4) and of page B (e >= 4); P = hi + lo in bf16.
+    const uint32_t h0 = pack_bf16(pa[0], pa[1]), h1 = pack_bf16(pa[2], pa[3]);
+    const uint32_t h2 = pack_bf16(pb[0], pb[1]), h3 = pack_bf16(pb[2], pb[3]);
+    const uint32_t l0 = pack_bf16(pa[0] - bf16_lo_f(h0), pa[1] - bf16_hi_f(h0));
+    const uint32_t l1 = pack_bf16(pa[2] - bf16_lo_f(h1), pa[3] - bf16_hi_f(h1));
+    const uint32_t l2 = pack_bf16(pb[0] - bf16_lo_f(h2), pb[1] - bf16_hi_f(h2));
+    const uint32_t l3 = pack_bf16(pb[2] - bf16_lo_f(h3), pb[3] - bf16_hi_f(h3));
+    if constexpr (!FP8) {
+      // bf16 V: one 16x16x16 product per page, its A operand (dim row
+      // r16*NT + n, tokens 4gq..4gq+3) is two of the loaded registers.
+      const s16x4 pha = s4(h0, h1), pla = s4(l0, l1);
+      const s16x4 phb = s4(h2, h3), plb = s4(l2, l3);
+#pragma unroll
+      for (int n = 0; n < G::NT; ++n) {
+        const s16x4 vta = s4(word(pr.va, 2 * n), word(pr.va, 2 * n + 1));
+        const s16x4 vtb = s4(word(pr.vb, 2 * n), word(pr.vb, 2 * n + 1));
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vta, pha, acc[n], 0, 0, 0);
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vta, pla, acc[n], 0, 0, 0);
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vtb, phb, acc[n], 0, 0, 0);
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vtb, plb, acc[n], 0, 0, 0);
+      }
+    } else {
+      // fp8 V: the converted registers form one 16x16x32 operand per tile,
+      // tokens of page A in items 0-3 and of page B in items 4-7.
+      const bf16x8 phi = __builtin_bit_cast(bf16x8, u4(h0, h1, h2, h3));
+      const bf16x8 plo = __builtin_bit_cast(bf16x8, u4(l0, l1, l2, l3));
+#pragma unroll
+      for (int n = 0; n < G::NT; ++n) {
+        const bf16x8 vt = v_frag<D, FP8>(pr.va, pr.vb, n);
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, phi, acc[n], 0, 0, 0);
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, plo, acc[n], 0, 0, 0);
+      }
+    }
+  };
+
+  // Pairs wave, wave + WAVES, ...; the next pair's loads are issued before
+  // the current pair is computed.
+  PairRegs<D, FP8> buf0, buf1;
+  int jp = wave;
+  if (jp < npairs) load_pair(buf0, jp);
+  while (jp < npairs) {
+    int jn = jp + WAVES;
+    if (jn < npairs) load_pair(buf1, jn);
+    compute_pair(buf0);
+    jp = jn;
+    if (jp >= npairs) break;
+    jn = jp + WAVES;
+    if (jn < npairs) load_pair(buf0, jn);
+    compute_pair(buf1);
+    jp = jn;
+  }
+
+  // Full softmax denominator of head r16 over this wave's pages.
+  l_run += __shfl_xor(l_run, 16);
+  l_run += __shfl_xor(l_run, 32);
+
+  if constexpr (WAVES > 1) {
+    __shared__ float sm_m[WAVES][16];
+    __shared__ float sm_l[WAVES][16];
+    __shared__ float sm_acc[WAVES - 1][G::NT * 4][64];
+    if (wave > 0) {
+      if (gq == 0) {
+        sm_m[wave][r16] = m_run;
+        sm_l[wave][r16] = l_run;
+      }
+#pragma unroll
+      for (int n = 0; n < G::NT; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sm_acc[wave - 1][n * 4 + r][lane] = acc[n][r];
+    }
+    __syncthreads();
+    if (wave > 0) return;
+    float m_all = m_run;
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) m_all = fmaxf(m_all, sm_m[w][r16]);
+    const float mc = (m_all == -INFINITY) ? 0.f : m_all * a.scale_log2;
+    const float f0 = __builtin_amdgcn_exp2f(m_run * a.scale_log2 - mc);
+    l_run *= f0;
+#pragma unroll
+    for (int n = 0; n < G::NT; ++n) acc[n] *= f0;
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) {
+      const float fw = __builtin_amdgcn_exp2f(sm_m[w][r16] * a.scale_log2 - mc);
+      l_run = fmaf(sm_l[w][r16], fw, l_run);
+#pragma unroll
+      for (int n = 0; n < G::NT; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          acc[n][r] = fmaf(sm_acc[w - 1][n * 4 + r][lane], fw, acc[n][r]);
+    }
+    m_run = m_all;
+  }
+
+  if (!head_ok) return;
+  const bool empty = !(l_run > 0.f);
+  const float inv = empty ? 0.f : 1.0f / l_run;
+  const float lse_v = empty ? -INFINITY
+                            : m_run * a.scale + __builtin_amdgcn_logf(l_run) * kLn2;
+  float* dst;
+  float* lse_dst;
+  if (it.w < 0) {
+    dst = a.out + (size_t(b) * a.hq + h) * D;
+    lse_dst = a.lse + size_t(b) * a.hq + h;
+  } else {
+    dst = a.o_part + (size_t(it.w) * a.group + r16) * D;
+    lse_dst = a.lse_part + size_t(it.w) * a.group + r16;
+  }
+  // Lane holds dims (4gq + r)*NT + n: NT contiguous floats for each r.
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float4* row = reinterpret_cast<float4*>(dst + (4 * gq + r) * G::NT);
+#pragma unroll
+    for (int n4 = 0; n4 < G::NT / 4; ++n4)
+      row[n4] = make_float4(acc[4 * n4][r] * inv, acc[4 * n4 + 1][r] * inv,
+                            acc[4 * n4 + 2][r] * inv, acc[4 * n4 + 3][r] * inv);
+  }
+  if (gq == 0) *lse_dst = lse_v;
+}
+
+// Block-wide reductions for 256 threads.
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// One workgroup per (split trajectory unit, head of the group).
+template <int D>
+__global__ void __launch_bounds__(256) decode_merge(const DecodeArgs a) {
+  constexpr int C = D / 4;          // threads per partial row (float4 each)
+  constexpr int SPAR = 256 / C;     // partial rows reduced in parallel
+  __shared__ float red[4];
+  __shared__ float4 part[SPAR][C];
+  const int tid = threadIdx.x;
+  const int4 mg = a.merges[blockIdx.x];
+  const int i = blockIdx.y;
+  const int unit = mg.x, slot0 = mg.y, n = mg.z;
+  const int b = unit / a.hkv;
+  const int kvh = unit - b * a.hkv;
+  const int h = kvh * a.group + i;
+  const float* lp = a.lse_part + size_t(slot0) * a.group + i;
+
+  float mx = -INFINITY;
+  for (int s = tid; s < n; s += 256) mx = fmaxf(mx, lp[size_t(s) * a.group]);
+  mx = wave_max(mx);
+  if ((tid & 63) == 0) red[tid >> 6] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  float sum = 0.f;
+  if (mx != -INFINITY)
+    for (int s = tid; s < n; s += 256) sum += expf(lp[size_t(s) * a.group] - mx);
+  sum = wave_sum(sum);
+  if ((tid & 63) == 0) red[tid >> 6] = sum;
+  __syncthreads();
+  sum = (red[0] + red[1]) + (red[2] + red[3]);
+  const float L = (mx == -INFINITY) ? -INFINITY : mx + logf(sum);
+
+  const int c = tid % C, s0 = tid / C;
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (L != -INFINITY) {
+    for (int s = s0; s < n; s += SPAR) {
+      const float w = expf(lp[size_t(s) * a.group] - L);
+      const float4 v = reinterpret_cast<const float4*>(
+          a.o_part + (size_t(slot0 + s) * a.group + i) * D)[c];
+      o.x = fmaf(w, v.x, o.x); o.y = fmaf(w, v.y, o.y);
+      o.z = fmaf(w, v.z, o.z); o.w = fmaf(w, v.w, o.w);
+    }
+  }
+  part[s0][c] = o;
+  __syncthreads();
+  if (s0 == 0) {
+    for (int s = 1; s < SPAR; ++s) {
+      const float4 v = part[s][c];
+      o.x += v.x; o.y += v.y; o.z += v.z; o.w += v.w;
+    }
+    reinterpret_cast<float4*>(a.out + (size_t(b) * a.hq + h) * D)[c] = o;
+    if (c == 0) a.lse[size_t(b) * a.hq + h] = L;
+  }
+}
+
+constexpr int kReadBlocks = 2048;
+
+__global__ void __launch_bounds__(256)
+hbm_read_kernel(const u32x4* __restrict__ src, size_t n16, float* sink) {
+  float s = 0.f;
+  const size_t stride = size_t(gridDim.x) * blockDim.x;
+  size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const u32x4 v0 = src[i], v1 = src[i + stride], v2 = src[i + 2 * stride],
+                v3 = src[i + 3 * stride];
+    s += (__uint_as_float(v0[0] ^ v1[1]) + __uint_as_float(v2[2] ^ v3[3]));
+  }
+  for (; i < n16; i += stride) s += __uint_as_float(src[i][0]);
+  s = wave_sum(s);
+  __shared__ float red[4];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ void __launch_bounds__(256)
+hbm_copy_kernel(u32x4* __restrict__ dst, const u32x4* __restrict__ src,
+                size_t n16) {
+  const size_t stride = size_t(gridDim.x) * blockDim.x;
+  for (size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n16;
+       i += stride)
+    dst[i] = src[i];
+}
+
+template <int D, bool FP8>
+hipError_t launch_partial(const laminar_plan* p, const DecodeArgs& a,
+                          hipStream_t stream) {
+  const dim3 grid(p->num_items);
+  switch (p->waves) {
+    case 1:
+      hipLaunchKernelGGL((decode_partial<D, FP8, 1>), grid, dim3(64), 0, stream, a);
+      break;
+    case 2:
+      hipLaunchKernelGGL((decode_partial<D, FP8, 2>), grid, dim3(128), 0, stream, a);
+      break;
+    default:
+      hipLaunchKernelGGL((decode_partial<D, FP8, 4>), grid, dim3(256), 0, stream, a);
+      break;
+  }
+  return hipGetLastError();
+}
+
+DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
+                     const void* v_pages, const int32_t* block_table,
+                     const int32_t* seq_lens, float* out, float* lse) {
+  DecodeArgs a;
+  const laminar_attn_desc& d = p->desc;
+  char* ws = static_cast<char*>(p->ws);
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pages = static_cast<const uint8_t*>(k_pages);
+  a.v_pages = static_cast<const uint8_t*>(v_pages);
+  a.k_scale = d.k_scale;
+  a.v_scale = d.v_scale;
+  a.block_table = block_table;
+  a.seq_lens = seq_lens;
+  a.out = out;
+  a.lse = lse;
+  a.items = reinterpret_cast<const int4*>(ws + p->off_items);
+  a.merges = reinterpret_cast<const int4*>(ws + p->off_merges);
+  a.lse_part = reinterpret_cast<float*>(ws + p->off_lse);
+  a.o_part = reinterpret_cast<float*>(ws + p->off_o);
+  a.hq = d.num_q_heads;
+  a.hkv = d.num_kv_heads;
+  a.group = p->group;
+  a.max_blocks = d.max_blocks_per_seq;
+  a.num_pages = d.num_pages;
+  a.scale_log2 = d.softmax_scale * kLog2e;
+  a.scale = d.softmax_scale;
+  return a;
+}
+
+laminar_status check_bound(const laminar_plan* p) {
+  if (!p) return LAMINAR_ERR_INVALID_ARG;
+  if (p->ws_bytes > 0 && (!p->ws || p->ws_size < p->ws_bytes))
+    return LAMINAR_ERR_WORKSPACE;
+  return LAMINAR_OK;
+}
+
+laminar_status run_partial(const laminar_plan* p, const DecodeArgs& a,
+                           hipStream_t stream) {
+  if (p->num_items == 0) return LAMINAR_OK;
+  const bool fp8 = p->desc.kv_dtype == LAMINAR_KV_FP8_E4M3FN;
+  hipError_t e;
+  if (p->desc.head_dim == 128)
+    e = fp8 ? launch_partial<128, true>(p, a, stream)
+            : launch_partial<128, false>(p, a, stream);
+  else
+    e = fp8 ? launch_partial<64, true>(p, a, stream)
+            : launch_partial<64, false>(p, a, stream);
+  return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+}
+
+laminar_status run_merge(const laminar_plan* p, const DecodeArgs& a,
+                         hipStream_t stream) {
+  if (p->num_merges == 0) return LAMINAR_OK;
+  const dim3 grid(p->num_merges, p->group);
+  if (p->desc.head_dim == 128)
+    hipLaunchKernelGGL((decode_merge<128>), grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_merge<64>), grid, dim3(256), 0, stream, a);
+  return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+}
+
+bool inputs_ok(const laminar_plan* p, const void* q, const void* k_pages,
+               const void* v_pages, const int32_t* block_table,
+               const int32_t* seq_lens, const float* out, const float* lse) {
+  if (p->desc.batch == 0) return true;
+  return q && k_pages && v_pages && block_table && seq_lens && out && lse;
+}
+
+}  // namespace
+
+extern "C" {
+
+laminar_status laminar_plan_bind_workspace(laminar_plan* plan, void* workspace,
+                                           size_t bytes, hipStream_t stream) {
+  if (!plan) return LAMINAR_ERR_INVALID_ARG;
+  if (plan->ws_bytes == 0) {
+    plan->ws = workspace;
+    plan->ws_size = bytes;
+    return LAMINAR_OK;
+  }
+  if (!workspace || bytes < plan->ws_bytes ||
+      (reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
+    return LAMINAR_ERR_WORKSPACE;
+  plan->ws = workspace;
+  plan->ws_size = bytes;
+  const size_t table_bytes = plan->tables.size() * sizeof(int32_t);
+  if (table_bytes == 0) return LAMINAR_OK;
+  // Items then merges, at their section offsets.
+  char* ws = static_cast<char*>(workspace);
+  const size_t item_bytes = size_t(plan->num_items) * 16;
+  hipError_t e = hipSuccess;
+  if (item_bytes)
+    e = hipMemcpyAsync(ws + plan->off_items, plan->tables.data(), item_bytes,
+                       hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess && plan->num_merges)
+    e = hipMemcpyAsync(ws + plan->off_merges,
+                       plan->tables.data() + size_t(4) * plan->num_items,
+                       size_t(plan->num_merges) * 16, hipMemcpyHostToDevice,
+                       stream);
+  return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+}
+
+laminar_status laminar_decode_attn_partial(const laminar_plan* plan,
+                                           const void* q, const void* k_pages,
+                                           const void* v_pages,
+                                           const int32_t* block_table,
+                                           const int32_t* seq_lens, float* out,
+                                           float* lse, hipStream_t stream) {
+  laminar_status st = check_bound(plan);
+  if (st != LAMINAR_OK) return st;
+  if (!inputs_ok(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse))
+    return LAMINAR_ERR_INVALID_ARG;
+  const DecodeArgs a = make_args(plan, q, k_pages, v_pages, block_table,
+                                 seq_lens, out, lse);
+  return run_partial(plan, a, stream);
+}
+
+laminar_status laminar_decode_attn_merge(const laminar_plan* plan, float* out,
+                                         float* lse, hipStream_t stream) {
+  laminar_status st = check_bound(plan);
+  if (st != LAMINAR_OK) return st;
+  if (plan->desc.batch > 0 && (!out || !lse)) return LAMINAR_ERR_INVALID_ARG;
+  const DecodeArgs a = make_args(plan, nullptr, nullptr, nullptr, nullptr,
+                                 nullptr, out, lse);
+  return run_merge(plan, a, stream);
+}
+
+laminar_status laminar_decode_attn(const laminar_plan* plan, const void* q,
+                                   const void* k_pages, const void* v_pages,
+                                   const int32_t* block_table,
+                                   const int32_t* seq_lens, float* out,
+                                   float* lse, hipStream_t stream) {
+  laminar_status st = check_bound(plan);
+  if (st != LAMINAR_OK) return st;
+  if (!inputs_ok(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse))
+    return LAMINAR_ERR_INVALID_ARG;
+  const DecodeArgs a = make_args(plan, q, k_pages, v_pages, block_table,
+                                 seq_lens, out, lse);
+  st = run_partial(plan, a, stream);
+  if (st != LAMINAR_OK) return st;
+  return run_merge(plan, a, stream);
+}
+
+int32_t laminar_hbm_read_sink_floats(void) { return kReadBlocks; }
+
+laminar_status laminar_hbm_read(const void* src, size_t bytes, float* sink,
+                                hipStream_t stream) {
+  if (!src || !sink || (bytes & 15) ||
+      (reinterpret_cast<uintptr_t>(src) & 15))
+    return LAMINAR_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(hbm_read_kernel, dim3(kReadBlocks), dim3(256), 0, stream,
+                     static_cast<const u32x4*>(src), bytes / 16, sink);
+  return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+}
+
+laminar_status laminar_hbm_copy(void* dst, const void* src, size_t bytes,
+                                hipStream_t stream) {
+  if (!src || !dst || (bytes & 15) ||
+      (reinterpret_cast<uintptr_t>(src) & 15) ||
+      (reinterpret_cast<uintptr_t>(dst) & 15))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (bytes == 0) return LAMINAR_OK;
+  hipLaunchKernelGGL(hbm_copy_kernel, dim3(kReadBlocks), dim3(256), 0, stream,
+                     static_cast<u32x4*>(dst), static_cast<const u32x4*>(src),
+                     bytes / 16);
+  return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,37 @@
+// Internal definition of the host-side plan shared by the planner and the
+// HIP entry points. Not part of the public C ABI.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "laminar_decode_attn.h"
+
+struct laminar_plan {
+  laminar_attn_desc desc;
+  int32_t group = 0;           // query heads per kv-head
+  int32_t pages_per_item = 0;  // chosen split size
+  int32_t waves = 0;           // wavefronts per work item
+  int32_t num_items = 0;
+  int32_t num_merges = 0;
+  int32_t num_slots = 0;       // partial (out, lse) records
+  // Host image of the device tables: items (4 int32 each) then merges.
+  std::vector<int32_t> tables;
+  // Workspace layout (byte offsets, 256-byte aligned sections).
+  size_t off_items = 0, off_merges = 0, off_lse = 0, off_o = 0;
+  size_t ws_bytes = 0;
+  // Bound workspace (device memory owned by the caller).
+  void* ws = nullptr;
+  size_t ws_size = 0;
+};
+
+namespace laminar_detail {
+// Wavefronts resident per CU that the automatic split assumes for one item
+// of one wavefront (two per SIMD with ~200 VGPRs per lane).
+constexpr int kResidentWavesPerCU = 8;
+// Work items per resident slot the automatic split aims for, so that the
+// longest-first order leaves little tail imbalance.
+constexpr int kItemsPerSlot = 3;
+constexpr int kDefaultWaves = 4;
+}  // namespace laminar_detail

@@ -1,0 +1,249 @@
+"""GPU parity: the HIP library through its C ABI against the fp64 oracle.
+
+Bar: fp32 out and lse within max-abs 1e-3 of the oracle on every case.
+Identities that hold exactly on the GPU (page permutation, prefix aliasing,
+run-to-run) are checked bitwise.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import decode_attention_from_host
+from workloads import custom_config, get_config, host_arrays, make_workload
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+
+
+def _say(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+
+
+def run_gpu(wl, pages_per_item=0, waves_per_item=0, block_table=None,
+            k_pages=None, v_pages=None, two_phase=False):
+    from paper_2510_12633_amd.api import PagedDecodeAttention
+    c = wl.cfg
+    dev = wl.q.device
+    bt_np = wl.block_table if block_table is None else block_table
+    bt = torch.as_tensor(bt_np, device=dev)
+    lens = torch.as_tensor(wl.seq_lens, device=dev)
+    att = PagedDecodeAttention(
+        batch=wl.batch, num_q_heads=c.num_q_heads, num_kv_heads=c.num_kv_heads,
+        head_dim=c.head_dim, num_pages=(wl.num_pages if k_pages is None
+                                        else k_pages.shape[0]),
+        max_blocks_per_seq=bt_np.shape[1], seq_lens_host=wl.seq_lens,
+        softmax_scale=wl.softmax_scale, kv_dtype=c.kv_dtype,
+        k_scale=wl.k_scale, v_scale=wl.v_scale,
+        pages_per_item=pages_per_item, waves_per_item=waves_per_item)
+    kp = wl.k_pages if k_pages is None else k_pages
+    vp = wl.v_pages if v_pages is None else v_pages
+    if two_phase:
+        out, lse = att.outputs()
+        att.partial(wl.q, kp, vp, bt, lens, out, lse)
+        att.merge(out, lse)
+    else:
+        out, lse = att(wl.q, kp, vp, bt, lens)
+    torch.cuda.synchronize()
+    res = out.cpu().numpy(), lse.cpu().numpy()
+    att.close()
+    return res
+
+
+def check(gpu, ref, what, seqs=None):
+    out, lse = gpu
+    ro, rl = ref
+    if seqs is not None:
+        out, lse = out[seqs], lse[seqs]
+    assert np.isfinite(out).all() and np.isfinite(lse[np.isfinite(rl)]).all(), what
+    eo = np.abs(out - ro).max() if out.size else 0.0
+    fin = np.isfinite(rl)
+    assert np.array_equal(np.isneginf(lse), np.isneginf(rl)), what
+    el = np.abs(lse[fin] - rl[fin]).max() if fin.any() else 0.0
+    _say(f"{what}: max|out err| {eo:.2e}  max|lse err| {el:.2e}")
+    assert eo <= TOL and el <= TOL, (what, eo, el)
+    return eo, el
+
+
+CUSTOM = [
+    ("g7_d128_ragged", custom_config([1, 15, 16, 17, 31, 32, 33, 1000, 4097, 9],
+                                     28, 4, 128)),
+    ("g5_d128_fp8", custom_config([1, 5, 16, 17, 250, 700, 3001], 40, 8, 128,
+                                  kv_dtype="fp8_e4m3fn")),
+    ("g16_d64", custom_config([3, 64, 100, 513], 32, 2, 64)),
+    ("g1_d128_mha", custom_config([40, 7, 300], 4, 4, 128)),
+    ("g8_d128_prefix", custom_config([10, 400, 1500, 64, 3, 2000, 1100, 90],
+                                     16, 2, 128, prefix_group=4,
+                                     prefix_tokens=1024)),
+    ("g4_d64_fp8_empty", custom_config([0, 17, 0, 64], 8, 2, 64,
+                                       kv_dtype="fp8_e4m3fn")),
+    ("g8_d64_odd_pages", custom_config([16 * 3, 16 * 5 + 1, 16 * 7 - 1], 8, 1, 64)),
+]
+
+
+def test_tiny_config_all_outputs():
+    _need_gpu()
+    wl = make_workload(1, device="cuda")
+    ref = decode_attention_from_host(host_arrays(wl))
+    for waves in (1, 2, 4):
+        for ppi in (0, 1, 4, 64):
+            check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves), ref,
+                  f"tiny waves={waves} pages_per_item={ppi}")
+    check(run_gpu(wl, two_phase=True), ref, "tiny partial+merge")
+
+
+@pytest.mark.parametrize("name,cfg", CUSTOM, ids=[c[0] for c in CUSTOM])
+def test_custom_shapes(name, cfg):
+    _need_gpu()
+    wl = make_workload(cfg, seed=31, device="cuda")
+    ref = decode_attention_from_host(host_arrays(wl), workers=4)
+    for waves in (1, 4):
+        for ppi in (0, 2, 5):
+            check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves), ref,
+                  f"{name} waves={waves} pages_per_item={ppi}")
+
+
+def test_forced_split_independence():
+    _need_gpu()
+    wl = make_workload(custom_config([5000, 777, 12000, 33], 28, 4, 128),
+                       seed=5, device="cuda")
+    base = run_gpu(wl, pages_per_item=100000)
+    for ppi in (1, 2, 7, 64):
+        o, l = run_gpu(wl, pages_per_item=ppi)
+        eo = np.abs(o - base[0]).max()
+        el = np.abs(l - base[1]).max()
+        _say(f"split {ppi} vs unsplit: {eo:.2e} {el:.2e}")
+        assert eo <= 1e-5 and el <= 1e-5
+
+
+def test_page_permutation_bitwise():
+    _need_gpu()
+    wl = make_workload(custom_config([33, 200, 513, 16, 3000], 28, 4, 128),
+                       seed=2, device="cuda")
+    base = run_gpu(wl)
+    p = wl.num_pages
+    perm = torch.randperm(p, generator=torch.Generator().manual_seed(0))
+    kp = torch.empty_like(wl.k_pages)
+    vp = torch.empty_like(wl.v_pages)
+    kp[perm.to(kp.device)] = wl.k_pages
+    vp[perm.to(vp.device)] = wl.v_pages
+    permn = perm.numpy()
+    bt = wl.block_table
+    bt2 = np.where(bt >= 0, permn[np.maximum(bt, 0)], -1).astype(np.int32)
+    o2, l2 = run_gpu(wl, block_table=bt2, k_pages=kp, v_pages=vp)
+    assert np.array_equal(base[0], o2) and np.array_equal(base[1], l2)
+
+
+def test_prefix_alias_equals_copy_bitwise():
+    _need_gpu()
+    cfg = custom_config([10, 400, 1500, 64, 3, 2000, 1100, 90], 16, 2, 128,
+                        prefix_group=4, prefix_tokens=1024)
+    wl = make_workload(cfg, seed=13, device="cuda")
+    base = run_gpu(wl)
+    bt = wl.block_table.copy()
+    extra = []
+    nxt = wl.num_pages
+    seen = set()
+    for b in range(bt.shape[0]):
+        for j in range(bt.shape[1]):
+            p = int(bt[b, j])
+            if p < 0:
+                continue
+            if p in seen:
+                extra.append(p)
+                bt[b, j] = nxt
+                nxt += 1
+            seen.add(p)
+    idx = torch.as_tensor(extra, device=wl.k_pages.device)
+    kp = torch.cat([wl.k_pages, wl.k_pages[idx]])
+    vp = torch.cat([wl.v_pages, wl.v_pages[idx]])
+    o2, l2 = run_gpu(wl, block_table=bt, k_pages=kp, v_pages=vp)
+    assert np.array_equal(base[0], o2) and np.array_equal(base[1], l2)
+
+
+def test_run_to_run_bitwise():
+    _need_gpu()
+    wl = make_workload(custom_config([5000, 777, 33, 12000], 40, 8, 128,
+                                     kv_dtype="fp8_e4m3fn"), seed=8,
+                       device="cuda")
+    a = run_gpu(wl)
+    b = run_gpu(wl)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_single_long_trajectory():
+    """B = 1 with the longest length of the agentic mix (98304 tokens)."""
+    _need_gpu()
+    wl = make_workload(custom_config([98304], 64, 8, 128), seed=17,
+                       device="cuda")
+    ref = decode_attention_from_host(host_arrays(wl), workers=8)
+    check(run_gpu(wl), ref, "B=1 n=98304 auto split")
+    check(run_gpu(wl, pages_per_item=1 << 20, waves_per_item=4), ref,
+          "B=1 n=98304 unsplit")
+
+
+def test_invalid_arguments_return_status():
+    _need_gpu()
+    from paper_2510_12633_amd import _native as N
+    from paper_2510_12633_amd.api import PagedDecodeAttention
+    wl = make_workload(1, device="cuda")
+    bt = torch.as_tensor(wl.block_table, device="cuda")
+    lens = torch.as_tensor(wl.seq_lens, device="cuda")
+    att = PagedDecodeAttention(
+        batch=4, num_q_heads=4, num_kv_heads=1, head_dim=64, num_pages=64,
+        max_blocks_per_seq=bt.shape[1], seq_lens_host=wl.seq_lens,
+        softmax_scale=wl.softmax_scale)
+    out, lse = att.outputs()
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_decode_attn(att.plan, None, wl.k_pages, wl.v_pages, bt, lens,
+                              out, lse, 0)
+    assert e.value.status == N.LAMINAR_ERR_INVALID_ARG
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_decode_attn(None, wl.q, wl.k_pages, wl.v_pages, bt, lens,
+                              out, lse, 0)
+    assert e.value.status == N.LAMINAR_ERR_INVALID_ARG
+    small = torch.empty(64, dtype=torch.uint8, device="cuda")
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_plan_bind_workspace(att.plan, small, 64, 0)
+    assert e.value.status == N.LAMINAR_ERR_WORKSPACE
+    # an unbound plan refuses to launch
+    plan = N.laminar_plan_create(att.desc, wl.seq_lens, 256)
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_decode_attn(plan, wl.q, wl.k_pages, wl.v_pages, bt, lens,
+                              out, lse, 0)
+    assert e.value.status == N.LAMINAR_ERR_WORKSPACE
+    N.laminar_plan_destroy(plan)
+    att.close()
+
+
+def _sample(lens, k, seed):
+    order = np.argsort(lens, kind="stable")
+    pick = {int(order[0]), int(order[-1]), int(order[len(order) // 2])}
+    rng = np.random.default_rng(seed)
+    while len(pick) < min(k, len(lens)):
+        pick.add(int(rng.integers(len(lens))))
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("idx", [2, 3, 4, 5])
+def test_full_size_config_sampled(idx):
+    """Full-size batch in the bench's launch configuration; the oracle checks
+    sampled trajectories (shortest, longest, median and random ones)."""
+    _need_gpu()
+    cfg = get_config(idx)
+    _say(f"generating {cfg.name}")
+    wl = make_workload(cfg, device="cuda")
+    out, lse = run_gpu(wl)
+    assert np.isfinite(out).all() and np.isfinite(lse).all()
+    seqs = _sample(wl.seq_lens, 6 if idx == 5 else 8, idx)
+    ref = decode_attention_from_host(host_arrays(wl, seqs), workers=8)
+    check((out, lse), ref, f"{cfg.name} sampled {seqs}", seqs=seqs)
+    del wl
+    torch.cuda.empty_cache()
