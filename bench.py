@@ -1,0 +1,378 @@
+#!/usr/bin/env python3
+"""Benchmark of paged grouped-query decode attention on one MI355X.
+
+One step is one pass of the whole hot path over one batch: plan the split of
+the batch's KV pages across CUs (host), upload the work list, run the split-KV
+partial kernel and the log-sum-exp merge. Inputs are generated on the GPU
+before timing and stay resident in HBM.
+
+Default workload: 256 trajectories with lognormal(median 2048, sigma 1)
+lengths clipped to [16, 32768], 28 query / 4 KV heads, head_dim 128, bf16 KV
+(a 7B-class rollout step before repack). Prints ONE JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME|N]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import platform
+import random
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn KV TB/s (fraction of HBM peak) + tokens/s at long-tail batch"
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+DEFAULT_WORKLOAD = "7b_pre_repack"
+PARTIAL_KERNEL = "decode_partial"
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2510_12633_amd", "csrc",
+                             "decode_attn.hip")
+
+
+def parse_args(argv=None):
+    p = argparse.ArgumentParser(description=__doc__,
+                                formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default=DEFAULT_WORKLOAD,
+                   help="workload name or 1-based index")
+    p.add_argument("--seed", type=int, default=None)
+    p.add_argument("--waves-per-item", type=int, default=0)
+    p.add_argument("--pages-per-item", type=int, default=0)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-budget-s", type=float, default=15.0,
+                   help="target seconds of oracle work for the CPU baseline")
+    p.add_argument("--no-calibrate", action="store_true",
+                   help="skip the HBM read/copy calibration kernels")
+    p.add_argument("--fixed-plan", action="store_true",
+                   help="plan once outside the timed loop (kernel-only steps)")
+    return p.parse_args(argv)
+
+
+def source_digest() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic(workload: str):
+    """HBM bytes per partial-kernel launch from the committed rocprofv3
+    --pmc summary, if it was taken on the current kernel source."""
+    path = os.path.join(PROFILE_DIR, f"{PARTIAL_KERNEL}_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None, None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256_16") != source_digest():
+        return None, "stale"
+    try:
+        return float(vals["hbm_bytes_per_launch"]), path
+    except (KeyError, ValueError):
+        return None, None
+
+
+class Rotation:
+    """Copies of the KV pools so that inputs under ~2 GB are not served from
+    the 256 MB Infinity Cache on back-to-back steps."""
+
+    def __init__(self, wl, min_bytes=2 << 30):
+        import torch
+        pool = wl.k_pages.numel() * wl.k_pages.element_size() * 2
+        n = max(1, math.ceil(min_bytes / max(pool, 1)))
+        n = min(n, 64)
+        self.k = [wl.k_pages] + [wl.k_pages.clone() for _ in range(n - 1)]
+        self.v = [wl.v_pages] + [wl.v_pages.clone() for _ in range(n - 1)]
+        self.n = n
+        torch.cuda.synchronize()
+
+    def get(self, i):
+        j = i % self.n
+        return self.k[j], self.v[j]
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.machine()
+
+
+def cpu_baseline(wl, budget_s: float):
+    """The fp64 oracle on the host over a bounded sample of the workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import decode_attention_from_host
+    from workloads import host_arrays
+
+    cores = len(os.sched_getaffinity(0))
+    rng = random.Random(0)
+    order = list(range(wl.batch))
+    rng.shuffle(order)
+    c = wl.cfg
+    per_tok = c.num_kv_heads * c.head_dim * 2 * c.kv_elem_bytes
+    with threadpool_limits(1):
+        # calibrate on a few trajectories, then size the sample to the budget
+        probe = order[:min(4, len(order))]
+        t0 = time.perf_counter()
+        decode_attention_from_host(host_arrays(wl, probe), workers=cores)
+        dt = max(time.perf_counter() - t0, 1e-3)
+        rate = max(int(wl.seq_lens[probe].sum()), 1) / dt       # tokens/s
+        want = rate * budget_s
+        sample, tot = [], 0
+        for b in order:
+            if tot >= want and sample:
+                break
+            sample.append(b)
+            tot += int(wl.seq_lens[b])
+        arrays = host_arrays(wl, sorted(sample))
+        t0 = time.perf_counter()
+        decode_attention_from_host(arrays, workers=cores)
+        dt = time.perf_counter() - t0
+    toks = int(wl.seq_lens[sample].sum())
+    return {
+        "value": toks * per_tok / dt / 1e12,
+        "unit": "TB/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": f"{len(sample)} of {wl.batch} trajectories ({toks} tokens, "
+                  f"{toks * per_tok / 1e9:.3f} GB of KV), fp64 numpy, "
+                  f"{cores} threads over trajectories, BLAS 1 thread each",
+        "seconds": dt,
+        "tokens_per_s": len(sample) / dt,
+        "cpu": cpu_model(),
+    }
+
+
+def calibrate(torch, N, nbytes=4 << 30, iters=10):
+    """Achievable HBM read and copy bandwidth (GB/s) on this device."""
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    sink = torch.empty(N.laminar_hbm_read_sink_floats(), dtype=torch.float32,
+                       device="cuda")
+    s = torch.cuda.current_stream()
+    h = s.cuda_stream
+    for _ in range(2):
+        N.laminar_hbm_read(buf, nbytes, sink, h)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for _ in range(iters):
+        N.laminar_hbm_read(buf, nbytes, sink, h)
+    e1.record(s)
+    torch.cuda.synchronize()
+    read = nbytes * iters / (e0.elapsed_time(e1) / 1e3) / 1e9
+    half = nbytes // 2
+    dst, src = buf[:half], buf[half:]
+    N.laminar_hbm_copy(dst, src, half, h)
+    e0.record(s)
+    for _ in range(iters):
+        N.laminar_hbm_copy(dst, src, half, h)
+    e1.record(s)
+    torch.cuda.synchronize()
+    copy = 2 * half * iters / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del buf
+    torch.cuda.empty_cache()
+    return read, copy
+
+
+def main(argv=None):
+    args = parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not "
+              "supported (the decode-attention path needs no collectives and "
+              "shards by trajectory or kv-head with no exchange).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2510_12633_amd import _native as N
+    from paper_2510_12633_amd.api import KV_DTYPES, num_cus
+    from workloads import get_config, make_workload
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    N.lib()      # fail loudly if the HIP library is not built
+
+    cfg = get_config(args.workload)
+    wl = make_workload(cfg, seed=args.seed, device="cuda")
+    dev_lens = torch.as_tensor(wl.seq_lens, device="cuda")
+    bt = torch.as_tensor(wl.block_table, device="cuda")
+    cus = num_cus()
+    desc = N.LaminarAttnDesc(
+        batch=wl.batch, num_q_heads=cfg.num_q_heads,
+        num_kv_heads=cfg.num_kv_heads, head_dim=cfg.head_dim, page_size=16,
+        num_pages=wl.num_pages, max_blocks_per_seq=wl.block_table.shape[1],
+        kv_dtype=KV_DTYPES[cfg.kv_dtype], softmax_scale=wl.softmax_scale,
+        k_scale=None if wl.k_scale is None else wl.k_scale.data_ptr(),
+        v_scale=None if wl.v_scale is None else wl.v_scale.data_ptr(),
+        pages_per_item=args.pages_per_item, waves_per_item=args.waves_per_item)
+    lens_host = np.ascontiguousarray(wl.seq_lens, dtype=np.int32)
+
+    kv_bytes = wl.kv_bytes_unique()
+    alg_bytes = wl.algorithmic_bytes()
+    rot = Rotation(wl) if kv_bytes < (1 << 30) else None
+
+    out = torch.empty((wl.batch, cfg.num_q_heads, cfg.head_dim),
+                      dtype=torch.float32, device="cuda")
+    lse = torch.empty((wl.batch, cfg.num_q_heads), dtype=torch.float32,
+                      device="cuda")
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+
+    # Workspace sized for this batch's plan; reused every step.
+    plan0 = N.laminar_plan_create(desc, lens_host, cus)
+    ws_bytes = N.laminar_plan_workspace_bytes(plan0)
+    n_items = N.laminar_plan_num_items(plan0)
+    n_merges = N.laminar_plan_num_merges(plan0)
+    ppi = N.laminar_plan_pages_per_item(plan0)
+    waves = N.laminar_plan_waves_per_item(plan0)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    N.laminar_plan_bind_workspace(plan0, ws, ws_bytes, sh)
+
+    steps, warm = args.steps, args.warmup
+    ev = [(torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    plan_ns = []
+    live = [plan0]
+
+    def one_step(i, events=None):
+        if args.fixed_plan:
+            plan = plan0
+        else:
+            t0 = time.perf_counter_ns()
+            plan = N.laminar_plan_create(desc, lens_host, cus)
+            N.laminar_plan_bind_workspace(plan, ws, ws_bytes, sh)
+            plan_ns.append(time.perf_counter_ns() - t0)
+            live.append(plan)
+        kp, vp = rot.get(i) if rot else (wl.k_pages, wl.v_pages)
+        if events:
+            events[0].record(stream)
+        N.laminar_decode_attn_partial(plan, wl.q, kp, vp, bt, dev_lens, out,
+                                      lse, sh)
+        if events:
+            events[1].record(stream)
+        N.laminar_decode_attn_merge(plan, out, lse, sh)
+        if events:
+            events[2].record(stream)
+
+    for i in range(warm):
+        one_step(i)
+    torch.cuda.synchronize()
+    # plans are destroyed only after the stream has passed their uploads
+    for p in live[1:]:
+        N.laminar_plan_destroy(p)
+    live[1:] = []
+    plan_ns.clear()
+
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(steps):
+        one_step(warm + i, ev[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    for p in live[1:]:
+        N.laminar_plan_destroy(p)
+    live[1:] = []
+
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / steps
+    k1 = [a.elapsed_time(b) for a, b, _ in ev]
+    k2 = [b.elapsed_time(c) for _, b, c in ev]
+    k1_ms = sum(k1) / len(k1)
+    k2_ms = sum(k2) / len(k2)
+    step_s = ms_step / 1e3
+
+    value = kv_bytes / step_s / 1e12
+    achieved = alg_bytes / (k1_ms / 1e3) / 1e9
+    traffic, traffic_src = read_traffic(cfg.name)
+    roofline = {
+        "bound": "hbm",
+        "kernel": PARTIAL_KERNEL,
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBPS, 4),
+        "traffic": traffic,
+        "algorithmic_bytes_per_launch": alg_bytes,
+        "avg_launch_ms": round(k1_ms, 5),
+    }
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 4),
+        "unit": "TB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.kv_dtype == "bf16" else "fp8e4m3-kv/bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name,
+            "batch": wl.batch,
+            "q_heads": cfg.num_q_heads,
+            "kv_heads": cfg.num_kv_heads,
+            "head_dim": cfg.head_dim,
+            "kv_dtype": cfg.kv_dtype,
+            "context_tokens": int(wl.seq_lens.sum()),
+            "seed": wl.seed,
+            "pages_per_item": ppi,
+            "waves_per_item": waves,
+            "work_items": n_items,
+            "merged_units": n_merges,
+            "plan_every_step": not args.fixed_plan,
+            "kv_pool_copies_rotated": rot.n if rot else 1,
+        },
+        "frac_hbm_peak": round(value * 1e3 / HBM_PEAK_GBPS, 4),
+        "tokens_per_s": round(wl.batch / step_s, 1),
+        "context_tokens_per_s": round(float(wl.seq_lens.sum()) / step_s, 1),
+        "kv_bytes": kv_bytes,
+        "algorithmic_bytes": alg_bytes,
+        "kernel_ms": {"decode_partial": round(k1_ms, 5),
+                      "decode_merge": round(k2_ms, 5)},
+        "plan_host_ms": round(sum(plan_ns) / max(len(plan_ns), 1) / 1e6, 5)
+        if plan_ns else None,
+        "wall_s_timed": round(wall, 4),
+        "roofline": roofline,
+    }
+    if traffic_src == "stale":
+        result["roofline"]["traffic_note"] = "counters predate the current kernel"
+    if not args.no_calibrate:
+        rd, cp = calibrate(torch, N)
+        result["hbm_calibration_GBps"] = {"read": round(rd, 1),
+                                          "copy": round(cp, 1)}
+        result["frac_of_calibrated_read"] = round(value * 1e3 / rd, 4)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget_s)
+    N.laminar_plan_destroy(plan0)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
