@@ -67,6 +67,14 @@ struct Geo {
   static constexpr int TILE = 16 * D * EB;      // bytes per tile
   static constexpr int KL = 8 * KK * EB / 16;   // 16-byte K loads per lane
   static constexpr int VL = 4 * NT * EB / 16;   // 16-byte V loads per lane
+  static constexpr int DPL = 4 / EB;            // dims per 16-byte V load
+  // Dim of row m of P*V tile n. Load j of a lane in row m covers dims
+  // j*16*DPL + m*DPL .. +DPL-1, so the 16 lanes of a group read one
+  // contiguous 256-byte run per load; tile n is element n % DPL of load
+  // n / DPL.
+  static constexpr int vdim(int n, int m) {
+    return (n / DPL) * 16 * DPL + m * DPL + n % DPL;
+  }
 };
 
 template <int D, bool FP8>
@@ -134,8 +142,8 @@ __device__ __forceinline__ bf16x8 k_frag(const u32x4 (&k)[Geo<D, FP8>::KL],
 }
 
 // A-operand fragment of V^T for dim tile n: lane (row m = lane%16, group gq)
-// holds dim m*NT + n of tokens 4gq..4gq+3 of page A (items 0-3) and of
-// page B (items 4-7).
+// holds dim Geo::vdim(n, m) of tokens 4gq..4gq+3 of page A (items 0-3) and
+// of page B (items 4-7).
 template <int D, bool FP8>
 __device__ __forceinline__ bf16x8 v_frag(const u32x4 (&va)[Geo<D, FP8>::VL],
                                          const u32x4 (&vb)[Geo<D, FP8>::VL],
@@ -223,7 +231,7 @@ decode_partial(const DecodeArgs a) {
   const uint8_t* vbase = a.v_pages + size_t(kvh) * G::TILE;
   const int32_t* bt = a.block_table + size_t(b) * a.max_blocks + p0;
   const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
-  const int voff = (gq * D + r16 * G::NT) * G::EB / 4;       // u32x4 units
+  const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
 
   // Block-table entries of this item, 64 pages per window, one per lane.
   int win = -1;
@@ -251,14 +259,20 @@ decode_partial(const DecodeArgs a) {
     const u32x4* kb = reinterpret_cast<const u32x4*>(kbase + size_t(ppb) * page_stride);
     const u32x4* va = reinterpret_cast<const u32x4*>(vbase + size_t(ppa) * page_stride);
     const u32x4* vb = reinterpret_cast<const u32x4*>(vbase + size_t(ppb) * page_stride);
+    // KV pages are streamed once per call: non-temporal loads keep them
+    // from displacing reusable lines in L2 and the Infinity Cache.
 #pragma unroll
-    for (int j = 0; j < G::KL; ++j) pr.ka[j] = ka[koff + j * 16];
+    for (int j = 0; j < G::KL; ++j)
+      pr.ka[j] = __builtin_nontemporal_load(&ka[koff + j * 16]);
 #pragma unroll
-    for (int j = 0; j < G::KL; ++j) pr.kb[j] = kb[koff + j * 16];
+    for (int j = 0; j < G::KL; ++j)
+      pr.kb[j] = __builtin_nontemporal_load(&kb[koff + j * 16]);
 #pragma unroll
-    for (int j = 0; j < G::VL; ++j) pr.va[j] = va[voff + j];
+    for (int j = 0; j < G::VL; ++j)
+      pr.va[j] = __builtin_nontemporal_load(&va[voff + j * 16]);
 #pragma unroll
-    for (int j = 0; j < G::VL; ++j) pr.vb[j] = vb[voff + j];
+    for (int j = 0; j < G::VL; ++j)
+      pr.vb[j] = __builtin_nontemporal_load(&vb[voff + j * 16]);
     if constexpr (FP8) {
       pr.ksa = a.k_scale[size_t(ppa) * a.hkv + kvh];
       pr.ksb = a.k_scale[size_t(ppb) * a.hkv + kvh];
@@ -424,14 +438,22 @@ decode_partial(const DecodeArgs a) {
     dst = a.o_part + (size_t(it.w) * a.group + r16) * D;
     lse_dst = a.lse_part + size_t(it.w) * a.group + r16;
   }
-  // Lane holds dims (4gq + r)*NT + n: NT contiguous floats for each r.
+  // Row 4gq + r of tile n is dim vdim(n, 4gq + r): for each load j the lane
+  // holds 4*DPL contiguous dims starting at j*16*DPL + 4gq*DPL, ordered
+  // (r, e) with n = j*DPL + e.
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float4* row = reinterpret_cast<float4*>(dst + (4 * gq + r) * G::NT);
+  for (int j = 0; j < G::NT / G::DPL; ++j) {
+    float vals[4 * G::DPL];
 #pragma unroll
-    for (int n4 = 0; n4 < G::NT / 4; ++n4)
-      row[n4] = make_float4(acc[4 * n4][r] * inv, acc[4 * n4 + 1][r] * inv,
-                            acc[4 * n4 + 2][r] * inv, acc[4 * n4 + 3][r] * inv);
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int e = 0; e < G::DPL; ++e)
+        vals[r * G::DPL + e] = acc[j * G::DPL + e][r] * inv;
+    float4* run = reinterpret_cast<float4*>(dst + G::vdim(j * G::DPL, 4 * gq));
+#pragma unroll
+    for (int k = 0; k < G::DPL; ++k)
+      run[k] = make_float4(vals[4 * k], vals[4 * k + 1], vals[4 * k + 2],
+                           vals[4 * k + 3]);
   }
   if (gq == 0) *lse_dst = lse_v;
 }
@@ -503,20 +525,29 @@ __global__ void __launch_bounds__(256) decode_merge(const DecodeArgs a) {
   }
 }
 
-constexpr int kReadBlocks = 2048;
+// Calibration kernels: each workgroup streams one contiguous chunk with
+// non-temporal 16-byte accesses, eight in flight per lane.
+constexpr int kCalibChunk16 = 4096;          // 64 KiB per workgroup
+constexpr int kReadSinkFloats = 1 << 16;     // workgroups per read pass
 
 __global__ void __launch_bounds__(256)
 hbm_read_kernel(const u32x4* __restrict__ src, size_t n16, float* sink) {
-  float s = 0.f;
-  const size_t stride = size_t(gridDim.x) * blockDim.x;
-  size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    const u32x4 v0 = src[i], v1 = src[i + stride], v2 = src[i + 2 * stride],
-                v3 = src[i + 3 * stride];
-    s += (__uint_as_float(v0[0] ^ v1[1]) + __uint_as_float(v2[2] ^ v3[3]));
+  uint32_t acc = 0;
+  for (size_t blk = blockIdx.x; blk * kCalibChunk16 < n16; blk += gridDim.x) {
+    const size_t beg = blk * kCalibChunk16;
+    const size_t end = beg + kCalibChunk16 < n16 ? beg + kCalibChunk16 : n16;
+    size_t i = beg + threadIdx.x;
+    for (; i + 7 * 256 < end; i += 8 * 256) {
+      u32x4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * 256]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+    }
+    for (; i < end; i += 256) acc ^= src[i][0];
   }
-  for (; i < n16; i += stride) s += __uint_as_float(src[i][0]);
-  s = wave_sum(s);
+  // Every lane's value feeds the workgroup sum, so no load is dead code.
+  float s = wave_sum(__uint_as_float(acc & 0x007FFFFFu));
   __shared__ float red[4];
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
   __syncthreads();
@@ -526,10 +557,25 @@ hbm_read_kernel(const u32x4* __restrict__ src, size_t n16, float* sink) {
 __global__ void __launch_bounds__(256)
 hbm_copy_kernel(u32x4* __restrict__ dst, const u32x4* __restrict__ src,
                 size_t n16) {
-  const size_t stride = size_t(gridDim.x) * blockDim.x;
-  for (size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n16;
-       i += stride)
-    dst[i] = src[i];
+  for (size_t blk = blockIdx.x; blk * kCalibChunk16 < n16; blk += gridDim.x) {
+    const size_t beg = blk * kCalibChunk16;
+    const size_t end = beg + kCalibChunk16 < n16 ? beg + kCalibChunk16 : n16;
+    size_t i = beg + threadIdx.x;
+    for (; i + 7 * 256 < end; i += 8 * 256) {
+      u32x4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * 256]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) __builtin_nontemporal_store(v[u], &dst[i + u * 256]);
+    }
+    for (; i < end; i += 256) dst[i] = src[i];
+  }
+}
+
+unsigned calib_grid(size_t n16) {
+  const size_t chunks = (n16 + kCalibChunk16 - 1) / kCalibChunk16;
+  return unsigned(chunks < size_t(kReadSinkFloats) ? (chunks ? chunks : 1)
+                                                   : size_t(kReadSinkFloats));
 }
 
 template <int D, bool FP8>
@@ -693,15 +739,16 @@ laminar_status laminar_decode_attn(const laminar_plan* plan, const void* q,
   return run_merge(plan, a, stream);
 }
 
-int32_t laminar_hbm_read_sink_floats(void) { return kReadBlocks; }
+int32_t laminar_hbm_read_sink_floats(void) { return kReadSinkFloats; }
 
 laminar_status laminar_hbm_read(const void* src, size_t bytes, float* sink,
                                 hipStream_t stream) {
   if (!src || !sink || (bytes & 15) ||
       (reinterpret_cast<uintptr_t>(src) & 15))
     return LAMINAR_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(hbm_read_kernel, dim3(kReadBlocks), dim3(256), 0, stream,
-                     static_cast<const u32x4*>(src), bytes / 16, sink);
+  hipLaunchKernelGGL(hbm_read_kernel, dim3(calib_grid(bytes / 16)), dim3(256),
+                     0, stream, static_cast<const u32x4*>(src), bytes / 16,
+                     sink);
   return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
 }
 
@@ -712,9 +759,9 @@ laminar_status laminar_hbm_copy(void* dst, const void* src, size_t bytes,
       (reinterpret_cast<uintptr_t>(dst) & 15))
     return LAMINAR_ERR_INVALID_ARG;
   if (bytes == 0) return LAMINAR_OK;
-  hipLaunchKernelGGL(hbm_copy_kernel, dim3(kReadBlocks), dim3(256), 0, stream,
-                     static_cast<u32x4*>(dst), static_cast<const u32x4*>(src),
-                     bytes / 16);
+  hipLaunchKernelGGL(hbm_copy_kernel, dim3(calib_grid(bytes / 16)), dim3(256),
+                     0, stream, static_cast<u32x4*>(dst),
+                     static_cast<const u32x4*>(src), bytes / 16);
   return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
 }
 
