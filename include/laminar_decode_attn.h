@@ -117,11 +117,17 @@ size_t laminar_plan_workspace_bytes(const laminar_plan* plan);
 
 /*
  * Bind a caller-owned device workspace of `bytes` >= workspace_bytes, 256-byte
- * aligned, and enqueue the copy of the plan's work and merge lists into it
- * on `stream`. The workspace must stay allocated, and must not be used by
- * anything else, while calls with this plan may run. The plan's host tables
- * must outlive the copy: do not destroy the plan before the stream has
- * passed it. Errors: INVALID_ARG, WORKSPACE, HIP.
+ * aligned, and enqueue the upload of the plan's work and merge lists into it
+ * on `stream`. The lists are first copied into a pinned host staging slot of
+ * the library (one small ring per device, allocated on first use and kept
+ * until the process exits), so the upload does not wait for earlier work on
+ * the stream and the plan may be destroyed as soon as this call returns.
+ * Lists larger than one staging slot (1 MiB, about 65k work items) are
+ * copied directly and the call waits for `stream` to finish the copy.
+ * The workspace must stay allocated, and must not be used by anything else,
+ * while calls with this plan may run; binding another plan to the same
+ * workspace on the same stream is ordered after those calls.
+ * Errors: INVALID_ARG, WORKSPACE, HIP.
  */
 laminar_status laminar_plan_bind_workspace(laminar_plan* plan, void* workspace,
                                            size_t bytes, hipStream_t stream);

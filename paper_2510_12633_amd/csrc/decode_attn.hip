@@ -23,6 +23,8 @@
 
 #include <cmath>
 #include <cstdint>
+#include <cstring>
+#include <mutex>
 
 #include "laminar_decode_attn.h"
 #include "plan_internal.h"
@@ -664,6 +666,63 @@ bool inputs_ok(const laminar_plan* p, const void* q, const void* k_pages,
   return q && k_pages && v_pages && block_table && seq_lens && out && lse;
 }
 
+// Pinned staging for plan uploads. A copy from pageable memory can block
+// the host until the stream drains; copying the tables into one of a few
+// pinned slots first keeps the upload asynchronous and lets the caller free
+// the plan as soon as bind returns. One ring per device, created on first
+// use and kept for the life of the process; a slot is reused only after
+// the event recorded behind its last upload has completed.
+struct StagingRing {
+  static constexpr int kSlots = 8;
+  static constexpr size_t kSlotBytes = size_t(1) << 20;
+  char* host = nullptr;
+  hipEvent_t done[kSlots] = {};
+  bool pending[kSlots] = {};
+  int next = 0;
+};
+
+constexpr int kMaxDevices = 64;
+std::mutex g_ring_mutex;
+StagingRing g_rings[kMaxDevices];
+
+laminar_status upload_tables(void* dst, const void* src, size_t bytes,
+                             hipStream_t stream) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return LAMINAR_ERR_HIP;
+  if (bytes > StagingRing::kSlotBytes || dev < 0 || dev >= kMaxDevices) {
+    // Too large for a slot: copy straight from the plan and wait for it, so
+    // the plan can still be freed when bind returns.
+    hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> lock(g_ring_mutex);
+  StagingRing& ring = g_rings[dev];
+  if (!ring.host) {
+    void* h = nullptr;
+    if (hipHostMalloc(&h, StagingRing::kSlots * StagingRing::kSlotBytes,
+                      hipHostMallocDefault) != hipSuccess)
+      return LAMINAR_ERR_HIP;
+    for (int i = 0; i < StagingRing::kSlots; ++i)
+      if (hipEventCreateWithFlags(&ring.done[i], hipEventDisableTiming) !=
+          hipSuccess)
+        return LAMINAR_ERR_HIP;
+    ring.host = static_cast<char*>(h);
+  }
+  const int slot = ring.next;
+  ring.next = (slot + 1) % StagingRing::kSlots;
+  if (ring.pending[slot] && hipEventSynchronize(ring.done[slot]) != hipSuccess)
+    return LAMINAR_ERR_HIP;
+  char* stage = ring.host + size_t(slot) * StagingRing::kSlotBytes;
+  std::memcpy(stage, src, bytes);
+  if (hipMemcpyAsync(dst, stage, bytes, hipMemcpyHostToDevice, stream) !=
+          hipSuccess ||
+      hipEventRecord(ring.done[slot], stream) != hipSuccess)
+    return LAMINAR_ERR_HIP;
+  ring.pending[slot] = true;
+  return LAMINAR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -683,19 +742,7 @@ laminar_status laminar_plan_bind_workspace(laminar_plan* plan, void* workspace,
   plan->ws_size = bytes;
   const size_t table_bytes = plan->tables.size() * sizeof(int32_t);
   if (table_bytes == 0) return LAMINAR_OK;
-  // Items then merges, at their section offsets.
-  char* ws = static_cast<char*>(workspace);
-  const size_t item_bytes = size_t(plan->num_items) * 16;
-  hipError_t e = hipSuccess;
-  if (item_bytes)
-    e = hipMemcpyAsync(ws + plan->off_items, plan->tables.data(), item_bytes,
-                       hipMemcpyHostToDevice, stream);
-  if (e == hipSuccess && plan->num_merges)
-    e = hipMemcpyAsync(ws + plan->off_merges,
-                       plan->tables.data() + size_t(4) * plan->num_items,
-                       size_t(plan->num_merges) * 16, hipMemcpyHostToDevice,
-                       stream);
-  return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+  return upload_tables(workspace, plan->tables.data(), table_bytes, stream);
 }
 
 laminar_status laminar_decode_attn_partial(const laminar_plan* plan,

@@ -124,12 +124,6 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   p->num_items = int32_t(items.size());
   p->num_merges = int32_t(merges.size());
   p->num_slots = slots;
-  p->tables.resize(size_t(4) * (items.size() + merges.size()));
-  if (!items.empty())
-    std::memcpy(p->tables.data(), items.data(), items.size() * sizeof(Item));
-  if (!merges.empty())
-    std::memcpy(p->tables.data() + 4 * items.size(), merges.data(),
-                merges.size() * sizeof(Item));
 
   size_t off = 0;
   p->off_items = off;
@@ -141,6 +135,16 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   p->off_o = off;
   off = align256(off + size_t(slots) * p->group * desc->head_dim * sizeof(float));
   p->ws_bytes = off;
+
+  // Byte image of the workspace up to the partial results: items, then
+  // merges, at their section offsets (zero padding between).
+  p->tables.assign(p->off_lse / sizeof(int32_t), 0);
+  if (!items.empty())
+    std::memcpy(p->tables.data() + p->off_items / 4, items.data(),
+                items.size() * sizeof(Item));
+  if (!merges.empty())
+    std::memcpy(p->tables.data() + p->off_merges / 4, merges.data(),
+                merges.size() * sizeof(Item));
   } catch (...) {            // host allocation failure: report, never throw
     delete p;
     return LAMINAR_ERR_INVALID_ARG;
@@ -173,7 +177,7 @@ int32_t laminar_plan_items_copy(const laminar_plan* plan, int32_t* dst,
                                 int32_t capacity) {
   if (!plan || !dst || capacity < 0) return -1;
   const int32_t n = std::min(capacity, plan->num_items);
-  std::memcpy(dst, plan->tables.data(), size_t(n) * 16);
+  std::memcpy(dst, plan->tables.data() + plan->off_items / 4, size_t(n) * 16);
   return n;
 }
 
@@ -181,8 +185,7 @@ int32_t laminar_plan_merges_copy(const laminar_plan* plan, int32_t* dst,
                                  int32_t capacity) {
   if (!plan || !dst || capacity < 0) return -1;
   const int32_t n = std::min(capacity, plan->num_merges);
-  std::memcpy(dst, plan->tables.data() + size_t(4) * plan->num_items,
-              size_t(n) * 16);
+  std::memcpy(dst, plan->tables.data() + plan->off_merges / 4, size_t(n) * 16);
   return n;
 }
 

@@ -16,7 +16,8 @@ struct laminar_plan {
   int32_t num_items = 0;
   int32_t num_merges = 0;
   int32_t num_slots = 0;       // partial (out, lse) records
-  // Host image of the device tables: items (4 int32 each) then merges.
+  // Host image of workspace bytes [0, off_lse): the work items (4 int32
+  // each) at off_items and the merge records at off_merges.
   std::vector<int32_t> tables;
   // Workspace layout (byte offsets, 256-byte aligned sections).
   size_t off_items = 0, off_merges = 0, off_lse = 0, off_o = 0;

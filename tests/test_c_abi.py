@@ -1,0 +1,233 @@
+"""CPU checks of the C ABI: exported symbols, the host planner, and the
+argument errors returned before any HIP call. No GPU is touched."""
+import ctypes
+import os
+import re
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2510_12633_amd import _native as N
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "laminar_decode_attn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(laminar_\w+)\s*\(", text)))
+
+
+def desc(batch=4, hq=28, hkv=4, d=128, pages=10**6, max_blocks=8192,
+         kv=N.LAMINAR_KV_BF16, scale=0.1, ppi=0, waves=0, k_scale=None,
+         v_scale=None, page_size=16):
+    return N.LaminarAttnDesc(batch=batch, num_q_heads=hq, num_kv_heads=hkv,
+                             head_dim=d, page_size=page_size, num_pages=pages,
+                             max_blocks_per_seq=max_blocks, kv_dtype=kv,
+                             softmax_scale=scale, k_scale=k_scale,
+                             v_scale=v_scale, pages_per_item=ppi,
+                             waves_per_item=waves)
+
+
+def plan_tables(d, lens, cus=256):
+    p = N.laminar_plan_create(d, np.asarray(lens, np.int32), cus)
+    try:
+        return (N.laminar_plan_items_copy(p), N.laminar_plan_merges_copy(p),
+                N.laminar_plan_pages_per_item(p), N.laminar_plan_waves_per_item(p),
+                N.laminar_plan_workspace_bytes(p))
+    finally:
+        N.laminar_plan_destroy(p)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = N.lib()
+    names = declared_functions()
+    assert len(names) >= 17
+    for name in names:
+        assert hasattr(lib, name), name
+    nm = shutil.which("nm")
+    if nm:
+        out = subprocess.run([nm, "-D", "--defined-only", N.library_path()],
+                             capture_output=True, text=True).stdout
+        exported = set(re.findall(r"\bT (laminar_\w+)", out))
+        assert set(names) <= exported, set(names) - exported
+
+
+def test_status_strings():
+    for st in range(5):
+        assert N.laminar_status_string(st) not in ("", "unknown status")
+    assert N.laminar_status_string(99) == "unknown status"
+
+
+def check_plan(lens, hkv, items, merges, ppi):
+    pages = -(-np.asarray(lens, np.int64) // 16)
+    covered = {}
+    by_unit = {}
+    for unit, p0, p1, slot in items:
+        b, h = divmod(int(unit), hkv)
+        assert 0 <= p0 <= p1 <= pages[b]
+        assert p1 - p0 <= ppi
+        by_unit.setdefault(int(unit), []).append((int(p0), int(p1), int(slot)))
+        for p in range(p0, p1):
+            key = (int(unit), p)
+            assert key not in covered
+            covered[key] = True
+    # every (trajectory, kv-head, page) exactly once; empty units once
+    assert len(covered) == int(pages.sum()) * hkv
+    assert set(by_unit) == set(range(len(lens) * hkv))
+    sizes = [p1 - p0 for _, p0, p1, _ in items]
+    assert sizes == sorted(sizes, reverse=True)
+    merged = {int(m[0]): (int(m[1]), int(m[2])) for m in merges}
+    assert len(merged) == len(merges)
+    all_slots = []
+    for unit, chunks in by_unit.items():
+        sz = [p1 - p0 for p0, p1, _ in chunks]
+        assert max(sz) - min(sz) <= 1
+        if len(chunks) == 1:
+            assert chunks[0][2] == -1 and unit not in merged
+        else:
+            slot0, n = merged[unit]
+            assert n == len(chunks)
+            got = sorted(s for _, _, s in chunks)
+            assert got == list(range(slot0, slot0 + n))
+            # slots follow page order inside the unit
+            assert [s for _, _, s in sorted(chunks)] == got
+            all_slots += got
+    assert len(all_slots) == len(set(all_slots))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_planner_invariants_random(seed):
+    rng = np.random.default_rng(seed)
+    b = int(rng.integers(1, 300))
+    lens = np.minimum(np.exp(rng.normal(7, 1.5, b)).astype(np.int64), 70000)
+    lens[rng.random(b) < 0.05] = 0
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    for ppi, waves in ((0, 0), (1, 1), (3, 2), (64, 4), (1 << 20, 0)):
+        d = desc(batch=b, hq=hkv * int(rng.integers(1, 9)), hkv=hkv, ppi=ppi,
+                 waves=waves)
+        items, merges, chosen, w, ws = plan_tables(d, lens)
+        if ppi:
+            assert chosen == ppi
+        assert w == (waves or 4)
+        check_plan(lens, hkv, items, merges, chosen)
+        assert ws % 256 == 0 and ws >= 16 * (len(items) + len(merges))
+
+
+def test_planner_auto_split_fills_the_gpu():
+    """Eight 64k-token trajectories x 4 kv-heads (32 units) still give
+    thousands of work items."""
+    lens = [65536] * 8
+    items, merges, chosen, waves, _ = plan_tables(desc(batch=8), lens)
+    assert len(items) >= 1000 and len(merges) == 32
+    assert chosen % (2 * waves) == 0
+    check_plan(lens, 4, items, merges, chosen)
+
+
+def test_planner_edge_lengths():
+    for lens in ([0], [1], [16], [17], [0, 0, 0], [98304], [1, 98304, 0, 15]):
+        d = desc(batch=len(lens), hq=64, hkv=8)
+        items, merges, chosen, _, _ = plan_tables(d, lens)
+        check_plan(lens, 8, items, merges, chosen)
+    items, merges, _, _, _ = plan_tables(desc(batch=0), [])
+    assert len(items) == 0 and len(merges) == 0
+
+
+def test_planner_deterministic():
+    rng = np.random.default_rng(3)
+    lens = rng.integers(0, 40000, 200)
+    a = plan_tables(desc(batch=200), lens)
+    b = plan_tables(desc(batch=200), lens)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def _status(d, lens, cus=256):
+    out = ctypes.c_void_p()
+    arr = None if lens is None else np.asarray(lens, np.int32)
+    ptr = None if arr is None else arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    st = N.lib().laminar_plan_create(None if d is None else ctypes.byref(d),
+                                     ptr, cus, ctypes.byref(out))
+    if out.value:
+        N.laminar_plan_destroy(out.value)
+    return st
+
+
+def test_planner_argument_errors():
+    INV, UNS = N.LAMINAR_ERR_INVALID_ARG, N.LAMINAR_ERR_UNSUPPORTED
+    assert _status(None, [1]) == INV
+    assert _status(desc(batch=1), None) == INV
+    assert _status(desc(batch=1), [1], cus=0) == INV
+    assert _status(desc(batch=1), [-1]) == INV
+    assert _status(desc(batch=1, max_blocks=2), [33]) == INV
+    assert _status(desc(batch=1, max_blocks=3), [33]) == N.LAMINAR_OK
+    assert _status(desc(batch=1, hq=30, hkv=4), [5]) == INV
+    assert _status(desc(batch=1, kv=N.LAMINAR_KV_FP8_E4M3FN), [5]) == INV
+    assert _status(desc(batch=1, kv=7), [5]) == INV
+    assert _status(desc(batch=1, scale=0.0), [5]) == INV
+    assert _status(desc(batch=1, waves=3), [5]) == INV
+    assert _status(desc(batch=1, ppi=-1), [5]) == INV
+    assert _status(desc(batch=1, pages=0), [5]) == INV
+    assert _status(desc(batch=1, page_size=32), [5]) == UNS
+    assert _status(desc(batch=1, d=96), [5]) == UNS
+    assert _status(desc(batch=1, hq=34, hkv=2), [5]) == UNS
+    st = N.lib().laminar_plan_create(ctypes.byref(desc(batch=1)),
+                                     np.asarray([5], np.int32).ctypes.data_as(
+                                         ctypes.POINTER(ctypes.c_int32)), 256,
+                                     None)
+    assert st == INV
+
+
+def test_call_errors_before_any_launch():
+    lib = N.lib()
+    assert lib.laminar_decode_attn(None, *([None] * 7), None) == \
+        N.LAMINAR_ERR_INVALID_ARG
+    assert lib.laminar_decode_attn_merge(None, None, None, None) == \
+        N.LAMINAR_ERR_INVALID_ARG
+    assert lib.laminar_plan_bind_workspace(None, None, 0, None) == \
+        N.LAMINAR_ERR_INVALID_ARG
+    p = N.laminar_plan_create(desc(batch=2), np.array([40, 9], np.int32), 256)
+    try:
+        # unbound plan
+        assert lib.laminar_decode_attn(p, 16, 16, 16, 16, 16, 16, 16, None) == \
+            N.LAMINAR_ERR_WORKSPACE
+        assert lib.laminar_decode_attn_partial(p, 16, 16, 16, 16, 16, 16, 16,
+                                               None) == N.LAMINAR_ERR_WORKSPACE
+        # too small / misaligned workspace
+        need = N.laminar_plan_workspace_bytes(p)
+        assert lib.laminar_plan_bind_workspace(p, 256, need - 1, None) == \
+            N.LAMINAR_ERR_WORKSPACE
+        assert lib.laminar_plan_bind_workspace(p, 257, need, None) == \
+            N.LAMINAR_ERR_WORKSPACE
+        assert lib.laminar_plan_bind_workspace(p, None, need, None) == \
+            N.LAMINAR_ERR_WORKSPACE
+    finally:
+        N.laminar_plan_destroy(p)
+    assert lib.laminar_hbm_read(None, 16, None, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert lib.laminar_hbm_read(16, 17, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert lib.laminar_hbm_copy(16, 16, 8, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert lib.laminar_plan_num_items(None) == -1
+    assert lib.laminar_plan_workspace_bytes(None) == 0
+
+
+def test_planner_under_address_and_ub_sanitizers(tmp_path):
+    gxx = shutil.which("g++")
+    if not gxx:
+        pytest.skip("g++ not available")
+    exe = tmp_path / "plan_check"
+    src = os.path.join(ROOT, "tests", "plan_check.cpp")
+    plan = os.path.join(ROOT, "paper_2510_12633_amd", "csrc", "plan.cpp")
+    cmd = [gxx, "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=all", "-I", os.path.join(ROOT, "include"),
+           "-I", os.path.dirname(plan), src, plan, "-o", str(exe)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    env = dict(os.environ,
+               ASAN_OPTIONS="detect_leaks=1:verify_asan_link_order=0",
+               UBSAN_OPTIONS="print_stacktrace=1")
+    r = subprocess.run([str(exe)], capture_output=True, text=True, env=env,
+                       timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "plan_check OK" in r.stdout
