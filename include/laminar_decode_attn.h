@@ -118,10 +118,12 @@ size_t laminar_plan_workspace_bytes(const laminar_plan* plan);
 /*
  * Bind a caller-owned device workspace of `bytes` >= workspace_bytes, 256-byte
  * aligned, and enqueue the upload of the plan's work and merge lists into it
- * on `stream`. The lists are first copied into a pinned host staging slot of
- * the library (one small ring per device, allocated on first use and kept
- * until the process exits), so the upload does not wait for earlier work on
- * the stream and the plan may be destroyed as soon as this call returns.
+ * on `stream`. The lists are first copied into a pinned, device-mapped host
+ * staging slot of the library (one small ring per device, allocated on first
+ * use and kept until the process exits) and a small kernel on `stream`
+ * copies them into the workspace, so the upload neither waits for earlier
+ * work on the stream nor crosses to a DMA engine, and the plan may be
+ * destroyed as soon as this call returns.
  * Lists larger than one staging slot (1 MiB, about 65k work items) are
  * copied directly and the call waits for `stream` to finish the copy.
  * The workspace must stay allocated, and must not be used by anything else,

@@ -666,16 +666,29 @@ bool inputs_ok(const laminar_plan* p, const void* q, const void* k_pages,
   return q && k_pages && v_pages && block_table && seq_lens && out && lse;
 }
 
-// Pinned staging for plan uploads. A copy from pageable memory can block
-// the host until the stream drains; copying the tables into one of a few
-// pinned slots first keeps the upload asynchronous and lets the caller free
-// the plan as soon as bind returns. One ring per device, created on first
-// use and kept for the life of the process; a slot is reused only after
-// the event recorded behind its last upload has completed.
+// Pinned staging for plan uploads. The tables are copied into one of a few
+// pinned, device-mapped host slots, and a small kernel on the caller's
+// stream copies them into the workspace. Compared with a DMA copy this keeps
+// the upload on the same hardware queue as the attention kernels (no
+// cross-engine hand-offs around it), never blocks the host on earlier work,
+// and lets the caller free the plan as soon as bind returns. One ring per
+// device, created on first use and kept for the life of the process; a slot
+// is reused only after the event recorded behind its last upload completed.
+// Copies n16 16-byte words from device-mapped pinned host memory.
+__global__ void __launch_bounds__(256)
+upload_kernel(u32x4* __restrict__ dst, const u32x4* __restrict__ src,
+              size_t n16) {
+  const size_t stride = size_t(gridDim.x) * blockDim.x;
+  for (size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n16;
+       i += stride)
+    dst[i] = src[i];
+}
+
 struct StagingRing {
   static constexpr int kSlots = 8;
   static constexpr size_t kSlotBytes = size_t(1) << 20;
   char* host = nullptr;
+  char* dev_view = nullptr;    // device address of `host`
   hipEvent_t done[kSlots] = {};
   bool pending[kSlots] = {};
   int next = 0;
@@ -700,9 +713,13 @@ laminar_status upload_tables(void* dst, const void* src, size_t bytes,
   StagingRing& ring = g_rings[dev];
   if (!ring.host) {
     void* h = nullptr;
+    void* hd = nullptr;
     if (hipHostMalloc(&h, StagingRing::kSlots * StagingRing::kSlotBytes,
-                      hipHostMallocDefault) != hipSuccess)
+                      hipHostMallocMapped | hipHostMallocPortable) !=
+            hipSuccess ||
+        hipHostGetDevicePointer(&hd, h, 0) != hipSuccess)
       return LAMINAR_ERR_HIP;
+    ring.dev_view = static_cast<char*>(hd);
     for (int i = 0; i < StagingRing::kSlots; ++i)
       if (hipEventCreateWithFlags(&ring.done[i], hipEventDisableTiming) !=
           hipSuccess)
@@ -715,8 +732,14 @@ laminar_status upload_tables(void* dst, const void* src, size_t bytes,
     return LAMINAR_ERR_HIP;
   char* stage = ring.host + size_t(slot) * StagingRing::kSlotBytes;
   std::memcpy(stage, src, bytes);
-  if (hipMemcpyAsync(dst, stage, bytes, hipMemcpyHostToDevice, stream) !=
-          hipSuccess ||
+  const size_t n16 = (bytes + 15) / 16;    // tables are 256-byte multiples
+  const unsigned blocks = unsigned(n16 < 64 * 256 ? (n16 + 255) / 256 : 64);
+  hipLaunchKernelGGL(upload_kernel, dim3(blocks), dim3(256), 0, stream,
+                     static_cast<u32x4*>(dst),
+                     reinterpret_cast<const u32x4*>(
+                         ring.dev_view + size_t(slot) * StagingRing::kSlotBytes),
+                     n16);
+  if (hipGetLastError() != hipSuccess ||
       hipEventRecord(ring.done[slot], stream) != hipSuccess)
     return LAMINAR_ERR_HIP;
   ring.pending[slot] = true;

@@ -81,7 +81,8 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
     // item gets at least one pair of pages.
     const int64_t slots = int64_t(num_cus) *
         std::max(1, laminar_detail::kResidentWavesPerCU / p->waves);
-    const int64_t target = slots * laminar_detail::kItemsPerSlot;
+    const int64_t target = slots * laminar_detail::kItemsPerSlotNum /
+                           laminar_detail::kItemsPerSlotDen;
     const int64_t step = 2 * int64_t(p->waves);
     chunk = std::max<int64_t>(step, (work + target - 1) / target);
     chunk = (chunk + step - 1) / step * step;

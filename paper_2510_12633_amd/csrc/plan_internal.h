@@ -31,8 +31,12 @@ namespace laminar_detail {
 // Wavefronts resident per CU that the automatic split assumes for one item
 // of one wavefront (two per SIMD with ~200 VGPRs per lane).
 constexpr int kResidentWavesPerCU = 8;
-// Work items per resident slot the automatic split aims for, so that the
-// longest-first order leaves little tail imbalance.
-constexpr int kItemsPerSlot = 3;
+// Work items per resident slot the automatic split aims for, as a ratio
+// kItemsPerSlotNum / kItemsPerSlotDen. Each item costs about one chain of
+// dependent memory latencies to start, so fewer, larger items are faster
+// until the longest-first order can no longer even out the tail; 1.5 was
+// the measured sweet spot on the 7B and post-repack workloads.
+constexpr int kItemsPerSlotNum = 3;
+constexpr int kItemsPerSlotDen = 2;
 constexpr int kDefaultWaves = 4;
 }  // namespace laminar_detail
