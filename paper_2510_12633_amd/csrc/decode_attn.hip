@@ -39,7 +39,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
+constexpr double kLn2d = 0.6931471805599453;
 
 struct DecodeArgs {
   const uint16_t* q;
@@ -55,6 +55,7 @@ struct DecodeArgs {
   float* lse_part;
   const int4* items;
   const int4* merges;
+  const int32_t* wave_items;  // persistent schedule: item range of each wave
   int32_t hq, hkv, group, max_blocks, num_pages;
   float scale_log2;  // softmax_scale * log2(e)
   float scale;       // softmax_scale
@@ -188,257 +189,236 @@ __device__ __forceinline__ void zero_tail_v(u32x4* v, int nv, int gq) {
   }
 }
 
-template <int D, bool FP8, int WAVES>
-__global__ void __launch_bounds__(64 * WAVES)
-__attribute__((amdgpu_waves_per_eu(2)))
-decode_partial(const DecodeArgs a) {
+// Wave-uniform description of one work item.
+struct ItemCtx {
+  int b, kvh, len, p0, npages, slot;
+};
+
+__device__ __forceinline__ ItemCtx read_item(const DecodeArgs& a, int idx) {
+  const int4 it = a.items[idx];
+  ItemCtx c;
+  c.b = it.x / a.hkv;
+  c.kvh = it.x - c.b * a.hkv;
+  c.len = a.seq_lens[c.b];
+  c.p0 = it.y;
+  c.npages = max(min(it.z, (c.len + 15) >> 4) - c.p0, 0);
+  c.slot = it.w;
+  return c;
+}
+
+// Block-table entries of pages w*64 .. w*64+63 of the item, one per lane
+// (-1 beyond the item).
+__device__ __forceinline__ int load_window(const DecodeArgs& a,
+                                           const ItemCtx& c, int w, int lane) {
+  const int j = w * 64 + lane;
+  return j < c.npages
+             ? a.block_table[size_t(c.b) * a.max_blocks + c.p0 + j]
+             : -1;
+}
+
+// Query fragment (B operand of QK^T): lane holds head r16 of the group,
+// dims (gq*KK + kk)*8 .. +7 for each step kk. Heads beyond the group are 0.
+template <int D, bool FP8>
+__device__ __forceinline__ void load_q(const DecodeArgs& a, const ItemCtx& c,
+                                       int r16, int gq,
+                                       bf16x8 (&qf)[Geo<D, FP8>::KK]) {
   using G = Geo<D, FP8>;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int r16 = lane & 15, gq = lane >> 4;
-
-  const int4 it = a.items[blockIdx.x];
-  const int unit = it.x;
-  const int b = unit / a.hkv;
-  const int kvh = unit - b * a.hkv;
-  const int len = a.seq_lens[b];
-  const int p0 = it.y;
-  const int p1 = min(it.z, (len + 15) >> 4);
-  const int npages = max(p1 - p0, 0);
-  const int npairs = (npages + 1) >> 1;
-
-  // Query fragment (B operand of QK^T): lane holds head r16 of the group,
-  // dims (gq*KK + kk)*8 .. +7 for each step kk. Heads beyond the group are 0.
   const bool head_ok = r16 < a.group;
-  const int h = kvh * a.group + r16;
-  bf16x8 qf[G::KK];
-  {
-    const u32x4* qp = reinterpret_cast<const u32x4*>(
-        a.q + (size_t(b) * a.hq + (head_ok ? h : 0)) * D) + gq * G::KK;
+  const int h = c.kvh * a.group + r16;
+  const u32x4* qp = reinterpret_cast<const u32x4*>(
+      a.q + (size_t(c.b) * a.hq + (head_ok ? h : 0)) * D) + gq * G::KK;
 #pragma unroll
-    for (int kk = 0; kk < G::KK; ++kk) {
-      const u32x4 v = head_ok ? qp[kk] : u4(0, 0, 0, 0);
-      qf[kk] = __builtin_bit_cast(bf16x8, v);
-    }
+  for (int kk = 0; kk < G::KK; ++kk) {
+    const u32x4 v = head_ok ? qp[kk] : u4(0, 0, 0, 0);
+    qf[kk] = __builtin_bit_cast(bf16x8, v);
   }
+}
 
-  f32x4 acc[G::NT];
-#pragma unroll
-  for (int n = 0; n < G::NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY;   // running max of raw scores, per head r16
-  float l_run = 0.f;         // this lane's share of the softmax denominator
-
+// Issue the loads of pages ja and ja+1 of the item (ja even; btv is the
+// block-table window holding them). Pages past the item, or whose table
+// entry lies outside the pool, get no valid tokens and read page 0.
+template <int D, bool FP8>
+__device__ __forceinline__ void issue_pair(const DecodeArgs& a,
+                                           const ItemCtx& c, int ja, int btv,
+                                           int koff, int voff,
+                                           PairRegs<D, FP8>& pr) {
+  using G = Geo<D, FP8>;
+  const bool has_b = ja + 1 < c.npages;
+  int ppa = __builtin_amdgcn_readlane(btv, ja & 63);
+  int ppb = has_b ? __builtin_amdgcn_readlane(btv, (ja + 1) & 63) : ppa;
+  const int base_tok = (c.p0 + ja) * 16;
+  int nva = min(16, c.len - base_tok);
+  int nvb = has_b ? min(16, c.len - base_tok - 16) : 0;
+  if (ppa < 0 || ppa >= a.num_pages) { ppa = 0; nva = 0; }
+  if (ppb < 0 || ppb >= a.num_pages) { ppb = 0; nvb = 0; }
+  pr.nva = nva;
+  pr.nvb = nvb;
   const size_t page_stride = size_t(a.hkv) * G::TILE;
-  const uint8_t* kbase = a.k_pages + size_t(kvh) * G::TILE;
-  const uint8_t* vbase = a.v_pages + size_t(kvh) * G::TILE;
-  const int32_t* bt = a.block_table + size_t(b) * a.max_blocks + p0;
-  const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
-  const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
+  const uint8_t* kbase = a.k_pages + size_t(c.kvh) * G::TILE;
+  const uint8_t* vbase = a.v_pages + size_t(c.kvh) * G::TILE;
+  const u32x4* ka = reinterpret_cast<const u32x4*>(kbase + size_t(ppa) * page_stride);
+  const u32x4* kb = reinterpret_cast<const u32x4*>(kbase + size_t(ppb) * page_stride);
+  const u32x4* va = reinterpret_cast<const u32x4*>(vbase + size_t(ppa) * page_stride);
+  const u32x4* vb = reinterpret_cast<const u32x4*>(vbase + size_t(ppb) * page_stride);
+  // KV pages are streamed once per call: non-temporal loads keep them from
+  // displacing reusable lines in L2 and the Infinity Cache.
+#pragma unroll
+  for (int j = 0; j < G::KL; ++j)
+    pr.ka[j] = __builtin_nontemporal_load(&ka[koff + j * 16]);
+#pragma unroll
+  for (int j = 0; j < G::KL; ++j)
+    pr.kb[j] = __builtin_nontemporal_load(&kb[koff + j * 16]);
+#pragma unroll
+  for (int j = 0; j < G::VL; ++j)
+    pr.va[j] = __builtin_nontemporal_load(&va[voff + j * 16]);
+#pragma unroll
+  for (int j = 0; j < G::VL; ++j)
+    pr.vb[j] = __builtin_nontemporal_load(&vb[voff + j * 16]);
+  if constexpr (FP8) {
+    pr.ksa = a.k_scale[size_t(ppa) * a.hkv + c.kvh];
+    pr.ksb = a.k_scale[size_t(ppb) * a.hkv + c.kvh];
+    pr.vsa = a.v_scale[size_t(ppa) * a.hkv + c.kvh];
+    pr.vsb = a.v_scale[size_t(ppb) * a.hkv + c.kvh];
+  }
+}
 
-  // Block-table entries of this item, 64 pages per window, one per lane.
-  int win = -1;
-  int btv = -1;
+// Running softmax state of the wave for the g heads of one item: lane
+// (head r16, group gq) holds the running max of head r16 (identical across
+// groups) as mc = max(score) * scale * log2(e) rounded once, its share of
+// the denominator sum(exp2(score * scale * log2(e) - mc)), and output rows
+// 4gq..4gq+3 of every 16-dim tile. Keeping the rounded mc itself makes the
+// rescale factor exp2(mc_old - mc_new) exactly 1 while the max is unchanged
+// (no drift over thousands of pages) and lets lse = mc * ln 2 + ln(l) use
+// the very offset the exponentials used. The denominator is a long sum of
+// positive terms, so it is carried in fp64.
+template <int D>
+struct Acc {
+  f32x4 o[D / 16];
+  float m;     // mc, in log2 units; -inf before the first valid token
+  double l;
+  __device__ __forceinline__ void reset() {
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n) o[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m = -INFINITY;
+    l = 0.f;
+  }
+};
 
-  auto load_pair = [&](PairRegs<D, FP8>& pr, int jp) {
-    const int ja = 2 * jp;                       // page index within item
-    const int w = ja >> 6;
-    if (w != win) {
-      const int j = w * 64 + lane;
-      btv = j < npages ? bt[j] : -1;
-      win = w;
-    }
-    const bool has_b = ja + 1 < npages;
-    int ppa = __builtin_amdgcn_readlane(btv, ja & 63);
-    int ppb = has_b ? __builtin_amdgcn_readlane(btv, (ja + 1) & 63) : ppa;
-    const int base_tok = (p0 + ja) * 16;
-    int nva = min(16, len - base_tok);
-    int nvb = has_b ? min(16, len - base_tok - 16) : 0;
-    if (ppa < 0 || ppa >= a.num_pages) { ppa = 0; nva = 0; }
-    if (ppb < 0 || ppb >= a.num_pages) { ppb = 0; nvb = 0; }
-    pr.nva = nva;
-    pr.nvb = nvb;
-    const u32x4* ka = reinterpret_cast<const u32x4*>(kbase + size_t(ppa) * page_stride);
-    const u32x4* kb = reinterpret_cast<const u32x4*>(kbase + size_t(ppb) * page_stride);
-    const u32x4* va = reinterpret_cast<const u32x4*>(vbase + size_t(ppa) * page_stride);
-    const u32x4* vb = reinterpret_cast<const u32x4*>(vbase + size_t(ppb) * page_stride);
-    // KV pages are streamed once per call: non-temporal loads keep them
-    // from displacing reusable lines in L2 and the Infinity Cache.
+template <int D, bool FP8>
+__device__ __forceinline__ void compute_pair(const DecodeArgs& a,
+                                             const bf16x8 (&qf)[Geo<D, FP8>::KK],
+                                             PairRegs<D, FP8>& pr, Acc<D>& st,
+                                             int gq) {
+  using G = Geo<D, FP8>;
+  // Scores S^T[token][head] of both pages: lane holds head r16, tokens
+  // 4gq..4gq+3 of page A (sa) and of page B (sb).
+  f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < G::KL; ++j)
-      pr.ka[j] = __builtin_nontemporal_load(&ka[koff + j * 16]);
-#pragma unroll
-    for (int j = 0; j < G::KL; ++j)
-      pr.kb[j] = __builtin_nontemporal_load(&kb[koff + j * 16]);
-#pragma unroll
-    for (int j = 0; j < G::VL; ++j)
-      pr.va[j] = __builtin_nontemporal_load(&va[voff + j * 16]);
-#pragma unroll
-    for (int j = 0; j < G::VL; ++j)
-      pr.vb[j] = __builtin_nontemporal_load(&vb[voff + j * 16]);
-    if constexpr (FP8) {
-      pr.ksa = a.k_scale[size_t(ppa) * a.hkv + kvh];
-      pr.ksb = a.k_scale[size_t(ppb) * a.hkv + kvh];
-      pr.vsa = a.v_scale[size_t(ppa) * a.hkv + kvh];
-      pr.vsb = a.v_scale[size_t(ppb) * a.hkv + kvh];
-    }
-  };
-
-  auto compute_pair = [&](PairRegs<D, FP8>& pr) {
-    // Scores S^T[token][head] of both pages: lane holds head r16, tokens
-    // 4gq..4gq+3 of page A (sa) and of page B (sb).
-    f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < G::KK; ++kk) {
-      sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_frag<D, FP8>(pr.ka, kk),
-                                                   qf[kk], sa, 0, 0, 0);
-      sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_frag<D, FP8>(pr.kb, kk),
-                                                   qf[kk], sb, 0, 0, 0);
-    }
-    if constexpr (FP8) {
-      sa *= pr.ksa;
-      sb *= pr.ksb;
-    }
-    if (pr.nva < 16 || pr.nvb < 16) {          // uniform: only at the tail
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        sa[r] = (4 * gq + r < pr.nva) ? sa[r] : -INFINITY;
-        sb[r] = (4 * gq + r < pr.nvb) ? sb[r] : -INFINITY;
-      }
-      zero_tail_v<D, FP8>(pr.va, pr.nva, gq);
-      zero_tail_v<D, FP8>(pr.vb, pr.nvb, gq);
-    }
-    float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])),
-                     fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float mc = (m_new == -INFINITY) ? 0.f : m_new * a.scale_log2;
-    const float alpha = __builtin_amdgcn_exp2f(m_run * a.scale_log2 - mc);
-    m_run = m_new;
-    float pa[4], pb[4];
+  for (int kk = 0; kk < G::KK; ++kk) {
+    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_frag<D, FP8>(pr.ka, kk),
+                                                 qf[kk], sa, 0, 0, 0);
+    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_frag<D, FP8>(pr.kb, kk),
+                                                 qf[kk], sb, 0, 0, 0);
+  }
+  if constexpr (FP8) {
+    sa *= pr.ksa;
+    sb *= pr.ksb;
+  }
+  if (pr.nva < 16 || pr.nvb < 16) {            // uniform: only at the tail
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      pa[r] = __builtin_amdgcn_exp2f(fmaf(sa[r], a.scale_log2, -mc));
-      pb[r] = __builtin_amdgcn_exp2f(fmaf(sb[r], a.scale_log2, -mc));
+      sa[r] = (4 * gq + r < pr.nva) ? sa[r] : -INFINITY;
+      sb[r] = (4 * gq + r < pr.nvb) ? sb[r] : -INFINITY;
     }
-    l_run = fmaf(l_run, alpha, ((pa[0] + pa[1]) + (pa[2] + pa[3])) +
-                                   ((pb[0] + pb[1]) + (pb[2] + pb[3])));
-#pragma unroll
-    for (int n = 0; n < G::NT; ++n) acc[n] *= alpha;
-    if constexpr (FP8) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        pa[r] *= pr.vsa;
-        pb[r] *= pr.vsb;
-      }
-    }
-    // P^T as B operand: lane holds head r16, slots 8gq+e = token 4gq+e of
-    // page A (e < 4) and of page B (e >= 4); P = hi + lo in bf16.
-    const uint32_t h0 = pack_bf16(pa[0], pa[1]), h1 = pack_bf16(pa[2], pa[3]);
-    const uint32_t h2 = pack_bf16(pb[0], pb[1]), h3 = pack_bf16(pb[2], pb[3]);
-    const uint32_t l0 = pack_bf16(pa[0] - bf16_lo_f(h0), pa[1] - bf16_hi_f(h0));
-    const uint32_t l1 = pack_bf16(pa[2] - bf16_lo_f(h1), pa[3] - bf16_hi_f(h1));
-    const uint32_t l2 = pack_bf16(pb[0] - bf16_lo_f(h2), pb[1] - bf16_hi_f(h2));
-    const uint32_t l3 = pack_bf16(pb[2] - bf16_lo_f(h3), pb[3] - bf16_hi_f(h3));
-    if constexpr (!FP8) {
-      // bf16 V: one 16x16x16 product per page, its A operand (dim row
-      // r16*NT + n, tokens 4gq..4gq+3) is two of the loaded registers.
-      const s16x4 pha = s4(h0, h1), pla = s4(l0, l1);
-      const s16x4 phb = s4(h2, h3), plb = s4(l2, l3);
-#pragma unroll
-      for (int n = 0; n < G::NT; ++n) {
-        const s16x4 vta = s4(word(pr.va, 2 * n), word(pr.va, 2 * n + 1));
-        const s16x4 vtb = s4(word(pr.vb, 2 * n), word(pr.vb, 2 * n + 1));
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vta, pha, acc[n], 0, 0, 0);
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vta, pla, acc[n], 0, 0, 0);
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vtb, phb, acc[n], 0, 0, 0);
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vtb, plb, acc[n], 0, 0, 0);
-      }
-    } else {
-      // fp8 V: the converted registers form one 16x16x32 operand per tile,
-      // tokens of page A in items 0-3 and of page B in items 4-7.
-      const bf16x8 phi = __builtin_bit_cast(bf16x8, u4(h0, h1, h2, h3));
-      const bf16x8 plo = __builtin_bit_cast(bf16x8, u4(l0, l1, l2, l3));
-#pragma unroll
-      for (int n = 0; n < G::NT; ++n) {
-        const bf16x8 vt = v_frag<D, FP8>(pr.va, pr.vb, n);
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, phi, acc[n], 0, 0, 0);
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, plo, acc[n], 0, 0, 0);
-      }
-    }
-  };
-
-  // Pairs wave, wave + WAVES, ...; the next pair's loads are issued before
-  // the current pair is computed.
-  PairRegs<D, FP8> buf0, buf1;
-  int jp = wave;
-  if (jp < npairs) load_pair(buf0, jp);
-  while (jp < npairs) {
-    int jn = jp + WAVES;
-    if (jn < npairs) load_pair(buf1, jn);
-    compute_pair(buf0);
-    jp = jn;
-    if (jp >= npairs) break;
-    jn = jp + WAVES;
-    if (jn < npairs) load_pair(buf0, jn);
-    compute_pair(buf1);
-    jp = jn;
+    zero_tail_v<D, FP8>(pr.va, pr.nva, gq);
+    zero_tail_v<D, FP8>(pr.vb, pr.nvb, gq);
   }
-
-  // Full softmax denominator of head r16 over this wave's pages.
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
-
-  if constexpr (WAVES > 1) {
-    __shared__ float sm_m[WAVES][16];
-    __shared__ float sm_l[WAVES][16];
-    __shared__ float sm_acc[WAVES - 1][G::NT * 4][64];
-    if (wave > 0) {
-      if (gq == 0) {
-        sm_m[wave][r16] = m_run;
-        sm_l[wave][r16] = l_run;
-      }
+  float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])),
+                   fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float mc_new = fmaxf(st.m, mx * a.scale_log2);   // -inf stays -inf
+  const float alpha = (st.m == -INFINITY)
+                          ? 0.f
+                          : __builtin_amdgcn_exp2f(st.m - mc_new);
+  const float mc = (mc_new == -INFINITY) ? 0.f : mc_new;
+  st.m = mc_new;
+  float pa[4], pb[4];
 #pragma unroll
-      for (int n = 0; n < G::NT; ++n)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sm_acc[wave - 1][n * 4 + r][lane] = acc[n][r];
-    }
-    __syncthreads();
-    if (wave > 0) return;
-    float m_all = m_run;
-#pragma unroll
-    for (int w = 1; w < WAVES; ++w) m_all = fmaxf(m_all, sm_m[w][r16]);
-    const float mc = (m_all == -INFINITY) ? 0.f : m_all * a.scale_log2;
-    const float f0 = __builtin_amdgcn_exp2f(m_run * a.scale_log2 - mc);
-    l_run *= f0;
-#pragma unroll
-    for (int n = 0; n < G::NT; ++n) acc[n] *= f0;
-#pragma unroll
-    for (int w = 1; w < WAVES; ++w) {
-      const float fw = __builtin_amdgcn_exp2f(sm_m[w][r16] * a.scale_log2 - mc);
-      l_run = fmaf(sm_l[w][r16], fw, l_run);
-#pragma unroll
-      for (int n = 0; n < G::NT; ++n)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          acc[n][r] = fmaf(sm_acc[w - 1][n * 4 + r][lane], fw, acc[n][r]);
-    }
-    m_run = m_all;
+  for (int r = 0; r < 4; ++r) {
+    pa[r] = __builtin_amdgcn_exp2f(fmaf(sa[r], a.scale_log2, -mc));
+    pb[r] = __builtin_amdgcn_exp2f(fmaf(sb[r], a.scale_log2, -mc));
   }
+  st.l = fma(st.l, double(alpha),
+             double(((pa[0] + pa[1]) + (pa[2] + pa[3])) +
+                    ((pb[0] + pb[1]) + (pb[2] + pb[3]))));
+#pragma unroll
+  for (int n = 0; n < G::NT; ++n) st.o[n] *= alpha;
+  if constexpr (FP8) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      pa[r] *= pr.vsa;
+      pb[r] *= pr.vsb;
+    }
+  }
+  // P^T as B operand: lane holds head r16, slots 8gq+e = token 4gq+e of
+  // page A (e < 4) and of page B (e >= 4); P = hi + lo in bf16.
+  const uint32_t h0 = pack_bf16(pa[0], pa[1]), h1 = pack_bf16(pa[2], pa[3]);
+  const uint32_t h2 = pack_bf16(pb[0], pb[1]), h3 = pack_bf16(pb[2], pb[3]);
+  const uint32_t l0 = pack_bf16(pa[0] - bf16_lo_f(h0), pa[1] - bf16_hi_f(h0));
+  const uint32_t l1 = pack_bf16(pa[2] - bf16_lo_f(h1), pa[3] - bf16_hi_f(h1));
+  const uint32_t l2 = pack_bf16(pb[0] - bf16_lo_f(h2), pb[1] - bf16_hi_f(h2));
+  const uint32_t l3 = pack_bf16(pb[2] - bf16_lo_f(h3), pb[3] - bf16_hi_f(h3));
+  if constexpr (!FP8) {
+    // bf16 V: one 16x16x16 product per page; its A operand (tile row r16,
+    // tokens 4gq..4gq+3) is two of the loaded registers.
+    const s16x4 pha = s4(h0, h1), pla = s4(l0, l1);
+    const s16x4 phb = s4(h2, h3), plb = s4(l2, l3);
+#pragma unroll
+    for (int n = 0; n < G::NT; ++n) {
+      const s16x4 vta = s4(word(pr.va, 2 * n), word(pr.va, 2 * n + 1));
+      const s16x4 vtb = s4(word(pr.vb, 2 * n), word(pr.vb, 2 * n + 1));
+      st.o[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vta, pha, st.o[n], 0, 0, 0);
+      st.o[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vta, pla, st.o[n], 0, 0, 0);
+      st.o[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vtb, phb, st.o[n], 0, 0, 0);
+      st.o[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vtb, plb, st.o[n], 0, 0, 0);
+    }
+  } else {
+    // fp8 V: the converted registers form one 16x16x32 operand per tile,
+    // tokens of page A in items 0-3 and of page B in items 4-7.
+    const bf16x8 phi = __builtin_bit_cast(bf16x8, u4(h0, h1, h2, h3));
+    const bf16x8 plo = __builtin_bit_cast(bf16x8, u4(l0, l1, l2, l3));
+#pragma unroll
+    for (int n = 0; n < G::NT; ++n) {
+      const bf16x8 vt = v_frag<D, FP8>(pr.va, pr.vb, n);
+      st.o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, phi, st.o[n], 0, 0, 0);
+      st.o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, plo, st.o[n], 0, 0, 0);
+    }
+  }
+}
 
-  if (!head_ok) return;
-  const bool empty = !(l_run > 0.f);
-  const float inv = empty ? 0.f : 1.0f / l_run;
-  const float lse_v = empty ? -INFINITY
-                            : m_run * a.scale + __builtin_amdgcn_logf(l_run) * kLn2;
+// Write the item's result: out/lse directly when the trajectory was not
+// split, else the partial record of its slot. st.l must already hold the
+// full denominator of head r16.
+template <int D, bool FP8>
+__device__ __forceinline__ void write_item(const DecodeArgs& a,
+                                           const ItemCtx& c, const Acc<D>& st,
+                                           int r16, int gq) {
+  using G = Geo<D, FP8>;
+  if (r16 >= a.group) return;
+  const int h = c.kvh * a.group + r16;
+  const bool empty = !(st.l > 0.0);
+  const float inv = empty ? 0.f : float(1.0 / st.l);
+  const float lse_v =
+      empty ? -INFINITY : float(double(st.m) * kLn2d + log(st.l));
   float* dst;
   float* lse_dst;
-  if (it.w < 0) {
-    dst = a.out + (size_t(b) * a.hq + h) * D;
-    lse_dst = a.lse + size_t(b) * a.hq + h;
+  if (c.slot < 0) {
+    dst = a.out + (size_t(c.b) * a.hq + h) * D;
+    lse_dst = a.lse + size_t(c.b) * a.hq + h;
   } else {
-    dst = a.o_part + (size_t(it.w) * a.group + r16) * D;
-    lse_dst = a.lse_part + size_t(it.w) * a.group + r16;
+    dst = a.o_part + (size_t(c.slot) * a.group + r16) * D;
+    lse_dst = a.lse_part + size_t(c.slot) * a.group + r16;
   }
   // Row 4gq + r of tile n is dim vdim(n, 4gq + r): for each load j the lane
   // holds 4*DPL contiguous dims starting at j*16*DPL + 4gq*DPL, ordered
@@ -450,7 +430,7 @@ decode_partial(const DecodeArgs a) {
     for (int r = 0; r < 4; ++r)
 #pragma unroll
       for (int e = 0; e < G::DPL; ++e)
-        vals[r * G::DPL + e] = acc[j * G::DPL + e][r] * inv;
+        vals[r * G::DPL + e] = st.o[j * G::DPL + e][r] * inv;
     float4* run = reinterpret_cast<float4*>(dst + G::vdim(j * G::DPL, 4 * gq));
 #pragma unroll
     for (int k = 0; k < G::DPL; ++k)
@@ -458,6 +438,178 @@ decode_partial(const DecodeArgs a) {
                            vals[4 * k + 3]);
   }
   if (gq == 0) *lse_dst = lse_v;
+}
+
+// Schedule "one workgroup per item": WAVES wavefronts share the item's page
+// pairs (wave w takes pairs w, w+WAVES, ...) and are combined through LDS.
+template <int D, bool FP8, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
+__attribute__((amdgpu_waves_per_eu(2)))
+decode_partial(const DecodeArgs a) {
+  using G = Geo<D, FP8>;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, gq = lane >> 4;
+  const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
+  const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
+
+  const ItemCtx c = read_item(a, blockIdx.x);
+  const int npairs = (c.npages + 1) >> 1;
+  bf16x8 qf[G::KK];
+  load_q<D, FP8>(a, c, r16, gq, qf);
+  Acc<D> st;
+  st.reset();
+
+  int win = -1, btv = -1;
+  auto issue = [&](PairRegs<D, FP8>& pr, int jp) {
+    const int ja = 2 * jp;
+    if ((ja >> 6) != win) {
+      win = ja >> 6;
+      btv = load_window(a, c, win, lane);
+    }
+    issue_pair<D, FP8>(a, c, ja, btv, koff, voff, pr);
+  };
+
+  // The next pair's loads are issued before the current pair is computed.
+  PairRegs<D, FP8> buf0, buf1;
+  int jp = wave;
+  if (jp < npairs) issue(buf0, jp);
+  while (jp < npairs) {
+    int jn = jp + WAVES;
+    if (jn < npairs) issue(buf1, jn);
+    compute_pair<D, FP8>(a, qf, buf0, st, gq);
+    jp = jn;
+    if (jp >= npairs) break;
+    jn = jp + WAVES;
+    if (jn < npairs) issue(buf0, jn);
+    compute_pair<D, FP8>(a, qf, buf1, st, gq);
+    jp = jn;
+  }
+
+  // Full softmax denominator of head r16 over this wave's pages.
+  st.l += __shfl_xor(st.l, 16);
+  st.l += __shfl_xor(st.l, 32);
+
+  if constexpr (WAVES > 1) {
+    __shared__ float sm_m[WAVES][16];
+    __shared__ double sm_l[WAVES][16];
+    __shared__ float sm_acc[WAVES - 1][G::NT * 4][64];
+    if (wave > 0) {
+      if (gq == 0) {
+        sm_m[wave][r16] = st.m;
+        sm_l[wave][r16] = st.l;
+      }
+#pragma unroll
+      for (int n = 0; n < G::NT; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sm_acc[wave - 1][n * 4 + r][lane] = st.o[n][r];
+    }
+    __syncthreads();
+    if (wave > 0) return;
+    float m_all = st.m;
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) m_all = fmaxf(m_all, sm_m[w][r16]);
+    const float mref = (m_all == -INFINITY) ? 0.f : m_all;
+    const float f0 = __builtin_amdgcn_exp2f(st.m - mref);   // 0 for -inf
+    st.l *= double(f0);
+#pragma unroll
+    for (int n = 0; n < G::NT; ++n) st.o[n] *= f0;
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) {
+      const float fw = __builtin_amdgcn_exp2f(sm_m[w][r16] - mref);
+      st.l = fma(sm_l[w][r16], double(fw), st.l);
+#pragma unroll
+      for (int n = 0; n < G::NT; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          st.o[n][r] = fmaf(sm_acc[w - 1][n * 4 + r][lane], fw, st.o[n][r]);
+    }
+    st.m = m_all;
+  }
+  write_item<D, FP8>(a, c, st, r16, gq);
+}
+
+// Schedule "persistent wavefronts": one wavefront per workgroup walks the
+// list of items the host assigned to it (longest-processing-time order).
+// While it works on one item it already holds the next item's record,
+// length and first block-table window, and it issues the next item's first
+// page pair and query before computing the current item's last pair, so
+// consecutive items stream without a start-up gap.
+template <int D, bool FP8>
+__global__ void __launch_bounds__(64)
+__attribute__((amdgpu_waves_per_eu(2)))
+decode_persistent(const DecodeArgs a) {
+  using G = Geo<D, FP8>;
+  const int lane = threadIdx.x;
+  const int r16 = lane & 15, gq = lane >> 4;
+  const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
+  const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
+  const int first = a.wave_items[blockIdx.x];
+  const int last = a.wave_items[blockIdx.x + 1];
+  if (first >= last) return;
+
+  int k = first;
+  ItemCtx cur = read_item(a, k);
+  int win = 0;
+  int btv = load_window(a, cur, 0, lane);
+  bf16x8 qf[G::KK], qn[G::KK];
+  load_q<D, FP8>(a, cur, r16, gq, qf);
+  bool has_nxt = k + 1 < last;
+  ItemCtx nxt = cur;
+  int btv_n = -1;
+  if (has_nxt) {
+    nxt = read_item(a, k + 1);
+    btv_n = load_window(a, nxt, 0, lane);
+  }
+  Acc<D> st;
+  st.reset();
+  int jp = 0;
+
+  // One step: compute pair jp of `cur` (held in A) after issuing the next
+  // pair, of `cur` or of the next item, into B. Returns false when done.
+  auto step = [&](PairRegs<D, FP8>& A, PairRegs<D, FP8>& B) -> bool {
+    const int npairs = (cur.npages + 1) >> 1;
+    const bool more = jp + 1 < npairs;
+    if (more) {
+      const int ja = 2 * (jp + 1);
+      if ((ja >> 6) != win) {
+        win = ja >> 6;
+        btv = load_window(a, cur, win, lane);
+      }
+      issue_pair<D, FP8>(a, cur, ja, btv, koff, voff, B);
+    } else if (has_nxt && nxt.npages > 0) {
+      issue_pair<D, FP8>(a, nxt, 0, btv_n, koff, voff, B);
+      load_q<D, FP8>(a, nxt, r16, gq, qn);
+    }
+    if (npairs > 0) compute_pair<D, FP8>(a, qf, A, st, gq);
+    if (more) {
+      ++jp;
+      return true;
+    }
+    st.l += __shfl_xor(st.l, 16);
+    st.l += __shfl_xor(st.l, 32);
+    write_item<D, FP8>(a, cur, st, r16, gq);
+    if (!has_nxt) return false;
+    ++k;
+    cur = nxt;
+    btv = btv_n;
+    win = 0;
+#pragma unroll
+    for (int kk = 0; kk < G::KK; ++kk) qf[kk] = qn[kk];
+    has_nxt = k + 1 < last;
+    if (has_nxt) {
+      nxt = read_item(a, k + 1);
+      btv_n = load_window(a, nxt, 0, lane);
+    }
+    st.reset();
+    jp = 0;
+    return true;
+  };
+
+  PairRegs<D, FP8> buf0, buf1;
+  if (cur.npages > 0) issue_pair<D, FP8>(a, cur, 0, btv, koff, voff, buf0);
+  while (step(buf0, buf1) && step(buf1, buf0)) {
+  }
 }
 
 // Block-wide reductions for 256 threads.
@@ -583,6 +735,11 @@ unsigned calib_grid(size_t n16) {
 template <int D, bool FP8>
 hipError_t launch_partial(const laminar_plan* p, const DecodeArgs& a,
                           hipStream_t stream) {
+  if (p->schedule == LAMINAR_SCHEDULE_PERSISTENT) {
+    hipLaunchKernelGGL((decode_persistent<D, FP8>), dim3(p->num_lists),
+                       dim3(64), 0, stream, a);
+    return hipGetLastError();
+  }
   const dim3 grid(p->num_items);
   switch (p->waves) {
     case 1:
@@ -615,6 +772,7 @@ DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
   a.lse = lse;
   a.items = reinterpret_cast<const int4*>(ws + p->off_items);
   a.merges = reinterpret_cast<const int4*>(ws + p->off_merges);
+  a.wave_items = reinterpret_cast<const int32_t*>(ws + p->off_lists);
   a.lse_part = reinterpret_cast<float*>(ws + p->off_lse);
   a.o_part = reinterpret_cast<float*>(ws + p->off_o);
   a.hq = d.num_q_heads;

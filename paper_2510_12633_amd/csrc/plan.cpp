@@ -10,8 +10,11 @@
 
 #include <algorithm>
 #include <cstring>
+#include <functional>
 #include <new>
 #include <numeric>
+#include <queue>
+#include <utility>
 
 #include "plan_internal.h"
 
@@ -31,6 +34,12 @@ laminar_status validate(const laminar_attn_desc* d, const int32_t* lens,
   if (d->pages_per_item < 0) return LAMINAR_ERR_INVALID_ARG;
   if (d->waves_per_item != 0 && d->waves_per_item != 1 &&
       d->waves_per_item != 2 && d->waves_per_item != 4)
+    return LAMINAR_ERR_INVALID_ARG;
+  if (d->schedule != LAMINAR_SCHEDULE_AUTO &&
+      d->schedule != LAMINAR_SCHEDULE_PER_ITEM &&
+      d->schedule != LAMINAR_SCHEDULE_PERSISTENT)
+    return LAMINAR_ERR_INVALID_ARG;
+  if (d->schedule == LAMINAR_SCHEDULE_PERSISTENT && d->waves_per_item > 1)
     return LAMINAR_ERR_INVALID_ARG;
   if (d->kv_dtype != LAMINAR_KV_BF16 && d->kv_dtype != LAMINAR_KV_FP8_E4M3FN)
     return LAMINAR_ERR_INVALID_ARG;
@@ -65,8 +74,13 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   p->desc = *desc;
   const int32_t B = desc->batch, hkv = desc->num_kv_heads;
   p->group = desc->num_q_heads / hkv;
-  p->waves = desc->waves_per_item ? desc->waves_per_item
-                                  : laminar_detail::kDefaultWaves;
+  p->schedule = desc->schedule == LAMINAR_SCHEDULE_PERSISTENT
+                    ? LAMINAR_SCHEDULE_PERSISTENT
+                    : LAMINAR_SCHEDULE_PER_ITEM;
+  const bool persistent = p->schedule == LAMINAR_SCHEDULE_PERSISTENT;
+  p->waves = persistent ? 1
+                        : (desc->waves_per_item ? desc->waves_per_item
+                                                : laminar_detail::kDefaultWaves);
 
   // Total work in (page, kv-head) tiles.
   int64_t work = 0;
@@ -77,12 +91,16 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   if (desc->pages_per_item > 0) {
     chunk = desc->pages_per_item;
   } else {
-    // Aim for kItemsPerSlot items per resident item slot; every wave of an
-    // item gets at least one pair of pages.
+    // Aim for a fixed number of items per resident item slot (a workgroup,
+    // or a wavefront list); every wave of an item gets at least one pair
+    // of pages.
     const int64_t slots = int64_t(num_cus) *
         std::max(1, laminar_detail::kResidentWavesPerCU / p->waves);
-    const int64_t target = slots * laminar_detail::kItemsPerSlotNum /
-                           laminar_detail::kItemsPerSlotDen;
+    const int64_t target =
+        persistent ? slots * laminar_detail::kListItemsNum /
+                         laminar_detail::kListItemsDen
+                   : slots * laminar_detail::kItemsPerSlotNum /
+                         laminar_detail::kItemsPerSlotDen;
     const int64_t step = 2 * int64_t(p->waves);
     chunk = std::max<int64_t>(step, (work + target - 1) / target);
     chunk = (chunk + step - 1) / step * step;
@@ -122,6 +140,36 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
     return (a.p1 - a.p0) > (b.p1 - b.p0);
   });
 
+  // Persistent schedule: assign items, longest first, to the least loaded
+  // of num_lists wavefront lists (longest-processing-time greedy), then
+  // store each list's items contiguously in assignment order.
+  std::vector<int32_t> list_off;
+  if (persistent) {
+    const int64_t lists = std::max<int64_t>(
+        1, std::min<int64_t>(int64_t(num_cus) * laminar_detail::kResidentWavesPerCU,
+                             int64_t(items.size())));
+    p->num_lists = int32_t(lists);
+    using Load = std::pair<int64_t, int32_t>;   // (cost so far, list)
+    std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
+    for (int32_t w = 0; w < int32_t(lists); ++w) heap.push({0, w});
+    std::vector<int32_t> owner(items.size());
+    std::vector<int32_t> count(size_t(lists) + 1, 0);
+    for (size_t i = 0; i < items.size(); ++i) {
+      Load top = heap.top();
+      heap.pop();
+      owner[i] = top.second;
+      ++count[size_t(top.second) + 1];
+      top.first += (items[i].p1 - items[i].p0) + laminar_detail::kItemCostPages;
+      heap.push(top);
+    }
+    list_off.assign(size_t(lists) + 1, 0);
+    for (int64_t w = 0; w < lists; ++w) list_off[w + 1] = list_off[w] + count[w + 1];
+    std::vector<Item> grouped(items.size());
+    std::vector<int32_t> fill(list_off.begin(), list_off.end() - 1);
+    for (size_t i = 0; i < items.size(); ++i) grouped[fill[owner[i]]++] = items[i];
+    items.swap(grouped);
+  }
+
   p->num_items = int32_t(items.size());
   p->num_merges = int32_t(merges.size());
   p->num_slots = slots;
@@ -129,6 +177,8 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   size_t off = 0;
   p->off_items = off;
   off = align256(off + items.size() * 16);
+  p->off_lists = off;
+  off = align256(off + list_off.size() * sizeof(int32_t));
   p->off_merges = off;
   off = align256(off + merges.size() * 16);
   p->off_lse = off;
@@ -143,6 +193,9 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   if (!items.empty())
     std::memcpy(p->tables.data() + p->off_items / 4, items.data(),
                 items.size() * sizeof(Item));
+  if (!list_off.empty())
+    std::memcpy(p->tables.data() + p->off_lists / 4, list_off.data(),
+                list_off.size() * sizeof(int32_t));
   if (!merges.empty())
     std::memcpy(p->tables.data() + p->off_merges / 4, merges.data(),
                 merges.size() * sizeof(Item));
@@ -187,6 +240,23 @@ int32_t laminar_plan_merges_copy(const laminar_plan* plan, int32_t* dst,
   if (!plan || !dst || capacity < 0) return -1;
   const int32_t n = std::min(capacity, plan->num_merges);
   std::memcpy(dst, plan->tables.data() + plan->off_merges / 4, size_t(n) * 16);
+  return n;
+}
+
+int32_t laminar_plan_schedule(const laminar_plan* plan) {
+  return plan ? plan->schedule : -1;
+}
+
+int32_t laminar_plan_num_lists(const laminar_plan* plan) {
+  return plan ? plan->num_lists : -1;
+}
+
+int32_t laminar_plan_list_offsets_copy(const laminar_plan* plan, int32_t* dst,
+                                       int32_t capacity) {
+  if (!plan || !dst || capacity < 0) return -1;
+  const int32_t total = plan->num_lists > 0 ? plan->num_lists + 1 : 0;
+  const int32_t n = std::min(capacity, total);
+  std::memcpy(dst, plan->tables.data() + plan->off_lists / 4, size_t(n) * 4);
   return n;
 }
 

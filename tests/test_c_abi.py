@@ -23,21 +23,25 @@ def declared_functions():
 
 def desc(batch=4, hq=28, hkv=4, d=128, pages=10**6, max_blocks=8192,
          kv=N.LAMINAR_KV_BF16, scale=0.1, ppi=0, waves=0, k_scale=None,
-         v_scale=None, page_size=16):
+         v_scale=None, page_size=16, schedule=0):
     return N.LaminarAttnDesc(batch=batch, num_q_heads=hq, num_kv_heads=hkv,
                              head_dim=d, page_size=page_size, num_pages=pages,
                              max_blocks_per_seq=max_blocks, kv_dtype=kv,
                              softmax_scale=scale, k_scale=k_scale,
                              v_scale=v_scale, pages_per_item=ppi,
-                             waves_per_item=waves)
+                             waves_per_item=waves, schedule=schedule)
 
 
-def plan_tables(d, lens, cus=256):
+def plan_tables(d, lens, cus=256, lists=False):
     p = N.laminar_plan_create(d, np.asarray(lens, np.int32), cus)
     try:
-        return (N.laminar_plan_items_copy(p), N.laminar_plan_merges_copy(p),
-                N.laminar_plan_pages_per_item(p), N.laminar_plan_waves_per_item(p),
-                N.laminar_plan_workspace_bytes(p))
+        res = (N.laminar_plan_items_copy(p), N.laminar_plan_merges_copy(p),
+               N.laminar_plan_pages_per_item(p), N.laminar_plan_waves_per_item(p),
+               N.laminar_plan_workspace_bytes(p))
+        if lists:
+            res = res + (N.laminar_plan_schedule(p),
+                         N.laminar_plan_list_offsets_copy(p))
+        return res
     finally:
         N.laminar_plan_destroy(p)
 
@@ -62,7 +66,7 @@ def test_status_strings():
     assert N.laminar_status_string(99) == "unknown status"
 
 
-def check_plan(lens, hkv, items, merges, ppi):
+def check_plan(lens, hkv, items, merges, ppi, offsets=None):
     pages = -(-np.asarray(lens, np.int64) // 16)
     covered = {}
     by_unit = {}
@@ -78,8 +82,15 @@ def check_plan(lens, hkv, items, merges, ppi):
     # every (trajectory, kv-head, page) exactly once; empty units once
     assert len(covered) == int(pages.sum()) * hkv
     assert set(by_unit) == set(range(len(lens) * hkv))
-    sizes = [p1 - p0 for _, p0, p1, _ in items]
-    assert sizes == sorted(sizes, reverse=True)
+    sizes = [int(p1 - p0) for _, p0, p1, _ in items]
+    if offsets is None:                     # per-item schedule: longest first
+        assert sizes == sorted(sizes, reverse=True)
+    else:                                   # persistent: lists partition items
+        assert offsets[0] == 0 and offsets[-1] == len(items)
+        assert np.all(np.diff(offsets) >= 1)
+        for w in range(len(offsets) - 1):
+            part = sizes[offsets[w]:offsets[w + 1]]
+            assert part == sorted(part, reverse=True)
     merged = {int(m[0]): (int(m[1]), int(m[2])) for m in merges}
     assert len(merged) == len(merges)
     all_slots = []
@@ -106,14 +117,22 @@ def test_planner_invariants_random(seed):
     lens = np.minimum(np.exp(rng.normal(7, 1.5, b)).astype(np.int64), 70000)
     lens[rng.random(b) < 0.05] = 0
     hkv = int(rng.choice([1, 2, 4, 8]))
-    for ppi, waves in ((0, 0), (1, 1), (3, 2), (64, 4), (1 << 20, 0)):
+    for ppi, waves, sched in ((0, 0, 1), (1, 1, 1), (3, 2, 1), (64, 4, 1),
+                              (1 << 20, 0, 1), (0, 0, 0), (0, 0, 2), (1, 0, 2),
+                              (5, 1, 2), (1 << 20, 0, 2)):
         d = desc(batch=b, hq=hkv * int(rng.integers(1, 9)), hkv=hkv, ppi=ppi,
-                 waves=waves)
-        items, merges, chosen, w, ws = plan_tables(d, lens)
+                 waves=waves, schedule=sched)
+        items, merges, chosen, w, ws, got_sched, offs = plan_tables(
+            d, lens, lists=True)
         if ppi:
             assert chosen == ppi
-        assert w == (waves or 4)
-        check_plan(lens, hkv, items, merges, chosen)
+        if sched in (0, 1):
+            assert got_sched == 1 and w == (waves or 4) and len(offs) == 0
+            check_plan(lens, hkv, items, merges, chosen)
+        else:
+            assert got_sched == 2 and w == 1
+            assert len(offs) == min(256 * 8, len(items)) + 1
+            check_plan(lens, hkv, items, merges, chosen, offsets=offs)
         assert ws % 256 == 0 and ws >= 16 * (len(items) + len(merges))
 
 
@@ -121,17 +140,24 @@ def test_planner_auto_split_fills_the_gpu():
     """Eight 64k-token trajectories x 4 kv-heads (32 units) still give
     thousands of work items."""
     lens = [65536] * 8
-    items, merges, chosen, waves, _ = plan_tables(desc(batch=8), lens)
-    assert len(items) >= 1000 and len(merges) == 32
+    items, merges, chosen, waves, _ = plan_tables(desc(batch=8, schedule=1), lens)
+    assert len(items) >= 700 and len(merges) == 32
     assert chosen % (2 * waves) == 0
     check_plan(lens, 4, items, merges, chosen)
+    items, merges, chosen, _, _, _, offs = plan_tables(
+        desc(batch=8, schedule=2), lens, lists=True)
+    assert len(items) >= 2048 and len(offs) == 2049
+    check_plan(lens, 4, items, merges, chosen, offsets=offs)
 
 
 def test_planner_edge_lengths():
     for lens in ([0], [1], [16], [17], [0, 0, 0], [98304], [1, 98304, 0, 15]):
-        d = desc(batch=len(lens), hq=64, hkv=8)
-        items, merges, chosen, _, _ = plan_tables(d, lens)
-        check_plan(lens, 8, items, merges, chosen)
+        for sched in (1, 2):
+            d = desc(batch=len(lens), hq=64, hkv=8, schedule=sched)
+            items, merges, chosen, _, _, _, offs = plan_tables(d, lens,
+                                                               lists=True)
+            check_plan(lens, 8, items, merges, chosen,
+                       offsets=offs if sched == 2 else None)
     items, merges, _, _, _ = plan_tables(desc(batch=0), [])
     assert len(items) == 0 and len(merges) == 0
 
@@ -168,6 +194,10 @@ def test_planner_argument_errors():
     assert _status(desc(batch=1, kv=7), [5]) == INV
     assert _status(desc(batch=1, scale=0.0), [5]) == INV
     assert _status(desc(batch=1, waves=3), [5]) == INV
+    assert _status(desc(batch=1, waves=4, schedule=2), [5]) == INV
+    assert _status(desc(batch=1, waves=4, schedule=1), [5]) == N.LAMINAR_OK
+    assert _status(desc(batch=1, waves=4), [5]) == N.LAMINAR_OK
+    assert _status(desc(batch=1, schedule=3), [5]) == INV
     assert _status(desc(batch=1, ppi=-1), [5]) == INV
     assert _status(desc(batch=1, pages=0), [5]) == INV
     assert _status(desc(batch=1, page_size=32), [5]) == UNS
