@@ -47,6 +47,8 @@ def parse_args(argv=None):
     p.add_argument("--seed", type=int, default=None)
     p.add_argument("--waves-per-item", type=int, default=0)
     p.add_argument("--pages-per-item", type=int, default=0)
+    p.add_argument("--schedule", type=int, default=0,
+                   help="0 auto, 1 one piece per workgroup, 2 dynamic queue")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=15.0,
                    help="target seconds of oracle work for the CPU baseline")
@@ -223,7 +225,8 @@ def main(argv=None):
         kv_dtype=KV_DTYPES[cfg.kv_dtype], softmax_scale=wl.softmax_scale,
         k_scale=None if wl.k_scale is None else wl.k_scale.data_ptr(),
         v_scale=None if wl.v_scale is None else wl.v_scale.data_ptr(),
-        pages_per_item=args.pages_per_item, waves_per_item=args.waves_per_item)
+        pages_per_item=args.pages_per_item, waves_per_item=args.waves_per_item,
+        schedule=args.schedule)
     lens_host = np.ascontiguousarray(wl.seq_lens, dtype=np.int32)
 
     kv_bytes = wl.kv_bytes_unique()
@@ -244,6 +247,8 @@ def main(argv=None):
     n_merges = N.laminar_plan_num_merges(plan0)
     ppi = N.laminar_plan_pages_per_item(plan0)
     waves = N.laminar_plan_waves_per_item(plan0)
+    schedule = N.laminar_plan_schedule(plan0)
+    lists = N.laminar_plan_num_lists(plan0)
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
     N.laminar_plan_bind_workspace(plan0, ws, ws_bytes, sh)
 
@@ -344,6 +349,8 @@ def main(argv=None):
             "seed": wl.seed,
             "pages_per_item": ppi,
             "waves_per_item": waves,
+            "schedule": {1: "per_item", 2: "dynamic"}.get(schedule, schedule),
+            "workgroup_lists": lists,
             "work_items": n_items,
             "merged_units": n_merges,
             "plan_every_step": not args.fixed_plan,

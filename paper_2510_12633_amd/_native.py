@@ -25,7 +25,7 @@ LAMINAR_KV_FP8_E4M3FN = 1
 
 LAMINAR_SCHEDULE_AUTO = 0
 LAMINAR_SCHEDULE_PER_ITEM = 1
-LAMINAR_SCHEDULE_PERSISTENT = 2
+LAMINAR_SCHEDULE_DYNAMIC = 2
 
 
 class LaminarAttnDesc(ctypes.Structure):
@@ -214,7 +214,7 @@ def laminar_plan_num_lists(plan) -> int:
 
 def laminar_plan_list_offsets_copy(plan) -> np.ndarray:
     n = laminar_plan_num_lists(plan)
-    total = n + 1 if n > 0 else 0
+    total = n + 1
     buf = np.zeros(total, dtype=np.int32)
     got = lib().laminar_plan_list_offsets_copy(
         plan, buf.ctypes.data_as(POINTER(c_int32)), total)

@@ -4,10 +4,10 @@
 // dominate each decode step (§5.2), so the kernels below are organised around
 // streaming 16-token KV pages from HBM once:
 //
-//  * decode_partial: one workgroup per work item (trajectory, kv-head, page
-//    range) from the host plan. Each wavefront takes pairs of pages in turn
-//    and keeps the next pair's loads in flight while it computes the current
-//    one. Per pair it forms the scores of all g query heads of the GQA group
+//  * decode_queue / decode_lists: workgroups pull work items (trajectory,
+//    kv-head, page range) from a device-wide queue, or walk host-made lists
+//    of them. Each wavefront takes pairs of pages in turn and keeps the next
+//    pair's loads in flight while it computes the current one. Per pair it forms the scores of all g query heads of the GQA group
 //    with bf16 matrix-core products (v_mfma_f32_16x16x32_bf16: 16 tokens x
 //    16 head slots, head_dim as the reduction), updates an online softmax in
 //    fp32, and accumulates P*V on the matrix cores with P split into a bf16
@@ -55,7 +55,9 @@ struct DecodeArgs {
   float* lse_part;
   const int4* items;
   const int4* merges;
-  const int32_t* wave_items;  // persistent schedule: item range of each wave
+  const int32_t* lists;       // lists[w] .. lists[w+1]: items of workgroup w
+  int* queue;                 // dynamic schedule: next item to hand out
+  int32_t num_items;
   int32_t hq, hkv, group, max_blocks, num_pages;
   float scale_log2;  // softmax_scale * log2(e)
   float scale;       // softmax_scale
@@ -440,20 +442,19 @@ __device__ __forceinline__ void write_item(const DecodeArgs& a,
   if (gq == 0) *lse_dst = lse_v;
 }
 
-// Schedule "one workgroup per item": WAVES wavefronts share the item's page
-// pairs (wave w takes pairs w, w+WAVES, ...) and are combined through LDS.
+// One work item by the WAVES wavefronts of a workgroup: wave w takes page
+// pairs w, w+WAVES, ..., each keeping the next pair's loads in flight while
+// it computes the current one; the waves are combined through LDS at the
+// end and wave 0 writes the result. Every thread of the workgroup must call
+// it (it contains workgroup barriers when WAVES > 1).
 template <int D, bool FP8, int WAVES>
-__global__ void __launch_bounds__(64 * WAVES)
-__attribute__((amdgpu_waves_per_eu(2)))
-decode_partial(const DecodeArgs a) {
+__device__ __forceinline__ void process_item(const DecodeArgs& a, int k,
+                                             int lane, int wave) {
   using G = Geo<D, FP8>;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, gq = lane >> 4;
   const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
   const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
-
-  const ItemCtx c = read_item(a, blockIdx.x);
+  const ItemCtx c = read_item(a, k);
   const int npairs = (c.npages + 1) >> 1;
   bf16x8 qf[G::KK];
   load_q<D, FP8>(a, c, r16, gq, qf);
@@ -470,7 +471,6 @@ decode_partial(const DecodeArgs a) {
     issue_pair<D, FP8>(a, c, ja, btv, koff, voff, pr);
   };
 
-  // The next pair's loads are issued before the current pair is computed.
   PairRegs<D, FP8> buf0, buf1;
   int jp = wave;
   if (jp < npairs) issue(buf0, jp);
@@ -502,114 +502,84 @@ decode_partial(const DecodeArgs a) {
 #pragma unroll
       for (int n = 0; n < G::NT; ++n)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sm_acc[wave - 1][n * 4 + r][lane] = st.o[n][r];
+        for (int r = 0; r < 4; ++r)
+          sm_acc[wave - 1][n * 4 + r][lane] = st.o[n][r];
     }
     __syncthreads();
-    if (wave > 0) return;
-    float m_all = st.m;
+    if (wave == 0) {
+      float m_all = st.m;
 #pragma unroll
-    for (int w = 1; w < WAVES; ++w) m_all = fmaxf(m_all, sm_m[w][r16]);
-    const float mref = (m_all == -INFINITY) ? 0.f : m_all;
-    const float f0 = __builtin_amdgcn_exp2f(st.m - mref);   // 0 for -inf
-    st.l *= double(f0);
+      for (int w = 1; w < WAVES; ++w) m_all = fmaxf(m_all, sm_m[w][r16]);
+      const float mref = (m_all == -INFINITY) ? 0.f : m_all;
+      const float f0 = __builtin_amdgcn_exp2f(st.m - mref);   // 0 for -inf
+      st.l *= double(f0);
 #pragma unroll
-    for (int n = 0; n < G::NT; ++n) st.o[n] *= f0;
+      for (int n = 0; n < G::NT; ++n) st.o[n] *= f0;
 #pragma unroll
-    for (int w = 1; w < WAVES; ++w) {
-      const float fw = __builtin_amdgcn_exp2f(sm_m[w][r16] - mref);
-      st.l = fma(sm_l[w][r16], double(fw), st.l);
+      for (int w = 1; w < WAVES; ++w) {
+        const float fw = __builtin_amdgcn_exp2f(sm_m[w][r16] - mref);
+        st.l = fma(sm_l[w][r16], double(fw), st.l);
 #pragma unroll
-      for (int n = 0; n < G::NT; ++n)
+        for (int n = 0; n < G::NT; ++n)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          st.o[n][r] = fmaf(sm_acc[w - 1][n * 4 + r][lane], fw, st.o[n][r]);
+          for (int r = 0; r < 4; ++r)
+            st.o[n][r] = fmaf(sm_acc[w - 1][n * 4 + r][lane], fw, st.o[n][r]);
+      }
+      st.m = m_all;
     }
-    st.m = m_all;
+    __syncthreads();          // LDS is reused by the next item
+    if (wave == 0) write_item<D, FP8>(a, c, st, r16, gq);
+  } else {
+    write_item<D, FP8>(a, c, st, r16, gq);
   }
-  write_item<D, FP8>(a, c, st, r16, gq);
 }
 
-// Schedule "persistent wavefronts": one wavefront per workgroup walks the
-// list of items the host assigned to it (longest-processing-time order).
-// While it works on one item it already holds the next item's record,
-// length and first block-table window, and it issues the next item's first
-// page pair and query before computing the current item's last pair, so
-// consecutive items stream without a start-up gap.
-template <int D, bool FP8>
-__global__ void __launch_bounds__(64)
+// Static lists: workgroup w processes items lists[w] .. lists[w+1]-1.
+template <int D, bool FP8, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
 __attribute__((amdgpu_waves_per_eu(2)))
-decode_persistent(const DecodeArgs a) {
-  using G = Geo<D, FP8>;
-  const int lane = threadIdx.x;
-  const int r16 = lane & 15, gq = lane >> 4;
-  const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
-  const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
-  const int first = a.wave_items[blockIdx.x];
-  const int last = a.wave_items[blockIdx.x + 1];
-  if (first >= last) return;
+decode_lists(const DecodeArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int first = a.lists[blockIdx.x];
+  const int last = a.lists[blockIdx.x + 1];
+  for (int k = first; k < last; ++k) process_item<D, FP8, WAVES>(a, k, lane, wave);
+}
 
-  int k = first;
-  ItemCtx cur = read_item(a, k);
-  int win = 0;
-  int btv = load_window(a, cur, 0, lane);
-  bf16x8 qf[G::KK], qn[G::KK];
-  load_q<D, FP8>(a, cur, r16, gq, qf);
-  bool has_nxt = k + 1 < last;
-  ItemCtx nxt = cur;
-  int btv_n = -1;
-  if (has_nxt) {
-    nxt = read_item(a, k + 1);
-    btv_n = load_window(a, nxt, 0, lane);
+// Dynamic queue: resident workgroups pull item indices (longest first) from
+// a device-wide counter. Workgroups are dealt to the XCDs round-robin by
+// index, and the XCDs do not stream at the same speed, so any fixed split
+// leaves the kernel waiting for the slowest XCD; pulling lets the faster
+// ones take more items. Each workgroup asks for its next index before
+// working on the current one. Exactly one pull per workgroup comes back
+// past the end; the pull that returns num_items + gridDim.x - 1 is the
+// last one of the launch and resets the counter for the next launch.
+template <int D, bool FP8, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
+__attribute__((amdgpu_waves_per_eu(2)))
+decode_queue(const DecodeArgs a) {
+  __shared__ int s_idx;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n = a.num_items;
+  if (threadIdx.x == 0)
+    s_idx = __hip_atomic_fetch_add(a.queue, 1, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  int idx = s_idx;
+  while (idx < n) {
+    int nxt = 0;
+    if (threadIdx.x == 0)
+      nxt = __hip_atomic_fetch_add(a.queue, 1, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+    process_item<D, FP8, WAVES>(a, idx, lane, wave);
+    __syncthreads();          // every thread has read s_idx
+    if (threadIdx.x == 0) s_idx = nxt;
+    __syncthreads();
+    idx = s_idx;
   }
-  Acc<D> st;
-  st.reset();
-  int jp = 0;
-
-  // One step: compute pair jp of `cur` (held in A) after issuing the next
-  // pair, of `cur` or of the next item, into B. Returns false when done.
-  auto step = [&](PairRegs<D, FP8>& A, PairRegs<D, FP8>& B) -> bool {
-    const int npairs = (cur.npages + 1) >> 1;
-    const bool more = jp + 1 < npairs;
-    if (more) {
-      const int ja = 2 * (jp + 1);
-      if ((ja >> 6) != win) {
-        win = ja >> 6;
-        btv = load_window(a, cur, win, lane);
-      }
-      issue_pair<D, FP8>(a, cur, ja, btv, koff, voff, B);
-    } else if (has_nxt && nxt.npages > 0) {
-      issue_pair<D, FP8>(a, nxt, 0, btv_n, koff, voff, B);
-      load_q<D, FP8>(a, nxt, r16, gq, qn);
-    }
-    if (npairs > 0) compute_pair<D, FP8>(a, qf, A, st, gq);
-    if (more) {
-      ++jp;
-      return true;
-    }
-    st.l += __shfl_xor(st.l, 16);
-    st.l += __shfl_xor(st.l, 32);
-    write_item<D, FP8>(a, cur, st, r16, gq);
-    if (!has_nxt) return false;
-    ++k;
-    cur = nxt;
-    btv = btv_n;
-    win = 0;
-#pragma unroll
-    for (int kk = 0; kk < G::KK; ++kk) qf[kk] = qn[kk];
-    has_nxt = k + 1 < last;
-    if (has_nxt) {
-      nxt = read_item(a, k + 1);
-      btv_n = load_window(a, nxt, 0, lane);
-    }
-    st.reset();
-    jp = 0;
-    return true;
-  };
-
-  PairRegs<D, FP8> buf0, buf1;
-  if (cur.npages > 0) issue_pair<D, FP8>(a, cur, 0, btv, koff, voff, buf0);
-  while (step(buf0, buf1) && step(buf1, buf0)) {
-  }
+  if (threadIdx.x == 0 && idx == n + int(gridDim.x) - 1)
+    __hip_atomic_store(a.queue, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Block-wide reductions for 256 threads.
@@ -732,25 +702,24 @@ unsigned calib_grid(size_t n16) {
                                                    : size_t(kReadSinkFloats));
 }
 
+template <int D, bool FP8, int WAVES>
+void launch_waves(const laminar_plan* p, const DecodeArgs& a,
+                  hipStream_t stream) {
+  if (p->schedule == LAMINAR_SCHEDULE_DYNAMIC)
+    hipLaunchKernelGGL((decode_queue<D, FP8, WAVES>), dim3(p->grid),
+                       dim3(64 * WAVES), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_lists<D, FP8, WAVES>), dim3(p->grid),
+                       dim3(64 * WAVES), 0, stream, a);
+}
+
 template <int D, bool FP8>
 hipError_t launch_partial(const laminar_plan* p, const DecodeArgs& a,
                           hipStream_t stream) {
-  if (p->schedule == LAMINAR_SCHEDULE_PERSISTENT) {
-    hipLaunchKernelGGL((decode_persistent<D, FP8>), dim3(p->num_lists),
-                       dim3(64), 0, stream, a);
-    return hipGetLastError();
-  }
-  const dim3 grid(p->num_items);
   switch (p->waves) {
-    case 1:
-      hipLaunchKernelGGL((decode_partial<D, FP8, 1>), grid, dim3(64), 0, stream, a);
-      break;
-    case 2:
-      hipLaunchKernelGGL((decode_partial<D, FP8, 2>), grid, dim3(128), 0, stream, a);
-      break;
-    default:
-      hipLaunchKernelGGL((decode_partial<D, FP8, 4>), grid, dim3(256), 0, stream, a);
-      break;
+    case 1: launch_waves<D, FP8, 1>(p, a, stream); break;
+    case 2: launch_waves<D, FP8, 2>(p, a, stream); break;
+    default: launch_waves<D, FP8, 4>(p, a, stream); break;
   }
   return hipGetLastError();
 }
@@ -772,7 +741,9 @@ DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
   a.lse = lse;
   a.items = reinterpret_cast<const int4*>(ws + p->off_items);
   a.merges = reinterpret_cast<const int4*>(ws + p->off_merges);
-  a.wave_items = reinterpret_cast<const int32_t*>(ws + p->off_lists);
+  a.lists = reinterpret_cast<const int32_t*>(ws + p->off_lists);
+  a.queue = reinterpret_cast<int*>(ws + p->off_queue);
+  a.num_items = p->num_items;
   a.lse_part = reinterpret_cast<float*>(ws + p->off_lse);
   a.o_part = reinterpret_cast<float*>(ws + p->off_o);
   a.hq = d.num_q_heads;

@@ -13,7 +13,6 @@
 #include <functional>
 #include <new>
 #include <numeric>
-#include <queue>
 #include <utility>
 
 #include "plan_internal.h"
@@ -21,6 +20,9 @@
 namespace {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Piece { int32_t unit, p0, p1; };
+struct Item { int32_t unit, p0, p1, slot; };
 
 laminar_status validate(const laminar_attn_desc* d, const int32_t* lens,
                         int32_t num_cus) {
@@ -37,9 +39,7 @@ laminar_status validate(const laminar_attn_desc* d, const int32_t* lens,
     return LAMINAR_ERR_INVALID_ARG;
   if (d->schedule != LAMINAR_SCHEDULE_AUTO &&
       d->schedule != LAMINAR_SCHEDULE_PER_ITEM &&
-      d->schedule != LAMINAR_SCHEDULE_PERSISTENT)
-    return LAMINAR_ERR_INVALID_ARG;
-  if (d->schedule == LAMINAR_SCHEDULE_PERSISTENT && d->waves_per_item > 1)
+      d->schedule != LAMINAR_SCHEDULE_DYNAMIC)
     return LAMINAR_ERR_INVALID_ARG;
   if (d->kv_dtype != LAMINAR_KV_BF16 && d->kv_dtype != LAMINAR_KV_FP8_E4M3FN)
     return LAMINAR_ERR_INVALID_ARG;
@@ -74,101 +74,160 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   p->desc = *desc;
   const int32_t B = desc->batch, hkv = desc->num_kv_heads;
   p->group = desc->num_q_heads / hkv;
-  p->schedule = desc->schedule == LAMINAR_SCHEDULE_PERSISTENT
-                    ? LAMINAR_SCHEDULE_PERSISTENT
+  p->schedule = desc->schedule == LAMINAR_SCHEDULE_DYNAMIC
+                    ? LAMINAR_SCHEDULE_DYNAMIC
                     : LAMINAR_SCHEDULE_PER_ITEM;
-  const bool persistent = p->schedule == LAMINAR_SCHEDULE_PERSISTENT;
-  p->waves = persistent ? 1
-                        : (desc->waves_per_item ? desc->waves_per_item
-                                                : laminar_detail::kDefaultWaves);
-
-  // Total work in (page, kv-head) tiles.
-  int64_t work = 0;
+  p->waves = desc->waves_per_item ? desc->waves_per_item
+                                  : laminar_detail::kDefaultWaves;
+  const int64_t units = int64_t(B) * hkv;
+  std::vector<int64_t> upages(static_cast<size_t>(units), 0);
+  int64_t work = 0;                        // (page, kv-head) tiles
   for (int32_t b = 0; b < B; ++b)
-    work += ((int64_t(seq_lens_host[b]) + 15) / 16) * hkv;
-
-  int64_t chunk;
-  if (desc->pages_per_item > 0) {
-    chunk = desc->pages_per_item;
-  } else {
-    // Aim for a fixed number of items per resident item slot (a workgroup,
-    // or a wavefront list); every wave of an item gets at least one pair
-    // of pages.
-    const int64_t slots = int64_t(num_cus) *
-        std::max(1, laminar_detail::kResidentWavesPerCU / p->waves);
-    const int64_t target =
-        persistent ? slots * laminar_detail::kListItemsNum /
-                         laminar_detail::kListItemsDen
-                   : slots * laminar_detail::kItemsPerSlotNum /
-                         laminar_detail::kItemsPerSlotDen;
-    const int64_t step = 2 * int64_t(p->waves);
-    chunk = std::max<int64_t>(step, (work + target - 1) / target);
-    chunk = (chunk + step - 1) / step * step;
-  }
-  p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
-
-  struct Item { int32_t unit, p0, p1, slot; };
-  std::vector<Item> items;
-  std::vector<Item> merges;   // (unit, slot0, n, 0)
-  items.reserve(size_t(B) * hkv);
-  int32_t slots = 0;
-  for (int32_t b = 0; b < B; ++b) {
-    const int64_t pages = (int64_t(seq_lens_host[b]) + 15) / 16;
     for (int32_t h = 0; h < hkv; ++h) {
-      const int32_t unit = b * hkv + h;
-      if (pages == 0) {              // writes out = 0, lse = -inf
-        items.push_back({unit, 0, 0, -1});
-        continue;
-      }
-      const int64_t n = (pages + chunk - 1) / chunk;
-      if (n == 1) {
-        items.push_back({unit, 0, int32_t(pages), -1});
-        continue;
-      }
+      upages[size_t(b) * hkv + h] = (int64_t(seq_lens_host[b]) + 15) / 16;
+      work += upages[size_t(b) * hkv + h];
+    }
+  const int64_t resident = int64_t(num_cus) *
+      std::max(1, laminar_detail::kResidentWavesPerCU / p->waves);
+  const int64_t step = 2 * int64_t(p->waves);   // one page pair per wave
+
+  // Pieces in launch order, grouped by list; list_off[l] .. list_off[l+1]
+  // are the pieces of list l.
+  std::vector<Piece> order;
+  std::vector<int32_t> list_off(1, 0);
+  order.reserve(size_t(units) + 1024);
+
+  if (p->schedule == LAMINAR_SCHEDULE_PER_ITEM) {
+    int64_t chunk;
+    if (desc->pages_per_item > 0) {
+      chunk = desc->pages_per_item;
+    } else {
+      const int64_t target = resident * laminar_detail::kItemsPerSlotNum /
+                             laminar_detail::kItemsPerSlotDen;
+      chunk = std::max<int64_t>(step, (work + target - 1) / target);
+      chunk = (chunk + step - 1) / step * step;
+    }
+    p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
+    for (int64_t u = 0; u < units; ++u) {
+      const int64_t pages = upages[size_t(u)];
+      const int64_t n = pages == 0 ? 1 : (pages + chunk - 1) / chunk;
       const int64_t base = pages / n, rem = pages % n;
       int64_t pos = 0;
-      merges.push_back({unit, slots, int32_t(n), 0});
       for (int64_t i = 0; i < n; ++i) {
         const int64_t sz = base + (i < rem ? 1 : 0);
-        items.push_back({unit, int32_t(pos), int32_t(pos + sz), slots++});
+        order.push_back({int32_t(u), int32_t(pos), int32_t(pos + sz)});
         pos += sz;
       }
     }
-  }
-  // Longest first; ties keep (trajectory, kv-head, page) order.
-  std::stable_sort(items.begin(), items.end(), [](const Item& a, const Item& b) {
-    return (a.p1 - a.p0) > (b.p1 - b.p0);
-  });
-
-  // Persistent schedule: assign items, longest first, to the least loaded
-  // of num_lists wavefront lists (longest-processing-time greedy), then
-  // store each list's items contiguously in assignment order.
-  std::vector<int32_t> list_off;
-  if (persistent) {
-    const int64_t lists = std::max<int64_t>(
-        1, std::min<int64_t>(int64_t(num_cus) * laminar_detail::kResidentWavesPerCU,
-                             int64_t(items.size())));
-    p->num_lists = int32_t(lists);
-    using Load = std::pair<int64_t, int32_t>;   // (cost so far, list)
-    std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
-    for (int32_t w = 0; w < int32_t(lists); ++w) heap.push({0, w});
-    std::vector<int32_t> owner(items.size());
-    std::vector<int32_t> count(size_t(lists) + 1, 0);
-    for (size_t i = 0; i < items.size(); ++i) {
-      Load top = heap.top();
-      heap.pop();
-      owner[i] = top.second;
-      ++count[size_t(top.second) + 1];
-      top.first += (items[i].p1 - items[i].p0) + laminar_detail::kItemCostPages;
-      heap.push(top);
+    // Longest first; ties keep (trajectory, kv-head, page) order. One
+    // piece per list: the hardware dispatcher hands them out greedily.
+    std::stable_sort(order.begin(), order.end(),
+                     [](const Piece& a, const Piece& b) {
+                       return (a.p1 - a.p0) > (b.p1 - b.p0);
+                     });
+    for (size_t i = 0; i < order.size(); ++i) list_off.push_back(int32_t(i + 1));
+  } else {
+    // Dynamic: pieces of about work / (kQueuePiecesPerWG * resident) pages,
+    // longest first, pulled from a device-wide queue by resident
+    // workgroups; the last kQueueTailNum / kQueueTailDen of the work (the
+    // smallest pieces) is re-cut into pieces of at most kQueueTailPages so
+    // the queue runs out on short items.
+    int64_t chunk;
+    if (desc->pages_per_item > 0) {
+      chunk = desc->pages_per_item;
+    } else {
+      const int64_t target = resident * laminar_detail::kQueuePiecesPerWG;
+      chunk = std::max<int64_t>(step, (work + target - 1) / target);
+      chunk = (chunk + step - 1) / step * step;
     }
-    list_off.assign(size_t(lists) + 1, 0);
-    for (int64_t w = 0; w < lists; ++w) list_off[w + 1] = list_off[w] + count[w + 1];
-    std::vector<Item> grouped(items.size());
-    std::vector<int32_t> fill(list_off.begin(), list_off.end() - 1);
-    for (size_t i = 0; i < items.size(); ++i) grouped[fill[owner[i]]++] = items[i];
-    items.swap(grouped);
+    p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
+    std::vector<Piece> big;
+    for (int64_t u = 0; u < units; ++u) {
+      const int64_t pages = upages[size_t(u)];
+      const int64_t n = pages == 0 ? 1 : (pages + chunk - 1) / chunk;
+      const int64_t base = pages / n, rem = pages % n;
+      int64_t pos = 0;
+      for (int64_t i = 0; i < n; ++i) {
+        const int64_t sz = base + (i < rem ? 1 : 0);
+        big.push_back({int32_t(u), int32_t(pos), int32_t(pos + sz)});
+        pos += sz;
+      }
+    }
+    std::stable_sort(big.begin(), big.end(), [](const Piece& a, const Piece& b) {
+      return (a.p1 - a.p0) > (b.p1 - b.p0);
+    });
+    const int64_t tail_work = work * laminar_detail::kQueueTailNum /
+                              laminar_detail::kQueueTailDen;
+    const int64_t tail_pages = std::min<int64_t>(
+        chunk, laminar_detail::kQueueTailPages);
+    size_t cut = big.size();
+    for (int64_t acc = 0; cut > 0 && acc + (big[cut - 1].p1 - big[cut - 1].p0) <= tail_work;) {
+      acc += big[cut - 1].p1 - big[cut - 1].p0;
+      --cut;
+    }
+    order.assign(big.begin(), big.begin() + int64_t(cut));
+    std::vector<Piece> tail;
+    for (size_t i = cut; i < big.size(); ++i) {
+      const Piece& pc = big[i];
+      const int64_t len = pc.p1 - pc.p0;
+      const int64_t n = len == 0 ? 1 : (len + tail_pages - 1) / tail_pages;
+      const int64_t base = len / n, rem = len % n;
+      int64_t pos = pc.p0;
+      for (int64_t j = 0; j < n; ++j) {
+        const int64_t sz = base + (j < rem ? 1 : 0);
+        tail.push_back({pc.unit, int32_t(pos), int32_t(pos + sz)});
+        pos += sz;
+      }
+    }
+    std::stable_sort(tail.begin(), tail.end(), [](const Piece& a, const Piece& b) {
+      return (a.p1 - a.p0) > (b.p1 - b.p0);
+    });
+    order.insert(order.end(), tail.begin(), tail.end());
+    list_off.push_back(int32_t(order.size()));   // one shared list
   }
+
+  // Partial slots: a unit cut into several pieces gets consecutive slots in
+  // page order and one merge record; a unit in one piece writes directly.
+  std::vector<int32_t> count(static_cast<size_t>(units), 0);
+  std::vector<int32_t> first_slot(static_cast<size_t>(units), -1);
+  for (const Piece& pc : order) ++count[size_t(pc.unit)];
+  std::vector<Item> merges;            // (unit, slot0, n, 0)
+  int32_t slots = 0;
+  for (int64_t u = 0; u < units; ++u)
+    if (count[size_t(u)] > 1) {
+      first_slot[size_t(u)] = slots;
+      merges.push_back({int32_t(u), slots, count[size_t(u)], 0});
+      slots += count[size_t(u)];
+    }
+  // Rank of each piece among its unit's pieces by first page.
+  std::vector<Item> items(order.size());
+  {
+    std::vector<std::vector<std::pair<int32_t, int32_t>>> per_unit;
+    std::vector<int32_t> split_index(static_cast<size_t>(units), -1);
+    for (size_t i = 0; i < order.size(); ++i) {
+      const Piece& pc = order[i];
+      items[i] = {pc.unit, pc.p0, pc.p1, -1};
+      if (count[size_t(pc.unit)] > 1) {
+        int32_t& si = split_index[size_t(pc.unit)];
+        if (si < 0) {
+          si = int32_t(per_unit.size());
+          per_unit.emplace_back();
+        }
+        per_unit[size_t(si)].push_back({pc.p0, int32_t(i)});
+      }
+    }
+    for (auto& v : per_unit) {
+      std::sort(v.begin(), v.end());
+      const int32_t unit = items[size_t(v[0].second)].unit;
+      for (size_t r = 0; r < v.size(); ++r)
+        items[size_t(v[r].second)].slot = first_slot[size_t(unit)] + int32_t(r);
+    }
+  }
+  p->num_lists = int32_t(list_off.size()) - 1;
+  p->grid = p->schedule == LAMINAR_SCHEDULE_DYNAMIC
+                ? int32_t(std::max<int64_t>(
+                      1, std::min<int64_t>(resident, int64_t(items.size()))))
+                : p->num_lists;
 
   p->num_items = int32_t(items.size());
   p->num_merges = int32_t(merges.size());
@@ -179,6 +238,8 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   off = align256(off + items.size() * 16);
   p->off_lists = off;
   off = align256(off + list_off.size() * sizeof(int32_t));
+  p->off_queue = off;                  // one int counter, zero in the image
+  off = align256(off + sizeof(int32_t));
   p->off_merges = off;
   off = align256(off + merges.size() * 16);
   p->off_lse = off;
@@ -254,7 +315,7 @@ int32_t laminar_plan_num_lists(const laminar_plan* plan) {
 int32_t laminar_plan_list_offsets_copy(const laminar_plan* plan, int32_t* dst,
                                        int32_t capacity) {
   if (!plan || !dst || capacity < 0) return -1;
-  const int32_t total = plan->num_lists > 0 ? plan->num_lists + 1 : 0;
+  const int32_t total = plan->num_lists + 1;
   const int32_t n = std::min(capacity, total);
   std::memcpy(dst, plan->tables.data() + plan->off_lists / 4, size_t(n) * 4);
   return n;

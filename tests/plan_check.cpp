@@ -27,7 +27,7 @@ static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves,
   d.kv_dtype = LAMINAR_KV_BF16;
   d.softmax_scale = 0.125f;
   d.pages_per_item = ppi;
-  d.waves_per_item = schedule == LAMINAR_SCHEDULE_PER_ITEM ? waves : 0;
+  d.waves_per_item = waves;
   d.schedule = schedule;
   laminar_plan* p = nullptr;
   if (laminar_plan_create(&d, lens.data(), 256, &p) != LAMINAR_OK || !p)
@@ -51,13 +51,16 @@ static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves,
     for (char c : v)
       if (!c) return fail("hole");
   const int lists = laminar_plan_num_lists(p);
-  if (lists > 0) {
+  if (lists >= 0) {
     std::vector<int32_t> off(size_t(lists) + 1);
     if (laminar_plan_list_offsets_copy(p, off.data(), lists + 1) != lists + 1)
       return fail("lists");
     if (off[0] != 0 || off[lists] != n) return fail("list range");
     for (int w = 0; w < lists; ++w)
       if (off[w + 1] <= off[w]) return fail("empty list");
+    if (lists == 0 && n != 0) return fail("items without lists");
+    if (laminar_plan_schedule(p) == LAMINAR_SCHEDULE_DYNAMIC && lists != 1)
+      return fail("dynamic plan with several lists");
   }
   const int m = laminar_plan_num_merges(p);
   std::vector<int32_t> merges(size_t(4) * (m > 0 ? m : 1));

@@ -66,7 +66,10 @@ def test_status_strings():
     assert N.laminar_status_string(99) == "unknown status"
 
 
-def check_plan(lens, hkv, items, merges, ppi, offsets=None):
+def check_plan(lens, hkv, items, merges, ppi, offsets=None, dynamic=False):
+    """Coverage, slot and ordering invariants of a plan. `offsets` are the
+    list offsets: per-item plans have one item per list, dynamic plans one
+    list (the queue) holding every item."""
     pages = -(-np.asarray(lens, np.int64) // 16)
     covered = {}
     by_unit = {}
@@ -82,21 +85,21 @@ def check_plan(lens, hkv, items, merges, ppi, offsets=None):
     # every (trajectory, kv-head, page) exactly once; empty units once
     assert len(covered) == int(pages.sum()) * hkv
     assert set(by_unit) == set(range(len(lens) * hkv))
-    sizes = [int(p1 - p0) for _, p0, p1, _ in items]
-    if offsets is None:                     # per-item schedule: longest first
-        assert sizes == sorted(sizes, reverse=True)
-    else:                                   # persistent: lists partition items
+    if offsets is not None:
         assert offsets[0] == 0 and offsets[-1] == len(items)
         assert np.all(np.diff(offsets) >= 1)
-        for w in range(len(offsets) - 1):
-            part = sizes[offsets[w]:offsets[w + 1]]
-            assert part == sorted(part, reverse=True)
+    sizes = [int(p1 - p0) for _, p0, p1, _ in items]
+    assert sizes == sorted(sizes, reverse=True)
+    if offsets is not None:
+        expect = [0, len(items)] if dynamic else np.arange(len(items) + 1)
+        assert np.array_equal(offsets, expect)
     merged = {int(m[0]): (int(m[1]), int(m[2])) for m in merges}
     assert len(merged) == len(merges)
     all_slots = []
     for unit, chunks in by_unit.items():
         sz = [p1 - p0 for p0, p1, _ in chunks]
-        assert max(sz) - min(sz) <= 1
+        if not dynamic:
+            assert max(sz) - min(sz) <= 1
         if len(chunks) == 1:
             assert chunks[0][2] == -1 and unit not in merged
         else:
@@ -118,22 +121,38 @@ def test_planner_invariants_random(seed):
     lens[rng.random(b) < 0.05] = 0
     hkv = int(rng.choice([1, 2, 4, 8]))
     for ppi, waves, sched in ((0, 0, 1), (1, 1, 1), (3, 2, 1), (64, 4, 1),
-                              (1 << 20, 0, 1), (0, 0, 0), (0, 0, 2), (1, 0, 2),
-                              (5, 1, 2), (1 << 20, 0, 2)):
+                              (1 << 20, 0, 1), (0, 0, 0), (0, 0, 2), (1, 1, 2),
+                              (5, 2, 2), (1 << 20, 4, 2)):
         d = desc(batch=b, hq=hkv * int(rng.integers(1, 9)), hkv=hkv, ppi=ppi,
                  waves=waves, schedule=sched)
         items, merges, chosen, w, ws, got_sched, offs = plan_tables(
             d, lens, lists=True)
         if ppi:
             assert chosen == ppi
+        assert w == (waves or 4)
         if sched in (0, 1):
-            assert got_sched == 1 and w == (waves or 4) and len(offs) == 0
-            check_plan(lens, hkv, items, merges, chosen)
-        else:
-            assert got_sched == 2 and w == 1
-            assert len(offs) == min(256 * 8, len(items)) + 1
+            assert got_sched == 1
             check_plan(lens, hkv, items, merges, chosen, offsets=offs)
+        else:
+            assert got_sched == 2
+            check_plan(lens, hkv, items, merges, chosen, offsets=offs,
+                       dynamic=True)
         assert ws % 256 == 0 and ws >= 16 * (len(items) + len(merges))
+
+
+def test_dynamic_queue_ends_on_small_pieces():
+    rng = np.random.default_rng(11)
+    lens = np.minimum(np.exp(rng.normal(7.6, 1.0, 256)).astype(np.int64), 32768)
+    d = desc(batch=256, hq=28, hkv=4, schedule=2)
+    items, merges, chosen, w, _, _, offs = plan_tables(d, lens, lists=True)
+    sizes = (items[:, 2] - items[:, 1]).astype(np.int64)
+    work = int((-(-lens // 16)).sum()) * 4
+    assert chosen % 8 == 0 and chosen >= -(-work // 1024)
+    # the smallest pieces, about the last eighth of the work, are <= 16 pages
+    tail = sizes[sizes <= 16]
+    assert np.all(sizes[len(sizes) - len(tail):] <= 16)
+    assert tail.sum() >= work // 8 - chosen
+    check_plan(lens, 4, items, merges, chosen, offsets=offs, dynamic=True)
 
 
 def test_planner_auto_split_fills_the_gpu():
@@ -146,8 +165,8 @@ def test_planner_auto_split_fills_the_gpu():
     check_plan(lens, 4, items, merges, chosen)
     items, merges, chosen, _, _, _, offs = plan_tables(
         desc(batch=8, schedule=2), lens, lists=True)
-    assert len(items) >= 2048 and len(offs) == 2049
-    check_plan(lens, 4, items, merges, chosen, offsets=offs)
+    assert len(items) >= 1024 and len(merges) == 32
+    check_plan(lens, 4, items, merges, chosen, offsets=offs, dynamic=True)
 
 
 def test_planner_edge_lengths():
@@ -156,8 +175,8 @@ def test_planner_edge_lengths():
             d = desc(batch=len(lens), hq=64, hkv=8, schedule=sched)
             items, merges, chosen, _, _, _, offs = plan_tables(d, lens,
                                                                lists=True)
-            check_plan(lens, 8, items, merges, chosen,
-                       offsets=offs if sched == 2 else None)
+            check_plan(lens, 8, items, merges, chosen, offsets=offs,
+                       dynamic=sched == 2)
     items, merges, _, _, _ = plan_tables(desc(batch=0), [])
     assert len(items) == 0 and len(merges) == 0
 
@@ -194,9 +213,8 @@ def test_planner_argument_errors():
     assert _status(desc(batch=1, kv=7), [5]) == INV
     assert _status(desc(batch=1, scale=0.0), [5]) == INV
     assert _status(desc(batch=1, waves=3), [5]) == INV
-    assert _status(desc(batch=1, waves=4, schedule=2), [5]) == INV
+    assert _status(desc(batch=1, waves=4, schedule=2), [5]) == N.LAMINAR_OK
     assert _status(desc(batch=1, waves=4, schedule=1), [5]) == N.LAMINAR_OK
-    assert _status(desc(batch=1, waves=4), [5]) == N.LAMINAR_OK
     assert _status(desc(batch=1, schedule=3), [5]) == INV
     assert _status(desc(batch=1, ppi=-1), [5]) == INV
     assert _status(desc(batch=1, pages=0), [5]) == INV

@@ -95,7 +95,7 @@ def test_tiny_config_all_outputs():
     ref = decode_attention_from_host(host_arrays(wl))
     for ppi in (0, 1, 4, 64):
         check(run_gpu(wl, pages_per_item=ppi, schedule=2), ref,
-              f"tiny persistent pages_per_item={ppi}")
+              f"tiny dynamic pages_per_item={ppi}")
         for waves in (1, 2, 4):
             check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves,
                           schedule=1), ref,
@@ -110,7 +110,7 @@ def test_custom_shapes(name, cfg):
     ref = decode_attention_from_host(host_arrays(wl), workers=4)
     for ppi in (0, 2, 5):
         check(run_gpu(wl, pages_per_item=ppi, schedule=2), ref,
-              f"{name} persistent pages_per_item={ppi}")
+              f"{name} dynamic pages_per_item={ppi}")
         for waves in (1, 4):
             check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves,
                           schedule=1), ref,
@@ -139,7 +139,8 @@ def test_no_rescale_drift_on_long_single_wave_items():
     wl = make_workload(custom_config([12000, 5000], 28, 4, 128), seed=5,
                        device="cuda")
     ro, rl = decode_attention_from_host(host_arrays(wl), workers=4)
-    for kw in (dict(schedule=1, waves_per_item=1), dict(schedule=2)):
+    for kw in (dict(schedule=1, waves_per_item=1),
+               dict(schedule=1, waves_per_item=4)):
         o, l = run_gpu(wl, pages_per_item=1 << 20, **kw)
         el = np.abs(l - rl).max()
         eo = np.abs(o - ro).max()
@@ -211,8 +212,7 @@ def test_single_long_trajectory():
     check(run_gpu(wl), ref, "B=1 n=98304 auto split")
     check(run_gpu(wl, pages_per_item=1 << 20, waves_per_item=4, schedule=1),
           ref, "B=1 n=98304 unsplit, 4 waves")
-    check(run_gpu(wl, pages_per_item=1 << 20, schedule=2), ref,
-          "B=1 n=98304 unsplit, persistent")
+    check(run_gpu(wl, schedule=2), ref, "B=1 n=98304 dynamic")
 
 
 def test_invalid_arguments_return_status():
