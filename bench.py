@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 METRIC = "decode-attn KV TB/s (fraction of HBM peak) + tokens/s at long-tail batch"
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
 DEFAULT_WORKLOAD = "7b_pre_repack"
-PARTIAL_KERNEL = "decode_partial"
+PARTIAL_KERNEL = "decode_items"
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2510_12633_amd", "csrc",
                              "decode_attn.hip")
@@ -47,8 +47,6 @@ def parse_args(argv=None):
     p.add_argument("--seed", type=int, default=None)
     p.add_argument("--waves-per-item", type=int, default=0)
     p.add_argument("--pages-per-item", type=int, default=0)
-    p.add_argument("--schedule", type=int, default=0,
-                   help="0 auto, 1 one piece per workgroup, 2 dynamic queue")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=15.0,
                    help="target seconds of oracle work for the CPU baseline")
@@ -225,8 +223,7 @@ def main(argv=None):
         kv_dtype=KV_DTYPES[cfg.kv_dtype], softmax_scale=wl.softmax_scale,
         k_scale=None if wl.k_scale is None else wl.k_scale.data_ptr(),
         v_scale=None if wl.v_scale is None else wl.v_scale.data_ptr(),
-        pages_per_item=args.pages_per_item, waves_per_item=args.waves_per_item,
-        schedule=args.schedule)
+        pages_per_item=args.pages_per_item, waves_per_item=args.waves_per_item)
     lens_host = np.ascontiguousarray(wl.seq_lens, dtype=np.int32)
 
     kv_bytes = wl.kv_bytes_unique()
@@ -247,8 +244,6 @@ def main(argv=None):
     n_merges = N.laminar_plan_num_merges(plan0)
     ppi = N.laminar_plan_pages_per_item(plan0)
     waves = N.laminar_plan_waves_per_item(plan0)
-    schedule = N.laminar_plan_schedule(plan0)
-    lists = N.laminar_plan_num_lists(plan0)
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
     N.laminar_plan_bind_workspace(plan0, ws, ws_bytes, sh)
 
@@ -349,8 +344,6 @@ def main(argv=None):
             "seed": wl.seed,
             "pages_per_item": ppi,
             "waves_per_item": waves,
-            "schedule": {1: "per_item", 2: "dynamic"}.get(schedule, schedule),
-            "workgroup_lists": lists,
             "work_items": n_items,
             "merged_units": n_merges,
             "plan_every_step": not args.fixed_plan,
@@ -361,7 +354,7 @@ def main(argv=None):
         "context_tokens_per_s": round(float(wl.seq_lens.sum()) / step_s, 1),
         "kv_bytes": kv_bytes,
         "algorithmic_bytes": alg_bytes,
-        "kernel_ms": {"decode_partial": round(k1_ms, 5),
+        "kernel_ms": {"decode_items": round(k1_ms, 5),
                       "decode_merge": round(k2_ms, 5)},
         "plan_host_ms": round(sum(plan_ns) / max(len(plan_ns), 1) / 1e6, 5)
         if plan_ns else None,

@@ -90,23 +90,7 @@ typedef struct {
                                   per work item (1 .. no split)              */
   int32_t waves_per_item;      /* 0: automatic (4); else 1, 2 or 4 wavefronts
                                   cooperate on one work item                 */
-  int32_t schedule;            /* laminar_schedule                           */
 } laminar_attn_desc;
-
-/* How work items are mapped onto the GPU. */
-typedef enum {
-  LAMINAR_SCHEDULE_AUTO = 0,        /* currently PER_ITEM (measured no slower) */
-  LAMINAR_SCHEDULE_PER_ITEM = 1,    /* near-equal pieces of at most
-                                       pages_per_item pages per trajectory and
-                                       kv-head, one workgroup each, longest
-                                       first                                   */
-  LAMINAR_SCHEDULE_DYNAMIC = 2      /* resident workgroups pull pieces, longest
-                                       first, from a device-wide queue (its
-                                       counter lives in the workspace and is
-                                       back at zero after every call); the
-                                       last eighth of the work is cut into
-                                       pieces of at most 16 pages            */
-} laminar_schedule;
 
 typedef struct laminar_plan laminar_plan;   /* opaque, host-owned */
 
@@ -122,7 +106,6 @@ typedef struct laminar_plan laminar_plan;   /* opaque, host-owned */
  * Errors: INVALID_ARG (NULL pointers, negative or inconsistent sizes, a
  * length needing more than max_blocks_per_seq pages, fp8 without scales),
  * UNSUPPORTED (head_dim not 64/128, group size above 16, page_size != 16).
- * An unknown schedule is INVALID_ARG.
  */
 laminar_status laminar_plan_create(const laminar_attn_desc* desc,
                                    const int32_t* seq_lens_host,
@@ -187,9 +170,8 @@ laminar_status laminar_decode_attn_partial(const laminar_plan* plan,
 laminar_status laminar_decode_attn_merge(const laminar_plan* plan, float* out,
                                          float* lse, hipStream_t stream);
 
-/* Plan introspection (host only). Items are listed in launch order,
- * grouped by list (list w owns items [offsets[w], offsets[w+1])). Each item
- * is 4 int32:
+/* Plan introspection (host only). Items are listed in launch order
+ * (longest first, one workgroup each). Each item is 4 int32:
  * (b * num_kv_heads + kvh, first page, end page, partial slot or -1 when the
  * item writes out/lse directly). Each merge is 4 int32: (unit, first slot,
  * number of slots, 0). *_copy writes min(count, capacity) records and returns
@@ -200,13 +182,6 @@ int32_t laminar_plan_pages_per_item(const laminar_plan* plan);
 int32_t laminar_plan_waves_per_item(const laminar_plan* plan);
 int32_t laminar_plan_items_copy(const laminar_plan* plan, int32_t* dst,
                                 int32_t capacity);
-int32_t laminar_plan_schedule(const laminar_plan* plan);
-/* Number of static lists of items (per-item schedule: one per item, one
- * workgroup each; dynamic: 1, the queue), and their num_lists + 1 item
- * offsets. */
-int32_t laminar_plan_num_lists(const laminar_plan* plan);
-int32_t laminar_plan_list_offsets_copy(const laminar_plan* plan, int32_t* dst,
-                                       int32_t capacity);
 int32_t laminar_plan_merges_copy(const laminar_plan* plan, int32_t* dst,
                                  int32_t capacity);
 

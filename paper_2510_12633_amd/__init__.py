@@ -11,9 +11,7 @@ from ._native import (LaminarAttnDesc, LaminarError, laminar_decode_attn,
                       laminar_hbm_copy, laminar_hbm_read,
                       laminar_hbm_read_sink_floats, laminar_plan_bind_workspace,
                       laminar_plan_create, laminar_plan_destroy,
-                      laminar_plan_items_copy, laminar_plan_list_offsets_copy,
-                      laminar_plan_merges_copy, laminar_plan_num_lists,
-                      laminar_plan_schedule,
+                      laminar_plan_items_copy, laminar_plan_merges_copy,
                       laminar_plan_num_items, laminar_plan_num_merges,
                       laminar_plan_pages_per_item, laminar_plan_waves_per_item,
                       laminar_plan_workspace_bytes, laminar_status_string)

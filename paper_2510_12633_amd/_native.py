@@ -23,10 +23,6 @@ LAMINAR_ERR_HIP = 4
 LAMINAR_KV_BF16 = 0
 LAMINAR_KV_FP8_E4M3FN = 1
 
-LAMINAR_SCHEDULE_AUTO = 0
-LAMINAR_SCHEDULE_PER_ITEM = 1
-LAMINAR_SCHEDULE_DYNAMIC = 2
-
 
 class LaminarAttnDesc(ctypes.Structure):
     _fields_ = [
@@ -43,7 +39,6 @@ class LaminarAttnDesc(ctypes.Structure):
         ("v_scale", c_void_p),
         ("pages_per_item", c_int32),
         ("waves_per_item", c_int32),
-        ("schedule", c_int32),
     ]
 
 
@@ -74,10 +69,6 @@ _SIGNATURES = {
     "laminar_plan_waves_per_item": (c_int32, [c_void_p]),
     "laminar_plan_items_copy": (c_int32, [c_void_p, POINTER(c_int32), c_int32]),
     "laminar_plan_merges_copy": (c_int32, [c_void_p, POINTER(c_int32), c_int32]),
-    "laminar_plan_schedule": (c_int32, [c_void_p]),
-    "laminar_plan_num_lists": (c_int32, [c_void_p]),
-    "laminar_plan_list_offsets_copy": (c_int32, [c_void_p, POINTER(c_int32),
-                                                 c_int32]),
     "laminar_plan_destroy": (None, [c_void_p]),
     "laminar_status_string": (ctypes.c_char_p, [c_int32]),
     "laminar_hbm_read_sink_floats": (c_int32, []),
@@ -201,24 +192,6 @@ def laminar_plan_merges_copy(plan) -> np.ndarray:
     got = lib().laminar_plan_merges_copy(
         plan, buf.ctypes.data_as(POINTER(c_int32)), n)
     assert got == n
-    return buf
-
-
-def laminar_plan_schedule(plan) -> int:
-    return int(lib().laminar_plan_schedule(plan))
-
-
-def laminar_plan_num_lists(plan) -> int:
-    return int(lib().laminar_plan_num_lists(plan))
-
-
-def laminar_plan_list_offsets_copy(plan) -> np.ndarray:
-    n = laminar_plan_num_lists(plan)
-    total = n + 1
-    buf = np.zeros(total, dtype=np.int32)
-    got = lib().laminar_plan_list_offsets_copy(
-        plan, buf.ctypes.data_as(POINTER(c_int32)), total)
-    assert got == total
     return buf
 
 

@@ -40,8 +40,7 @@ class PagedDecodeAttention:
                  k_scale: Optional[torch.Tensor] = None,
                  v_scale: Optional[torch.Tensor] = None,
                  pages_per_item: int = 0, waves_per_item: int = 0,
-                 schedule: int = 0, cus: Optional[int] = None, device="cuda",
-                 stream=None):
+                 cus: Optional[int] = None, device="cuda", stream=None):
         self.desc = N.LaminarAttnDesc(
             batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
             head_dim=head_dim, page_size=16, num_pages=num_pages,
@@ -49,8 +48,7 @@ class PagedDecodeAttention:
             kv_dtype=KV_DTYPES[kv_dtype], softmax_scale=softmax_scale,
             k_scale=None if k_scale is None else k_scale.data_ptr(),
             v_scale=None if v_scale is None else v_scale.data_ptr(),
-            pages_per_item=pages_per_item, waves_per_item=waves_per_item,
-            schedule=schedule)
+            pages_per_item=pages_per_item, waves_per_item=waves_per_item)
         self.device = torch.device(device)
         self._scales = (k_scale, v_scale)        # keep alive
         if cus is None:
@@ -111,13 +109,6 @@ class PagedDecodeAttention:
     @property
     def waves_per_item(self) -> int:
         return N.laminar_plan_waves_per_item(self.plan)
-
-    @property
-    def schedule(self) -> int:
-        return N.laminar_plan_schedule(self.plan)
-
-    def list_offsets(self) -> np.ndarray:
-        return N.laminar_plan_list_offsets_copy(self.plan)
 
     def items(self) -> np.ndarray:
         return N.laminar_plan_items_copy(self.plan)

@@ -4,10 +4,10 @@
 // dominate each decode step (§5.2), so the kernels below are organised around
 // streaming 16-token KV pages from HBM once:
 //
-//  * decode_queue / decode_lists: workgroups pull work items (trajectory,
-//    kv-head, page range) from a device-wide queue, or walk host-made lists
-//    of them. Each wavefront takes pairs of pages in turn and keeps the next
-//    pair's loads in flight while it computes the current one. Per pair it forms the scores of all g query heads of the GQA group
+//  * decode_items: one workgroup per work item (trajectory, kv-head, page
+//    range) of the host plan. Each wavefront takes pairs of pages in turn
+//    and keeps the next pair's loads in flight while it computes the current
+//    one. Per pair it forms the scores of all g query heads of the GQA group
 //    with bf16 matrix-core products (v_mfma_f32_16x16x32_bf16: 16 tokens x
 //    16 head slots, head_dim as the reduction), updates an online softmax in
 //    fp32, and accumulates P*V on the matrix cores with P split into a bf16
@@ -55,9 +55,6 @@ struct DecodeArgs {
   float* lse_part;
   const int4* items;
   const int4* merges;
-  const int32_t* lists;       // lists[w] .. lists[w+1]: items of workgroup w
-  int* queue;                 // dynamic schedule: next item to hand out
-  int32_t num_items;
   int32_t hq, hkv, group, max_blocks, num_pages;
   float scale_log2;  // softmax_scale * log2(e)
   float scale;       // softmax_scale
@@ -291,13 +288,12 @@ __device__ __forceinline__ void issue_pair(const DecodeArgs& a,
 // 4gq..4gq+3 of every 16-dim tile. Keeping the rounded mc itself makes the
 // rescale factor exp2(mc_old - mc_new) exactly 1 while the max is unchanged
 // (no drift over thousands of pages) and lets lse = mc * ln 2 + ln(l) use
-// the very offset the exponentials used. The denominator is a long sum of
-// positive terms, so it is carried in fp64.
+// the very offset the exponentials used.
 template <int D>
 struct Acc {
   f32x4 o[D / 16];
   float m;     // mc, in log2 units; -inf before the first valid token
-  double l;
+  float l;
   __device__ __forceinline__ void reset() {
 #pragma unroll
     for (int n = 0; n < D / 16; ++n) o[n] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -351,9 +347,8 @@ __device__ __forceinline__ void compute_pair(const DecodeArgs& a,
     pa[r] = __builtin_amdgcn_exp2f(fmaf(sa[r], a.scale_log2, -mc));
     pb[r] = __builtin_amdgcn_exp2f(fmaf(sb[r], a.scale_log2, -mc));
   }
-  st.l = fma(st.l, double(alpha),
-             double(((pa[0] + pa[1]) + (pa[2] + pa[3])) +
-                    ((pb[0] + pb[1]) + (pb[2] + pb[3]))));
+  st.l = fmaf(st.l, alpha, ((pa[0] + pa[1]) + (pa[2] + pa[3])) +
+                               ((pb[0] + pb[1]) + (pb[2] + pb[3])));
 #pragma unroll
   for (int n = 0; n < G::NT; ++n) st.o[n] *= alpha;
   if constexpr (FP8) {
@@ -409,10 +404,10 @@ __device__ __forceinline__ void write_item(const DecodeArgs& a,
   using G = Geo<D, FP8>;
   if (r16 >= a.group) return;
   const int h = c.kvh * a.group + r16;
-  const bool empty = !(st.l > 0.0);
-  const float inv = empty ? 0.f : float(1.0 / st.l);
+  const bool empty = !(st.l > 0.f);
+  const float inv = empty ? 0.f : 1.0f / st.l;
   const float lse_v =
-      empty ? -INFINITY : float(double(st.m) * kLn2d + log(st.l));
+      empty ? -INFINITY : float(double(st.m) * kLn2d + log(double(st.l)));
   float* dst;
   float* lse_dst;
   if (c.slot < 0) {
@@ -442,144 +437,104 @@ __device__ __forceinline__ void write_item(const DecodeArgs& a,
   if (gq == 0) *lse_dst = lse_v;
 }
 
-// One work item by the WAVES wavefronts of a workgroup: wave w takes page
-// pairs w, w+WAVES, ..., each keeping the next pair's loads in flight while
-// it computes the current one; the waves are combined through LDS at the
-// end and wave 0 writes the result. Every thread of the workgroup must call
-// it (it contains workgroup barriers when WAVES > 1).
+// One workgroup per work item (trajectory, kv-head, page range), in the
+// plan's longest-first order; the hardware dispatcher hands items to CUs as
+// workgroups finish. The WAVES wavefronts share the item's page pairs (wave
+// w takes pairs w, w+WAVES, ...), each keeping the next pair's loads in
+// flight while it computes the current one; the waves are combined through
+// LDS at the end and wave 0 writes the result.
 template <int D, bool FP8, int WAVES>
-__device__ __forceinline__ void process_item(const DecodeArgs& a, int k,
-                                             int lane, int wave) {
+__global__ void __launch_bounds__(64 * WAVES)
+__attribute__((amdgpu_waves_per_eu(2)))
+decode_items(const DecodeArgs a) {
   using G = Geo<D, FP8>;
-  const int r16 = lane & 15, gq = lane >> 4;
-  const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
-  const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
-  const ItemCtx c = read_item(a, k);
-  const int npairs = (c.npages + 1) >> 1;
-  bf16x8 qf[G::KK];
-  load_q<D, FP8>(a, c, r16, gq, qf);
-  Acc<D> st;
-  st.reset();
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int k = blockIdx.x;
+  {
+    using G = Geo<D, FP8>;
+    const int r16 = lane & 15, gq = lane >> 4;
+    const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
+    const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
+    const ItemCtx c = read_item(a, k);
+    const int npairs = (c.npages + 1) >> 1;
+    bf16x8 qf[G::KK];
+    load_q<D, FP8>(a, c, r16, gq, qf);
+    Acc<D> st;
+    st.reset();
 
-  int win = -1, btv = -1;
-  auto issue = [&](PairRegs<D, FP8>& pr, int jp) {
-    const int ja = 2 * jp;
-    if ((ja >> 6) != win) {
-      win = ja >> 6;
-      btv = load_window(a, c, win, lane);
-    }
-    issue_pair<D, FP8>(a, c, ja, btv, koff, voff, pr);
-  };
-
-  PairRegs<D, FP8> buf0, buf1;
-  int jp = wave;
-  if (jp < npairs) issue(buf0, jp);
-  while (jp < npairs) {
-    int jn = jp + WAVES;
-    if (jn < npairs) issue(buf1, jn);
-    compute_pair<D, FP8>(a, qf, buf0, st, gq);
-    jp = jn;
-    if (jp >= npairs) break;
-    jn = jp + WAVES;
-    if (jn < npairs) issue(buf0, jn);
-    compute_pair<D, FP8>(a, qf, buf1, st, gq);
-    jp = jn;
-  }
-
-  // Full softmax denominator of head r16 over this wave's pages.
-  st.l += __shfl_xor(st.l, 16);
-  st.l += __shfl_xor(st.l, 32);
-
-  if constexpr (WAVES > 1) {
-    __shared__ float sm_m[WAVES][16];
-    __shared__ double sm_l[WAVES][16];
-    __shared__ float sm_acc[WAVES - 1][G::NT * 4][64];
-    if (wave > 0) {
-      if (gq == 0) {
-        sm_m[wave][r16] = st.m;
-        sm_l[wave][r16] = st.l;
+    int win = -1, btv = -1;
+    auto issue = [&](PairRegs<D, FP8>& pr, int jp) {
+      const int ja = 2 * jp;
+      if ((ja >> 6) != win) {
+        win = ja >> 6;
+        btv = load_window(a, c, win, lane);
       }
-#pragma unroll
-      for (int n = 0; n < G::NT; ++n)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          sm_acc[wave - 1][n * 4 + r][lane] = st.o[n][r];
+      issue_pair<D, FP8>(a, c, ja, btv, koff, voff, pr);
+    };
+
+    PairRegs<D, FP8> buf0, buf1;
+    int jp = wave;
+    if (jp < npairs) issue(buf0, jp);
+    while (jp < npairs) {
+      int jn = jp + WAVES;
+      if (jn < npairs) issue(buf1, jn);
+      compute_pair<D, FP8>(a, qf, buf0, st, gq);
+      jp = jn;
+      if (jp >= npairs) break;
+      jn = jp + WAVES;
+      if (jn < npairs) issue(buf0, jn);
+      compute_pair<D, FP8>(a, qf, buf1, st, gq);
+      jp = jn;
     }
-    __syncthreads();
-    if (wave == 0) {
-      float m_all = st.m;
-#pragma unroll
-      for (int w = 1; w < WAVES; ++w) m_all = fmaxf(m_all, sm_m[w][r16]);
-      const float mref = (m_all == -INFINITY) ? 0.f : m_all;
-      const float f0 = __builtin_amdgcn_exp2f(st.m - mref);   // 0 for -inf
-      st.l *= double(f0);
-#pragma unroll
-      for (int n = 0; n < G::NT; ++n) st.o[n] *= f0;
-#pragma unroll
-      for (int w = 1; w < WAVES; ++w) {
-        const float fw = __builtin_amdgcn_exp2f(sm_m[w][r16] - mref);
-        st.l = fma(sm_l[w][r16], double(fw), st.l);
+
+    // Full softmax denominator of head r16 over this wave's pages.
+    st.l += __shfl_xor(st.l, 16);
+    st.l += __shfl_xor(st.l, 32);
+
+    if constexpr (WAVES > 1) {
+      __shared__ float sm_m[WAVES][16];
+      __shared__ float sm_l[WAVES][16];
+      __shared__ float sm_acc[WAVES - 1][G::NT * 4][64];
+      if (wave > 0) {
+        if (gq == 0) {
+          sm_m[wave][r16] = st.m;
+          sm_l[wave][r16] = st.l;
+        }
 #pragma unroll
         for (int n = 0; n < G::NT; ++n)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            st.o[n][r] = fmaf(sm_acc[w - 1][n * 4 + r][lane], fw, st.o[n][r]);
+            sm_acc[wave - 1][n * 4 + r][lane] = st.o[n][r];
       }
-      st.m = m_all;
+      __syncthreads();
+      if (wave == 0) {
+        float m_all = st.m;
+#pragma unroll
+        for (int w = 1; w < WAVES; ++w) m_all = fmaxf(m_all, sm_m[w][r16]);
+        const float mref = (m_all == -INFINITY) ? 0.f : m_all;
+        const float f0 = __builtin_amdgcn_exp2f(st.m - mref);   // 0 for -inf
+        st.l *= f0;
+#pragma unroll
+        for (int n = 0; n < G::NT; ++n) st.o[n] *= f0;
+#pragma unroll
+        for (int w = 1; w < WAVES; ++w) {
+          const float fw = __builtin_amdgcn_exp2f(sm_m[w][r16] - mref);
+          st.l = fmaf(sm_l[w][r16], fw, st.l);
+#pragma unroll
+          for (int n = 0; n < G::NT; ++n)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              st.o[n][r] = fmaf(sm_acc[w - 1][n * 4 + r][lane], fw, st.o[n][r]);
+        }
+        st.m = m_all;
+      }
+      __syncthreads();          // LDS is reused by the next item
+      if (wave == 0) write_item<D, FP8>(a, c, st, r16, gq);
+    } else {
+      write_item<D, FP8>(a, c, st, r16, gq);
     }
-    __syncthreads();          // LDS is reused by the next item
-    if (wave == 0) write_item<D, FP8>(a, c, st, r16, gq);
-  } else {
-    write_item<D, FP8>(a, c, st, r16, gq);
   }
-}
-
-// Static lists: workgroup w processes items lists[w] .. lists[w+1]-1.
-template <int D, bool FP8, int WAVES>
-__global__ void __launch_bounds__(64 * WAVES)
-__attribute__((amdgpu_waves_per_eu(2)))
-decode_lists(const DecodeArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int first = a.lists[blockIdx.x];
-  const int last = a.lists[blockIdx.x + 1];
-  for (int k = first; k < last; ++k) process_item<D, FP8, WAVES>(a, k, lane, wave);
-}
-
-// Dynamic queue: resident workgroups pull item indices (longest first) from
-// a device-wide counter. Workgroups are dealt to the XCDs round-robin by
-// index, and the XCDs do not stream at the same speed, so any fixed split
-// leaves the kernel waiting for the slowest XCD; pulling lets the faster
-// ones take more items. Each workgroup asks for its next index before
-// working on the current one. Exactly one pull per workgroup comes back
-// past the end; the pull that returns num_items + gridDim.x - 1 is the
-// last one of the launch and resets the counter for the next launch.
-template <int D, bool FP8, int WAVES>
-__global__ void __launch_bounds__(64 * WAVES)
-__attribute__((amdgpu_waves_per_eu(2)))
-decode_queue(const DecodeArgs a) {
-  __shared__ int s_idx;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int n = a.num_items;
-  if (threadIdx.x == 0)
-    s_idx = __hip_atomic_fetch_add(a.queue, 1, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  int idx = s_idx;
-  while (idx < n) {
-    int nxt = 0;
-    if (threadIdx.x == 0)
-      nxt = __hip_atomic_fetch_add(a.queue, 1, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-    process_item<D, FP8, WAVES>(a, idx, lane, wave);
-    __syncthreads();          // every thread has read s_idx
-    if (threadIdx.x == 0) s_idx = nxt;
-    __syncthreads();
-    idx = s_idx;
-  }
-  if (threadIdx.x == 0 && idx == n + int(gridDim.x) - 1)
-    __hip_atomic_store(a.queue, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Block-wide reductions for 256 threads.
@@ -702,24 +657,20 @@ unsigned calib_grid(size_t n16) {
                                                    : size_t(kReadSinkFloats));
 }
 
-template <int D, bool FP8, int WAVES>
-void launch_waves(const laminar_plan* p, const DecodeArgs& a,
-                  hipStream_t stream) {
-  if (p->schedule == LAMINAR_SCHEDULE_DYNAMIC)
-    hipLaunchKernelGGL((decode_queue<D, FP8, WAVES>), dim3(p->grid),
-                       dim3(64 * WAVES), 0, stream, a);
-  else
-    hipLaunchKernelGGL((decode_lists<D, FP8, WAVES>), dim3(p->grid),
-                       dim3(64 * WAVES), 0, stream, a);
-}
-
 template <int D, bool FP8>
 hipError_t launch_partial(const laminar_plan* p, const DecodeArgs& a,
                           hipStream_t stream) {
+  const dim3 grid(p->num_items);
   switch (p->waves) {
-    case 1: launch_waves<D, FP8, 1>(p, a, stream); break;
-    case 2: launch_waves<D, FP8, 2>(p, a, stream); break;
-    default: launch_waves<D, FP8, 4>(p, a, stream); break;
+    case 1:
+      hipLaunchKernelGGL((decode_items<D, FP8, 1>), grid, dim3(64), 0, stream, a);
+      break;
+    case 2:
+      hipLaunchKernelGGL((decode_items<D, FP8, 2>), grid, dim3(128), 0, stream, a);
+      break;
+    default:
+      hipLaunchKernelGGL((decode_items<D, FP8, 4>), grid, dim3(256), 0, stream, a);
+      break;
   }
   return hipGetLastError();
 }
@@ -741,9 +692,6 @@ DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
   a.lse = lse;
   a.items = reinterpret_cast<const int4*>(ws + p->off_items);
   a.merges = reinterpret_cast<const int4*>(ws + p->off_merges);
-  a.lists = reinterpret_cast<const int32_t*>(ws + p->off_lists);
-  a.queue = reinterpret_cast<int*>(ws + p->off_queue);
-  a.num_items = p->num_items;
   a.lse_part = reinterpret_cast<float*>(ws + p->off_lse);
   a.o_part = reinterpret_cast<float*>(ws + p->off_o);
   a.hq = d.num_q_heads;

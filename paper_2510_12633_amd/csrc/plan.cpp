@@ -37,10 +37,6 @@ laminar_status validate(const laminar_attn_desc* d, const int32_t* lens,
   if (d->waves_per_item != 0 && d->waves_per_item != 1 &&
       d->waves_per_item != 2 && d->waves_per_item != 4)
     return LAMINAR_ERR_INVALID_ARG;
-  if (d->schedule != LAMINAR_SCHEDULE_AUTO &&
-      d->schedule != LAMINAR_SCHEDULE_PER_ITEM &&
-      d->schedule != LAMINAR_SCHEDULE_DYNAMIC)
-    return LAMINAR_ERR_INVALID_ARG;
   if (d->kv_dtype != LAMINAR_KV_BF16 && d->kv_dtype != LAMINAR_KV_FP8_E4M3FN)
     return LAMINAR_ERR_INVALID_ARG;
   if (d->kv_dtype == LAMINAR_KV_FP8_E4M3FN && (!d->k_scale || !d->v_scale))
@@ -74,9 +70,6 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   p->desc = *desc;
   const int32_t B = desc->batch, hkv = desc->num_kv_heads;
   p->group = desc->num_q_heads / hkv;
-  p->schedule = desc->schedule == LAMINAR_SCHEDULE_DYNAMIC
-                    ? LAMINAR_SCHEDULE_DYNAMIC
-                    : LAMINAR_SCHEDULE_PER_ITEM;
   p->waves = desc->waves_per_item ? desc->waves_per_item
                                   : laminar_detail::kDefaultWaves;
   const int64_t units = int64_t(B) * hkv;
@@ -91,100 +84,39 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
       std::max(1, laminar_detail::kResidentWavesPerCU / p->waves);
   const int64_t step = 2 * int64_t(p->waves);   // one page pair per wave
 
-  // Pieces in launch order, grouped by list; list_off[l] .. list_off[l+1]
-  // are the pieces of list l.
-  std::vector<Piece> order;
-  std::vector<int32_t> list_off(1, 0);
-  order.reserve(size_t(units) + 1024);
-
-  if (p->schedule == LAMINAR_SCHEDULE_PER_ITEM) {
-    int64_t chunk;
-    if (desc->pages_per_item > 0) {
-      chunk = desc->pages_per_item;
-    } else {
-      const int64_t target = resident * laminar_detail::kItemsPerSlotNum /
-                             laminar_detail::kItemsPerSlotDen;
-      chunk = std::max<int64_t>(step, (work + target - 1) / target);
-      chunk = (chunk + step - 1) / step * step;
-    }
-    p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
-    for (int64_t u = 0; u < units; ++u) {
-      const int64_t pages = upages[size_t(u)];
-      const int64_t n = pages == 0 ? 1 : (pages + chunk - 1) / chunk;
-      const int64_t base = pages / n, rem = pages % n;
-      int64_t pos = 0;
-      for (int64_t i = 0; i < n; ++i) {
-        const int64_t sz = base + (i < rem ? 1 : 0);
-        order.push_back({int32_t(u), int32_t(pos), int32_t(pos + sz)});
-        pos += sz;
-      }
-    }
-    // Longest first; ties keep (trajectory, kv-head, page) order. One
-    // piece per list: the hardware dispatcher hands them out greedily.
-    std::stable_sort(order.begin(), order.end(),
-                     [](const Piece& a, const Piece& b) {
-                       return (a.p1 - a.p0) > (b.p1 - b.p0);
-                     });
-    for (size_t i = 0; i < order.size(); ++i) list_off.push_back(int32_t(i + 1));
+  int64_t chunk;
+  if (desc->pages_per_item > 0) {
+    chunk = desc->pages_per_item;
   } else {
-    // Dynamic: pieces of about work / (kQueuePiecesPerWG * resident) pages,
-    // longest first, pulled from a device-wide queue by resident
-    // workgroups; the last kQueueTailNum / kQueueTailDen of the work (the
-    // smallest pieces) is re-cut into pieces of at most kQueueTailPages so
-    // the queue runs out on short items.
-    int64_t chunk;
-    if (desc->pages_per_item > 0) {
-      chunk = desc->pages_per_item;
-    } else {
-      const int64_t target = resident * laminar_detail::kQueuePiecesPerWG;
-      chunk = std::max<int64_t>(step, (work + target - 1) / target);
-      chunk = (chunk + step - 1) / step * step;
-    }
-    p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
-    std::vector<Piece> big;
-    for (int64_t u = 0; u < units; ++u) {
-      const int64_t pages = upages[size_t(u)];
-      const int64_t n = pages == 0 ? 1 : (pages + chunk - 1) / chunk;
-      const int64_t base = pages / n, rem = pages % n;
-      int64_t pos = 0;
-      for (int64_t i = 0; i < n; ++i) {
-        const int64_t sz = base + (i < rem ? 1 : 0);
-        big.push_back({int32_t(u), int32_t(pos), int32_t(pos + sz)});
-        pos += sz;
-      }
-    }
-    std::stable_sort(big.begin(), big.end(), [](const Piece& a, const Piece& b) {
-      return (a.p1 - a.p0) > (b.p1 - b.p0);
-    });
-    const int64_t tail_work = work * laminar_detail::kQueueTailNum /
-                              laminar_detail::kQueueTailDen;
-    const int64_t tail_pages = std::min<int64_t>(
-        chunk, laminar_detail::kQueueTailPages);
-    size_t cut = big.size();
-    for (int64_t acc = 0; cut > 0 && acc + (big[cut - 1].p1 - big[cut - 1].p0) <= tail_work;) {
-      acc += big[cut - 1].p1 - big[cut - 1].p0;
-      --cut;
-    }
-    order.assign(big.begin(), big.begin() + int64_t(cut));
-    std::vector<Piece> tail;
-    for (size_t i = cut; i < big.size(); ++i) {
-      const Piece& pc = big[i];
-      const int64_t len = pc.p1 - pc.p0;
-      const int64_t n = len == 0 ? 1 : (len + tail_pages - 1) / tail_pages;
-      const int64_t base = len / n, rem = len % n;
-      int64_t pos = pc.p0;
-      for (int64_t j = 0; j < n; ++j) {
-        const int64_t sz = base + (j < rem ? 1 : 0);
-        tail.push_back({pc.unit, int32_t(pos), int32_t(pos + sz)});
-        pos += sz;
-      }
-    }
-    std::stable_sort(tail.begin(), tail.end(), [](const Piece& a, const Piece& b) {
-      return (a.p1 - a.p0) > (b.p1 - b.p0);
-    });
-    order.insert(order.end(), tail.begin(), tail.end());
-    list_off.push_back(int32_t(order.size()));   // one shared list
+    // Aim for kItemsPerSlot items per resident workgroup; every wave of an
+    // item gets at least one pair of pages.
+    const int64_t target = resident * laminar_detail::kItemsPerSlotNum /
+                           laminar_detail::kItemsPerSlotDen;
+    chunk = std::max<int64_t>(step, (work + target - 1) / target);
+    chunk = (chunk + step - 1) / step * step;
   }
+  p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
+
+  // Near-equal page-aligned pieces of every unit, launched longest first
+  // (ties keep trajectory, kv-head, page order); the hardware dispatcher
+  // hands them to CUs greedily as workgroups finish.
+  std::vector<Piece> order;
+  order.reserve(size_t(units) + size_t(work / chunk) + 1);
+  for (int64_t u = 0; u < units; ++u) {
+    const int64_t pages = upages[size_t(u)];
+    const int64_t n = pages == 0 ? 1 : (pages + chunk - 1) / chunk;
+    const int64_t base = pages / n, rem = pages % n;
+    int64_t pos = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      const int64_t sz = base + (i < rem ? 1 : 0);
+      order.push_back({int32_t(u), int32_t(pos), int32_t(pos + sz)});
+      pos += sz;
+    }
+  }
+  std::stable_sort(order.begin(), order.end(),
+                   [](const Piece& a, const Piece& b) {
+                     return (a.p1 - a.p0) > (b.p1 - b.p0);
+                   });
 
   // Partial slots: a unit cut into several pieces gets consecutive slots in
   // page order and one merge record; a unit in one piece writes directly.
@@ -223,11 +155,6 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
         items[size_t(v[r].second)].slot = first_slot[size_t(unit)] + int32_t(r);
     }
   }
-  p->num_lists = int32_t(list_off.size()) - 1;
-  p->grid = p->schedule == LAMINAR_SCHEDULE_DYNAMIC
-                ? int32_t(std::max<int64_t>(
-                      1, std::min<int64_t>(resident, int64_t(items.size()))))
-                : p->num_lists;
 
   p->num_items = int32_t(items.size());
   p->num_merges = int32_t(merges.size());
@@ -236,10 +163,6 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   size_t off = 0;
   p->off_items = off;
   off = align256(off + items.size() * 16);
-  p->off_lists = off;
-  off = align256(off + list_off.size() * sizeof(int32_t));
-  p->off_queue = off;                  // one int counter, zero in the image
-  off = align256(off + sizeof(int32_t));
   p->off_merges = off;
   off = align256(off + merges.size() * 16);
   p->off_lse = off;
@@ -254,9 +177,6 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   if (!items.empty())
     std::memcpy(p->tables.data() + p->off_items / 4, items.data(),
                 items.size() * sizeof(Item));
-  if (!list_off.empty())
-    std::memcpy(p->tables.data() + p->off_lists / 4, list_off.data(),
-                list_off.size() * sizeof(int32_t));
   if (!merges.empty())
     std::memcpy(p->tables.data() + p->off_merges / 4, merges.data(),
                 merges.size() * sizeof(Item));
@@ -301,23 +221,6 @@ int32_t laminar_plan_merges_copy(const laminar_plan* plan, int32_t* dst,
   if (!plan || !dst || capacity < 0) return -1;
   const int32_t n = std::min(capacity, plan->num_merges);
   std::memcpy(dst, plan->tables.data() + plan->off_merges / 4, size_t(n) * 16);
-  return n;
-}
-
-int32_t laminar_plan_schedule(const laminar_plan* plan) {
-  return plan ? plan->schedule : -1;
-}
-
-int32_t laminar_plan_num_lists(const laminar_plan* plan) {
-  return plan ? plan->num_lists : -1;
-}
-
-int32_t laminar_plan_list_offsets_copy(const laminar_plan* plan, int32_t* dst,
-                                       int32_t capacity) {
-  if (!plan || !dst || capacity < 0) return -1;
-  const int32_t total = plan->num_lists + 1;
-  const int32_t n = std::min(capacity, total);
-  std::memcpy(dst, plan->tables.data() + plan->off_lists / 4, size_t(n) * 4);
   return n;
 }
 

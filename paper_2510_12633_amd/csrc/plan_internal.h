@@ -13,20 +13,15 @@ struct laminar_plan {
   int32_t group = 0;           // query heads per kv-head
   int32_t pages_per_item = 0;  // chosen split size
   int32_t waves = 0;           // wavefronts per work item
-  int32_t schedule = 0;        // LAMINAR_SCHEDULE_PER_ITEM or _DYNAMIC
-  int32_t num_lists = 0;       // static lists of items (dynamic: one queue)
-  int32_t grid = 0;            // workgroups launched
   int32_t num_items = 0;
   int32_t num_merges = 0;
   int32_t num_slots = 0;       // partial (out, lse) records
   // Host image of workspace bytes [0, off_lse): the work items (4 int32
-  // each, in launch order) at off_items, the list offsets (num_lists + 1
-  // int32) at off_lists, the queue counter (0) at off_queue and the merge
-  // records at off_merges.
+  // each, in launch order) at off_items and the merge records at
+  // off_merges.
   std::vector<int32_t> tables;
   // Workspace layout (byte offsets, 256-byte aligned sections).
-  size_t off_items = 0, off_lists = 0, off_queue = 0, off_merges = 0;
-  size_t off_lse = 0, off_o = 0;
+  size_t off_items = 0, off_merges = 0, off_lse = 0, off_o = 0;
   size_t ws_bytes = 0;
   // Bound workspace (device memory owned by the caller).
   void* ws = nullptr;
@@ -45,11 +40,4 @@ constexpr int kResidentWavesPerCU = 8;
 constexpr int kItemsPerSlotNum = 3;
 constexpr int kItemsPerSlotDen = 2;
 constexpr int kDefaultWaves = 4;
-// Dynamic schedule: big pieces per resident workgroup the automatic split
-// aims for, and the fraction of the work (kQueueTailNum / kQueueTailDen, the
-// smallest pieces) re-cut into pieces of at most kQueueTailPages pages.
-constexpr int64_t kQueuePiecesPerWG = 2;
-constexpr int64_t kQueueTailNum = 1;
-constexpr int64_t kQueueTailDen = 8;
-constexpr int64_t kQueueTailPages = 16;
 }  // namespace laminar_detail

@@ -14,8 +14,7 @@ static int fail(const char* what) {
   return 1;
 }
 
-static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves,
-                 int schedule) {
+static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves) {
   laminar_attn_desc d = {};
   d.batch = int32_t(lens.size());
   d.num_q_heads = hkv * 4;
@@ -28,7 +27,6 @@ static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves,
   d.softmax_scale = 0.125f;
   d.pages_per_item = ppi;
   d.waves_per_item = waves;
-  d.schedule = schedule;
   laminar_plan* p = nullptr;
   if (laminar_plan_create(&d, lens.data(), 256, &p) != LAMINAR_OK || !p)
     return fail("create");
@@ -50,18 +48,6 @@ static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves,
   for (auto& v : seen)
     for (char c : v)
       if (!c) return fail("hole");
-  const int lists = laminar_plan_num_lists(p);
-  if (lists >= 0) {
-    std::vector<int32_t> off(size_t(lists) + 1);
-    if (laminar_plan_list_offsets_copy(p, off.data(), lists + 1) != lists + 1)
-      return fail("lists");
-    if (off[0] != 0 || off[lists] != n) return fail("list range");
-    for (int w = 0; w < lists; ++w)
-      if (off[w + 1] <= off[w]) return fail("empty list");
-    if (lists == 0 && n != 0) return fail("items without lists");
-    if (laminar_plan_schedule(p) == LAMINAR_SCHEDULE_DYNAMIC && lists != 1)
-      return fail("dynamic plan with several lists");
-  }
   const int m = laminar_plan_num_merges(p);
   std::vector<int32_t> merges(size_t(4) * (m > 0 ? m : 1));
   if (laminar_plan_merges_copy(p, merges.data(), m) != m) return fail("merges");
@@ -83,8 +69,7 @@ int main() {
     const int hkv = 1 << (rng() % 4);
     const int ppis[] = {0, 1, 2, 7, 64, 1 << 20};
     const int waves[] = {0, 1, 2, 4};
-    if (check(lens, hkv, ppis[rng() % 6], waves[rng() % 4], int(rng() % 3)))
-      return 1;
+    if (check(lens, hkv, ppis[rng() % 6], waves[rng() % 4])) return 1;
   }
   // argument errors must not touch the output or leak
   laminar_plan* p = reinterpret_cast<laminar_plan*>(0x1);

@@ -23,25 +23,21 @@ def declared_functions():
 
 def desc(batch=4, hq=28, hkv=4, d=128, pages=10**6, max_blocks=8192,
          kv=N.LAMINAR_KV_BF16, scale=0.1, ppi=0, waves=0, k_scale=None,
-         v_scale=None, page_size=16, schedule=0):
+         v_scale=None, page_size=16):
     return N.LaminarAttnDesc(batch=batch, num_q_heads=hq, num_kv_heads=hkv,
                              head_dim=d, page_size=page_size, num_pages=pages,
                              max_blocks_per_seq=max_blocks, kv_dtype=kv,
                              softmax_scale=scale, k_scale=k_scale,
                              v_scale=v_scale, pages_per_item=ppi,
-                             waves_per_item=waves, schedule=schedule)
+                             waves_per_item=waves)
 
 
-def plan_tables(d, lens, cus=256, lists=False):
+def plan_tables(d, lens, cus=256):
     p = N.laminar_plan_create(d, np.asarray(lens, np.int32), cus)
     try:
-        res = (N.laminar_plan_items_copy(p), N.laminar_plan_merges_copy(p),
-               N.laminar_plan_pages_per_item(p), N.laminar_plan_waves_per_item(p),
-               N.laminar_plan_workspace_bytes(p))
-        if lists:
-            res = res + (N.laminar_plan_schedule(p),
-                         N.laminar_plan_list_offsets_copy(p))
-        return res
+        return (N.laminar_plan_items_copy(p), N.laminar_plan_merges_copy(p),
+                N.laminar_plan_pages_per_item(p), N.laminar_plan_waves_per_item(p),
+                N.laminar_plan_workspace_bytes(p))
     finally:
         N.laminar_plan_destroy(p)
 
@@ -66,10 +62,8 @@ def test_status_strings():
     assert N.laminar_status_string(99) == "unknown status"
 
 
-def check_plan(lens, hkv, items, merges, ppi, offsets=None, dynamic=False):
-    """Coverage, slot and ordering invariants of a plan. `offsets` are the
-    list offsets: per-item plans have one item per list, dynamic plans one
-    list (the queue) holding every item."""
+def check_plan(lens, hkv, items, merges, ppi):
+    """Coverage, size, ordering and slot invariants of a plan."""
     pages = -(-np.asarray(lens, np.int64) // 16)
     covered = {}
     by_unit = {}
@@ -85,21 +79,14 @@ def check_plan(lens, hkv, items, merges, ppi, offsets=None, dynamic=False):
     # every (trajectory, kv-head, page) exactly once; empty units once
     assert len(covered) == int(pages.sum()) * hkv
     assert set(by_unit) == set(range(len(lens) * hkv))
-    if offsets is not None:
-        assert offsets[0] == 0 and offsets[-1] == len(items)
-        assert np.all(np.diff(offsets) >= 1)
     sizes = [int(p1 - p0) for _, p0, p1, _ in items]
-    assert sizes == sorted(sizes, reverse=True)
-    if offsets is not None:
-        expect = [0, len(items)] if dynamic else np.arange(len(items) + 1)
-        assert np.array_equal(offsets, expect)
+    assert sizes == sorted(sizes, reverse=True)         # longest first
     merged = {int(m[0]): (int(m[1]), int(m[2])) for m in merges}
     assert len(merged) == len(merges)
     all_slots = []
     for unit, chunks in by_unit.items():
         sz = [p1 - p0 for p0, p1, _ in chunks]
-        if not dynamic:
-            assert max(sz) - min(sz) <= 1
+        assert max(sz) - min(sz) <= 1                   # near-equal pieces
         if len(chunks) == 1:
             assert chunks[0][2] == -1 and unit not in merged
         else:
@@ -120,63 +107,32 @@ def test_planner_invariants_random(seed):
     lens = np.minimum(np.exp(rng.normal(7, 1.5, b)).astype(np.int64), 70000)
     lens[rng.random(b) < 0.05] = 0
     hkv = int(rng.choice([1, 2, 4, 8]))
-    for ppi, waves, sched in ((0, 0, 1), (1, 1, 1), (3, 2, 1), (64, 4, 1),
-                              (1 << 20, 0, 1), (0, 0, 0), (0, 0, 2), (1, 1, 2),
-                              (5, 2, 2), (1 << 20, 4, 2)):
+    for ppi, waves in ((0, 0), (1, 1), (3, 2), (64, 4), (1 << 20, 0)):
         d = desc(batch=b, hq=hkv * int(rng.integers(1, 9)), hkv=hkv, ppi=ppi,
-                 waves=waves, schedule=sched)
-        items, merges, chosen, w, ws, got_sched, offs = plan_tables(
-            d, lens, lists=True)
+                 waves=waves)
+        items, merges, chosen, w, ws = plan_tables(d, lens)
         if ppi:
             assert chosen == ppi
         assert w == (waves or 4)
-        if sched in (0, 1):
-            assert got_sched == 1
-            check_plan(lens, hkv, items, merges, chosen, offsets=offs)
-        else:
-            assert got_sched == 2
-            check_plan(lens, hkv, items, merges, chosen, offsets=offs,
-                       dynamic=True)
+        check_plan(lens, hkv, items, merges, chosen)
         assert ws % 256 == 0 and ws >= 16 * (len(items) + len(merges))
-
-
-def test_dynamic_queue_ends_on_small_pieces():
-    rng = np.random.default_rng(11)
-    lens = np.minimum(np.exp(rng.normal(7.6, 1.0, 256)).astype(np.int64), 32768)
-    d = desc(batch=256, hq=28, hkv=4, schedule=2)
-    items, merges, chosen, w, _, _, offs = plan_tables(d, lens, lists=True)
-    sizes = (items[:, 2] - items[:, 1]).astype(np.int64)
-    work = int((-(-lens // 16)).sum()) * 4
-    assert chosen % 8 == 0 and chosen >= -(-work // 1024)
-    # the smallest pieces, about the last eighth of the work, are <= 16 pages
-    tail = sizes[sizes <= 16]
-    assert np.all(sizes[len(sizes) - len(tail):] <= 16)
-    assert tail.sum() >= work // 8 - chosen
-    check_plan(lens, 4, items, merges, chosen, offsets=offs, dynamic=True)
 
 
 def test_planner_auto_split_fills_the_gpu():
     """Eight 64k-token trajectories x 4 kv-heads (32 units) still give
-    thousands of work items."""
+    about 1.5 items per resident 4-wave workgroup (512 on 256 CUs)."""
     lens = [65536] * 8
-    items, merges, chosen, waves, _ = plan_tables(desc(batch=8, schedule=1), lens)
+    items, merges, chosen, waves, _ = plan_tables(desc(batch=8), lens)
     assert len(items) >= 700 and len(merges) == 32
     assert chosen % (2 * waves) == 0
     check_plan(lens, 4, items, merges, chosen)
-    items, merges, chosen, _, _, _, offs = plan_tables(
-        desc(batch=8, schedule=2), lens, lists=True)
-    assert len(items) >= 1024 and len(merges) == 32
-    check_plan(lens, 4, items, merges, chosen, offsets=offs, dynamic=True)
 
 
 def test_planner_edge_lengths():
     for lens in ([0], [1], [16], [17], [0, 0, 0], [98304], [1, 98304, 0, 15]):
-        for sched in (1, 2):
-            d = desc(batch=len(lens), hq=64, hkv=8, schedule=sched)
-            items, merges, chosen, _, _, _, offs = plan_tables(d, lens,
-                                                               lists=True)
-            check_plan(lens, 8, items, merges, chosen, offsets=offs,
-                       dynamic=sched == 2)
+        d = desc(batch=len(lens), hq=64, hkv=8)
+        items, merges, chosen, _, _ = plan_tables(d, lens)
+        check_plan(lens, 8, items, merges, chosen)
     items, merges, _, _, _ = plan_tables(desc(batch=0), [])
     assert len(items) == 0 and len(merges) == 0
 
@@ -213,9 +169,7 @@ def test_planner_argument_errors():
     assert _status(desc(batch=1, kv=7), [5]) == INV
     assert _status(desc(batch=1, scale=0.0), [5]) == INV
     assert _status(desc(batch=1, waves=3), [5]) == INV
-    assert _status(desc(batch=1, waves=4, schedule=2), [5]) == N.LAMINAR_OK
-    assert _status(desc(batch=1, waves=4, schedule=1), [5]) == N.LAMINAR_OK
-    assert _status(desc(batch=1, schedule=3), [5]) == INV
+    assert _status(desc(batch=1, waves=4), [5]) == N.LAMINAR_OK
     assert _status(desc(batch=1, ppi=-1), [5]) == INV
     assert _status(desc(batch=1, pages=0), [5]) == INV
     assert _status(desc(batch=1, page_size=32), [5]) == UNS
@@ -279,3 +233,27 @@ def test_planner_under_address_and_ub_sanitizers(tmp_path):
                        timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "plan_check OK" in r.stdout
+
+
+def test_attention_kernels_do_not_spill():
+    """The page-pair double buffer fills most of the register file; a spill
+    to scratch in the hot loop costs ~15% of bandwidth, so every attention
+    kernel instantiation must compile without scratch."""
+    from paper_2510_12633_amd import build as B
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    src = os.path.join(B.CSRC, "decode_attn.hip")
+    cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang",
+           "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", B.INCLUDE,
+           "-I", B.CSRC, "-c", src, "-o", os.devnull,
+           "-Rpass-analysis=kernel-resource-usage"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-2000:]
+    names = re.findall(r"Function Name: (\S+)", r.stderr)
+    scratch = [int(x) for x in
+               re.findall(r"ScratchSize \[bytes/lane\]: (\d+)", r.stderr)]
+    assert len(names) == len(scratch) and names
+    kernels = [(n, sc) for n, sc in zip(names, scratch) if "decode_items" in n]
+    assert len(kernels) == 12          # 2 head dims x 2 dtypes x 3 waves
+    assert all(sc == 0 for _, sc in kernels), kernels

@@ -28,7 +28,7 @@ def _say(msg):
 
 
 def run_gpu(wl, pages_per_item=0, waves_per_item=0, block_table=None,
-            k_pages=None, v_pages=None, two_phase=False, schedule=0):
+            k_pages=None, v_pages=None, two_phase=False):
     from paper_2510_12633_amd.api import PagedDecodeAttention
     c = wl.cfg
     dev = wl.q.device
@@ -42,8 +42,7 @@ def run_gpu(wl, pages_per_item=0, waves_per_item=0, block_table=None,
         max_blocks_per_seq=bt_np.shape[1], seq_lens_host=wl.seq_lens,
         softmax_scale=wl.softmax_scale, kv_dtype=c.kv_dtype,
         k_scale=wl.k_scale, v_scale=wl.v_scale,
-        pages_per_item=pages_per_item, waves_per_item=waves_per_item,
-        schedule=schedule)
+        pages_per_item=pages_per_item, waves_per_item=waves_per_item)
     kp = wl.k_pages if k_pages is None else k_pages
     vp = wl.v_pages if v_pages is None else v_pages
     if two_phase:
@@ -94,12 +93,9 @@ def test_tiny_config_all_outputs():
     wl = make_workload(1, device="cuda")
     ref = decode_attention_from_host(host_arrays(wl))
     for ppi in (0, 1, 4, 64):
-        check(run_gpu(wl, pages_per_item=ppi, schedule=2), ref,
-              f"tiny dynamic pages_per_item={ppi}")
         for waves in (1, 2, 4):
-            check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves,
-                          schedule=1), ref,
-                  f"tiny per-item waves={waves} pages_per_item={ppi}")
+            check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves), ref,
+                  f"tiny waves={waves} pages_per_item={ppi}")
     check(run_gpu(wl, two_phase=True), ref, "tiny partial+merge")
 
 
@@ -109,12 +105,9 @@ def test_custom_shapes(name, cfg):
     wl = make_workload(cfg, seed=31, device="cuda")
     ref = decode_attention_from_host(host_arrays(wl), workers=4)
     for ppi in (0, 2, 5):
-        check(run_gpu(wl, pages_per_item=ppi, schedule=2), ref,
-              f"{name} dynamic pages_per_item={ppi}")
-        for waves in (1, 4):
-            check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves,
-                          schedule=1), ref,
-                  f"{name} per-item waves={waves} pages_per_item={ppi}")
+        for waves in (1, 2, 4):
+            check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves), ref,
+                  f"{name} waves={waves} pages_per_item={ppi}")
 
 
 def test_forced_split_independence():
@@ -122,12 +115,12 @@ def test_forced_split_independence():
     wl = make_workload(custom_config([5000, 777, 12000, 33], 28, 4, 128),
                        seed=5, device="cuda")
     base = run_gpu(wl, pages_per_item=100000)
-    for sched in (1, 2):
+    for waves in (1, 4):
         for ppi in (1, 2, 7, 64):
-            o, l = run_gpu(wl, pages_per_item=ppi, schedule=sched)
+            o, l = run_gpu(wl, pages_per_item=ppi, waves_per_item=waves)
             eo = np.abs(o - base[0]).max()
             el = np.abs(l - base[1]).max()
-            _say(f"schedule {sched} split {ppi} vs unsplit: {eo:.2e} {el:.2e}")
+            _say(f"waves {waves} split {ppi} vs unsplit: {eo:.2e} {el:.2e}")
             assert eo <= 1e-5 and el <= 1e-5
 
 
@@ -139,8 +132,7 @@ def test_no_rescale_drift_on_long_single_wave_items():
     wl = make_workload(custom_config([12000, 5000], 28, 4, 128), seed=5,
                        device="cuda")
     ro, rl = decode_attention_from_host(host_arrays(wl), workers=4)
-    for kw in (dict(schedule=1, waves_per_item=1),
-               dict(schedule=1, waves_per_item=4)):
+    for kw in (dict(waves_per_item=1), dict(waves_per_item=4)):
         o, l = run_gpu(wl, pages_per_item=1 << 20, **kw)
         el = np.abs(l - rl).max()
         eo = np.abs(o - ro).max()
@@ -210,9 +202,10 @@ def test_single_long_trajectory():
                        device="cuda")
     ref = decode_attention_from_host(host_arrays(wl), workers=8)
     check(run_gpu(wl), ref, "B=1 n=98304 auto split")
-    check(run_gpu(wl, pages_per_item=1 << 20, waves_per_item=4, schedule=1),
-          ref, "B=1 n=98304 unsplit, 4 waves")
-    check(run_gpu(wl, schedule=2), ref, "B=1 n=98304 dynamic")
+    check(run_gpu(wl, pages_per_item=1 << 20, waves_per_item=4), ref,
+          "B=1 n=98304 unsplit, 4 waves")
+    check(run_gpu(wl, pages_per_item=1 << 20, waves_per_item=1), ref,
+          "B=1 n=98304 unsplit, 1 wave")
 
 
 def test_invalid_arguments_return_status():
