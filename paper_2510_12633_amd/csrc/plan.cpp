@@ -10,10 +10,8 @@
 
 #include <algorithm>
 #include <cstring>
-#include <functional>
 #include <new>
-#include <numeric>
-#include <utility>
+#include <stdexcept>
 
 #include "plan_internal.h"
 
@@ -21,7 +19,6 @@ namespace {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-struct Piece { int32_t unit, p0, p1; };
 struct Item { int32_t unit, p0, p1, slot; };
 
 laminar_status validate(const laminar_attn_desc* d, const int32_t* lens,
@@ -72,14 +69,9 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   p->group = desc->num_q_heads / hkv;
   p->waves = desc->waves_per_item ? desc->waves_per_item
                                   : laminar_detail::kDefaultWaves;
-  const int64_t units = int64_t(B) * hkv;
-  std::vector<int64_t> upages(static_cast<size_t>(units), 0);
   int64_t work = 0;                        // (page, kv-head) tiles
   for (int32_t b = 0; b < B; ++b)
-    for (int32_t h = 0; h < hkv; ++h) {
-      upages[size_t(b) * hkv + h] = (int64_t(seq_lens_host[b]) + 15) / 16;
-      work += upages[size_t(b) * hkv + h];
-    }
+    work += (int64_t(seq_lens_host[b]) + 15) / 16 * hkv;
   const int64_t resident = int64_t(num_cus) *
       std::max(1, laminar_detail::kResidentWavesPerCU / p->waves);
   const int64_t step = 2 * int64_t(p->waves);   // one page pair per wave
@@ -97,90 +89,76 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   }
   p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
 
-  // Near-equal page-aligned pieces of every unit, launched longest first
-  // (ties keep trajectory, kv-head, page order); the hardware dispatcher
-  // hands them to CUs greedily as workgroups finish.
-  std::vector<Piece> order;
-  order.reserve(size_t(units) + size_t(work / chunk) + 1);
-  for (int64_t u = 0; u < units; ++u) {
-    const int64_t pages = upages[size_t(u)];
-    const int64_t n = pages == 0 ? 1 : (pages + chunk - 1) / chunk;
-    const int64_t base = pages / n, rem = pages % n;
-    int64_t pos = 0;
-    for (int64_t i = 0; i < n; ++i) {
-      const int64_t sz = base + (i < rem ? 1 : 0);
-      order.push_back({int32_t(u), int32_t(pos), int32_t(pos + sz)});
-      pos += sz;
+  // Near-equal page-aligned pieces of every unit (trajectory, kv-head):
+  // n = ceil(pages / chunk) pieces, the first pages % n of them one page
+  // longer; all kv-heads of a trajectory are cut alike. A unit cut into
+  // several pieces gets n consecutive partial slots in page order and one
+  // merge record; a unit in one piece writes out/lse directly.
+  struct Cut { uint32_t n, base, rem; };
+  std::vector<Cut> cuts(static_cast<size_t>(B));
+  const uint32_t chunk32 = uint32_t(std::min<int64_t>(chunk, UINT32_MAX));
+  int64_t total = 0, merges = 0, slots = 0;
+  uint32_t longest = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    const uint32_t pages = (uint32_t(seq_lens_host[b]) + 15) / 16;  // < 2^27
+    const uint32_t n = pages == 0 ? 1 : (pages - 1) / chunk32 + 1;
+    const uint32_t base = pages / n;
+    const uint32_t rem = pages - base * n;
+    cuts[size_t(b)] = {n, base, rem};
+    total += int64_t(n) * hkv;
+    longest = std::max(longest, base + (rem ? 1 : 0));
+    if (n > 1) {
+      merges += hkv;
+      slots += int64_t(n) * hkv;
     }
   }
-  std::stable_sort(order.begin(), order.end(),
-                   [](const Piece& a, const Piece& b) {
-                     return (a.p1 - a.p0) > (b.p1 - b.p0);
-                   });
+  if (total > INT32_MAX || slots > INT32_MAX) throw std::length_error("items");
 
-  // Partial slots: a unit cut into several pieces gets consecutive slots in
-  // page order and one merge record; a unit in one piece writes directly.
-  std::vector<int32_t> count(static_cast<size_t>(units), 0);
-  std::vector<int32_t> first_slot(static_cast<size_t>(units), -1);
-  for (const Piece& pc : order) ++count[size_t(pc.unit)];
-  std::vector<Item> merges;            // (unit, slot0, n, 0)
-  int32_t slots = 0;
-  for (int64_t u = 0; u < units; ++u)
-    if (count[size_t(u)] > 1) {
-      first_slot[size_t(u)] = slots;
-      merges.push_back({int32_t(u), slots, count[size_t(u)], 0});
-      slots += count[size_t(u)];
-    }
-  // Rank of each piece among its unit's pieces by first page.
-  std::vector<Item> items(order.size());
-  {
-    std::vector<std::vector<std::pair<int32_t, int32_t>>> per_unit;
-    std::vector<int32_t> split_index(static_cast<size_t>(units), -1);
-    for (size_t i = 0; i < order.size(); ++i) {
-      const Piece& pc = order[i];
-      items[i] = {pc.unit, pc.p0, pc.p1, -1};
-      if (count[size_t(pc.unit)] > 1) {
-        int32_t& si = split_index[size_t(pc.unit)];
-        if (si < 0) {
-          si = int32_t(per_unit.size());
-          per_unit.emplace_back();
-        }
-        per_unit[size_t(si)].push_back({pc.p0, int32_t(i)});
-      }
-    }
-    for (auto& v : per_unit) {
-      std::sort(v.begin(), v.end());
-      const int32_t unit = items[size_t(v[0].second)].unit;
-      for (size_t r = 0; r < v.size(); ++r)
-        items[size_t(v[r].second)].slot = first_slot[size_t(unit)] + int32_t(r);
-    }
-  }
-
-  p->num_items = int32_t(items.size());
-  p->num_merges = int32_t(merges.size());
-  p->num_slots = slots;
-
+  p->num_items = int32_t(total);
+  p->num_merges = int32_t(merges);
+  p->num_slots = int32_t(slots);
   size_t off = 0;
   p->off_items = off;
-  off = align256(off + items.size() * 16);
+  off = align256(off + size_t(total) * 16);
   p->off_merges = off;
-  off = align256(off + merges.size() * 16);
+  off = align256(off + size_t(merges) * 16);
   p->off_lse = off;
   off = align256(off + size_t(slots) * p->group * sizeof(float));
   p->off_o = off;
   off = align256(off + size_t(slots) * p->group * desc->head_dim * sizeof(float));
   p->ws_bytes = off;
 
-  // Byte image of the workspace up to the partial results: items, then
-  // merges, at their section offsets (zero padding between).
+  // The tables are built in place in the byte image of the workspace up to
+  // the partial results (items, then merges, at their section offsets).
   p->tables.assign(p->off_lse / sizeof(int32_t), 0);
-  if (!items.empty())
-    std::memcpy(p->tables.data() + p->off_items / 4, items.data(),
-                items.size() * sizeof(Item));
-  if (!merges.empty())
-    std::memcpy(p->tables.data() + p->off_merges / 4, merges.data(),
-                merges.size() * sizeof(Item));
-  } catch (...) {            // host allocation failure: report, never throw
+  Item* items = reinterpret_cast<Item*>(p->tables.data() + p->off_items / 4);
+  Item* mrec = reinterpret_cast<Item*>(p->tables.data() + p->off_merges / 4);
+
+  // Launch order: longest first; equal lengths keep (trajectory, kv-head,
+  // page) order. The hardware dispatcher hands the workgroups to CUs
+  // greedily as earlier ones finish. A stable counting sort on the length.
+  std::vector<int64_t> start(size_t(longest) + 2, 0);
+  for (const Cut& c : cuts) {
+    start[longest - c.base] += int64_t(c.n - c.rem) * hkv;
+    if (c.rem) start[longest - c.base - 1] += int64_t(c.rem) * hkv;
+  }
+  int64_t acc = 0;
+  for (auto& v : start) { const int64_t c = v; v = acc; acc += c; }
+  int32_t next_slot = 0, m = 0;
+  for (int64_t u = 0; u < int64_t(B) * hkv; ++u) {
+    const Cut c = cuts[size_t(u / hkv)];
+    const bool split = c.n > 1;
+    if (split) mrec[m++] = {int32_t(u), next_slot, int32_t(c.n), 0};
+    int32_t pos = 0;
+    for (uint32_t i = 0; i < c.n; ++i) {
+      const uint32_t sz = c.base + (i < c.rem ? 1 : 0);
+      items[start[longest - sz]++] = {int32_t(u), pos, pos + int32_t(sz),
+                                      split ? next_slot + int32_t(i) : -1};
+      pos += int32_t(sz);
+    }
+    if (split) next_slot += int32_t(c.n);
+  }
+  } catch (...) {     // host allocation failure or too many items: report
     delete p;
     return LAMINAR_ERR_INVALID_ARG;
   }
