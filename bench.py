@@ -52,6 +52,8 @@ def parse_args(argv=None):
                    help="target seconds of oracle work for the CPU baseline")
     p.add_argument("--no-calibrate", action="store_true",
                    help="skip the HBM read/copy calibration kernels")
+    p.add_argument("--no-append", action="store_true",
+                   help="skip the KV-append timing")
     p.add_argument("--fixed-plan", action="store_true",
                    help="plan once outside the timed loop (kernel-only steps)")
     return p.parse_args(argv)
@@ -188,6 +190,47 @@ def calibrate(torch, N, nbytes=4 << 30, iters=10):
     del buf
     torch.cuda.empty_cache()
     return read, copy
+
+
+def measure_append(torch, wl, steps=24):
+    """Time the KV append (one launch per decode step) on this workload's
+    pools, copied and grown by ``steps`` tokens per trajectory. Returns None
+    for workloads with shared prefix pages (a shared last page would need a
+    copy before it is written)."""
+    from paper_2510_12633_amd.api import kv_append
+    from workloads import make_decode_run
+    if wl.cfg.prefix_group:
+        return None
+    run = make_decode_run(wl, steps=steps, seed=11, mix="normal")
+    dev = run.k_pages.device
+    bt = torch.as_tensor(run.block_table, device=dev)
+    lens = [torch.as_tensor(run.lens_after(i), device=dev) for i in range(steps)]
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    warm = 4
+    for i in range(steps):
+        if i >= warm:
+            ev[i].record(stream)
+        kv_append(run.k_new[i], run.v_new[i], bt, lens[i], run.k_pages,
+                  run.v_pages, run.k_scale, run.v_scale,
+                  kv_dtype=wl.cfg.kv_dtype, stream=stream)
+    ev[steps].record(stream)
+    torch.cuda.synchronize()
+    times = [ev[i].elapsed_time(ev[i + 1]) for i in range(warm, steps)]
+    us = 1e3 * sum(times) / len(times)
+    c = wl.cfg
+    units = wl.batch * c.num_kv_heads
+    e = 1 if c.kv_dtype == "fp8_e4m3fn" else 2
+    nbytes = (units * c.head_dim * 2 * 2            # new K and V, bf16
+              + units * c.head_dim * e * 2          # their slots in the pages
+              + wl.batch * 8                        # table entry + length
+              + (units * 2 * 4 * 2 if e == 1 else 0))   # scales read + written
+    del run
+    return {"kernel": "kv_append_kernel", "us_per_call": round(us, 3),
+            "algorithmic_bytes_per_call": nbytes,
+            "GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "bound": "launch/latency (a few hundred bytes per trajectory)",
+            "timed_calls": len(times)}
 
 
 def main(argv=None):
@@ -368,6 +411,10 @@ def main(argv=None):
         result["hbm_calibration_GBps"] = {"read": round(rd, 1),
                                           "copy": round(cp, 1)}
         result["frac_of_calibrated_read"] = round(value * 1e3 / rd, 4)
+    if not args.no_append:
+        app = measure_append(torch, wl)
+        if app is not None:
+            result["kv_append"] = app
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget_s)
     N.laminar_plan_destroy(plan0)

@@ -1,6 +1,7 @@
 """MI355X-native paged grouped-query decode attention (HIP, gfx950).
 
-The C ABI is declared in include/laminar_decode_attn.h; ``_native`` binds it
+The C ABI is declared in include/laminar_decode_attn.h and
+include/laminar_kv_append.h; ``_native`` binds it
 with ctypes under the same names and ``api.PagedDecodeAttention`` owns a plan
 and its device workspace. Every step of the computation runs in the HIP
 library; there is no CPU fallback.
@@ -9,10 +10,11 @@ from . import _native
 from ._native import (LaminarAttnDesc, LaminarError, laminar_decode_attn,
                       laminar_decode_attn_merge, laminar_decode_attn_partial,
                       laminar_hbm_copy, laminar_hbm_read,
-                      laminar_hbm_read_sink_floats, laminar_plan_bind_workspace,
+                      laminar_hbm_read_sink_floats, laminar_kv_append,
+                      laminar_plan_bind_workspace,
                       laminar_plan_create, laminar_plan_destroy,
                       laminar_plan_items_copy, laminar_plan_merges_copy,
                       laminar_plan_num_items, laminar_plan_num_merges,
                       laminar_plan_pages_per_item, laminar_plan_waves_per_item,
                       laminar_plan_workspace_bytes, laminar_status_string)
-from .api import PagedDecodeAttention
+from .api import PagedDecodeAttention, kv_append

@@ -1,4 +1,5 @@
-"""ctypes binding of the C ABI in include/laminar_decode_attn.h.
+"""ctypes binding of the C ABI in include/laminar_decode_attn.h and
+include/laminar_kv_append.h.
 
 Argument marshalling only: every step of the computation runs in the HIP
 library. Importing this module does not touch the GPU; loading fails loudly
@@ -74,6 +75,8 @@ _SIGNATURES = {
     "laminar_hbm_read_sink_floats": (c_int32, []),
     "laminar_hbm_read": (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p]),
     "laminar_hbm_copy": (c_int32, [c_void_p, c_void_p, c_size_t, c_void_p]),
+    "laminar_kv_append": (c_int32, [POINTER(LaminarAttnDesc)] + [c_void_p] * 8
+                          + [c_void_p]),
 }
 
 
@@ -197,6 +200,14 @@ def laminar_plan_merges_copy(plan) -> np.ndarray:
 
 def laminar_plan_destroy(plan):
     lib().laminar_plan_destroy(plan)
+
+
+def laminar_kv_append(desc: LaminarAttnDesc, k_new, v_new, block_table,
+                      seq_lens, k_pages, v_pages, k_scale, v_scale, stream):
+    _check(lib().laminar_kv_append(
+        ctypes.byref(desc), _ptr(k_new), _ptr(v_new), _ptr(block_table),
+        _ptr(seq_lens), _ptr(k_pages), _ptr(v_pages), _ptr(k_scale),
+        _ptr(v_scale), _ptr(stream)), "laminar_kv_append")
 
 
 def laminar_hbm_read_sink_floats() -> int:

@@ -130,3 +130,18 @@ class PagedDecodeAttention:
             self.close()
         except Exception:
             pass
+
+
+def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages,
+              k_scale=None, v_scale=None, *, kv_dtype: str = "bf16",
+              stream=None):
+    """Append the current token's K/V ([B, Hkv, D] bf16) to the paged pools
+    in place (pools [P, Hkv, 16*D]; fp8 scales [P, Hkv] updated too)."""
+    b, hkv, d = k_new.shape
+    desc = N.LaminarAttnDesc(
+        batch=b, num_q_heads=hkv, num_kv_heads=hkv, head_dim=d, page_size=16,
+        num_pages=k_pages.shape[0], max_blocks_per_seq=block_table.shape[1],
+        kv_dtype=KV_DTYPES[kv_dtype], softmax_scale=1.0, k_scale=None,
+        v_scale=None, pages_per_item=0, waves_per_item=0)
+    N.laminar_kv_append(desc, k_new, v_new, block_table, seq_lens, k_pages,
+                        v_pages, k_scale, v_scale, _stream_handle(stream))

@@ -18,7 +18,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "liblaminar_decode_attn.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 
-SOURCES = [os.path.join(CSRC, "decode_attn.hip"), os.path.join(CSRC, "plan.cpp")]
+SOURCES = [os.path.join(CSRC, "decode_attn.hip"),
+           os.path.join(CSRC, "kv_append.hip"), os.path.join(CSRC, "plan.cpp")]
 
 # Packed fp32 VALU forms are switched off for all device code.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -12,13 +12,17 @@ import pytest
 from paper_2510_12633_amd import _native as N
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "laminar_decode_attn.h")
+INCLUDE = os.path.join(ROOT, "include")
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(laminar_\w+)\s*\(", text)))
+    names = set()
+    for h in sorted(os.listdir(INCLUDE)):
+        if h.endswith(".h"):
+            text = open(os.path.join(INCLUDE, h)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(laminar_\w+)\s*\(", text))
+    return sorted(names)
 
 
 def desc(batch=4, hq=28, hkv=4, d=128, pages=10**6, max_blocks=8192,
@@ -45,7 +49,7 @@ def plan_tables(d, lens, cus=256):
 def test_library_exports_every_declared_symbol():
     lib = N.lib()
     names = declared_functions()
-    assert len(names) >= 17
+    assert len(names) >= 18 and "laminar_kv_append" in names
     for name in names:
         assert hasattr(lib, name), name
     nm = shutil.which("nm")
@@ -212,6 +216,34 @@ def test_call_errors_before_any_launch():
     assert lib.laminar_hbm_copy(16, 16, 8, None) == N.LAMINAR_ERR_INVALID_ARG
     assert lib.laminar_plan_num_items(None) == -1
     assert lib.laminar_plan_workspace_bytes(None) == 0
+
+
+def test_kv_append_errors_before_any_launch():
+    lib = N.lib()
+    INV, UNS = N.LAMINAR_ERR_INVALID_ARG, N.LAMINAR_ERR_UNSUPPORTED
+
+    def call(d, k_new=16, v_new=16, bt=16, lens=16, kp=16, vp=16, ks=16,
+             vs=16):
+        return lib.laminar_kv_append(
+            None if d is None else ctypes.byref(d), k_new, v_new, bt, lens, kp,
+            vp, ks, vs, None)
+
+    assert call(None) == INV
+    assert call(desc(batch=0)) == N.LAMINAR_OK          # nothing to append
+    assert call(desc(batch=-1)) == INV
+    assert call(desc(hkv=0)) == INV
+    assert call(desc(pages=0)) == INV
+    assert call(desc(max_blocks=-1)) == INV
+    assert call(desc(kv=7)) == INV
+    assert call(desc(page_size=32)) == UNS
+    assert call(desc(d=96)) == UNS
+    assert call(desc(), k_new=None) == INV
+    assert call(desc(), lens=None) == INV
+    assert call(desc(), vp=None) == INV
+    assert call(desc(), k_new=24) == INV                # misaligned
+    fp8 = desc(kv=N.LAMINAR_KV_FP8_E4M3FN)
+    assert call(fp8, ks=None) == INV
+    assert call(fp8, vs=None) == INV
 
 
 def test_planner_under_address_and_ub_sanitizers(tmp_path):
