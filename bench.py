@@ -52,6 +52,9 @@ def parse_args(argv=None):
                    help="target seconds of oracle work for the CPU baseline")
     p.add_argument("--no-calibrate", action="store_true",
                    help="skip the HBM read/copy calibration kernels")
+    p.add_argument("--cascade", choices=("auto", "off"), default="auto",
+                   help="decode shared prompt prefixes once per group when "
+                        "the workload has them (auto) or not at all (off)")
     p.add_argument("--no-append", action="store_true",
                    help="skip the KV-append timing")
     p.add_argument("--fixed-plan", action="store_true",
@@ -281,7 +284,17 @@ def main(argv=None):
     sh = stream.cuda_stream
 
     # Workspace sized for this batch's plan; reused every step.
-    plan0 = N.laminar_plan_create(desc, lens_host, cus)
+    from workloads import prefix_groups
+    group_of, group_pages = prefix_groups(wl)
+    use_cascade = group_of is not None and args.cascade != "off"
+
+    def make_plan():
+        if use_cascade:
+            return N.laminar_plan_create_cascade(desc, lens_host, group_of,
+                                                 group_pages, cus)
+        return N.laminar_plan_create(desc, lens_host, cus)
+
+    plan0 = make_plan()
     ws_bytes = N.laminar_plan_workspace_bytes(plan0)
     n_items = N.laminar_plan_num_items(plan0)
     n_merges = N.laminar_plan_num_merges(plan0)
@@ -302,7 +315,7 @@ def main(argv=None):
             plan = plan0
         else:
             t0 = time.perf_counter_ns()
-            plan = N.laminar_plan_create(desc, lens_host, cus)
+            plan = make_plan()
             N.laminar_plan_bind_workspace(plan, ws, ws_bytes, sh)
             plan_ns.append(time.perf_counter_ns() - t0)
             live.append(plan)
@@ -390,6 +403,7 @@ def main(argv=None):
             "work_items": n_items,
             "merged_units": n_merges,
             "plan_every_step": not args.fixed_plan,
+            "cascade_prefix": use_cascade,
             "kv_pool_copies_rotated": rot.n if rot else 1,
         },
         "frac_hbm_peak": round(value * 1e3 / HBM_PEAK_GBPS, 4),

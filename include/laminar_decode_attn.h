@@ -111,6 +111,32 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
                                    const int32_t* seq_lens_host,
                                    int32_t num_cus, laminar_plan** out);
 
+/*
+ * Cascade plan for batches whose trajectories share prompt prefixes (the
+ * paper's GRPO groups: 16 responses per prompt, §8 "Settings"). Group
+ * g's members are the trajectories b with group_of_host[b] == g (-1: no
+ * group); the caller guarantees that blocks 0 .. group_pages_host[g] - 1 of
+ * every member (as far as the member is long) map to the same physical
+ * pages. The shared pages of up to waves_per_item x (16 / g_q) members
+ * (g_q = num_q_heads / num_kv_heads) are then read once per kv-head: one
+ * work item gives each wavefront the query rows of 16 / g_q members and
+ * masks each row at its member's length, and each member's result is the
+ * log-sum-exp merge of that partial with its own pages' partials. Exact:
+ * the result is the same attention as laminar_plan_create's, up to fp32
+ * rounding. Groups of one member, or with no shared page, decode as usual.
+ * All arrays are host memory read during the call. num_groups == 0 is
+ * laminar_plan_create.
+ * Errors: those of laminar_plan_create, and INVALID_ARG for num_groups < 0,
+ * NULL group arrays with num_groups > 0, group_of outside [-1, num_groups)
+ * or a negative group_pages entry.
+ */
+laminar_status laminar_plan_create_cascade(const laminar_attn_desc* desc,
+                                           const int32_t* seq_lens_host,
+                                           const int32_t* group_of_host,
+                                           int32_t num_groups,
+                                           const int32_t* group_pages_host,
+                                           int32_t num_cus, laminar_plan** out);
+
 /* Bytes of device workspace the plan needs (work list, merge list, partial
  * outputs). 0 for a NULL plan. */
 size_t laminar_plan_workspace_bytes(const laminar_plan* plan);
@@ -173,9 +199,13 @@ laminar_status laminar_decode_attn_merge(const laminar_plan* plan, float* out,
 /* Plan introspection (host only). Items are listed in launch order
  * (longest first, one workgroup each). Each item is 4 int32:
  * (b * num_kv_heads + kvh, first page, end page, partial slot or -1 when the
- * item writes out/lse directly). Each merge is 4 int32: (unit, first slot,
- * number of slots, 0). *_copy writes min(count, capacity) records and returns
- * the number written, or -1 for a NULL argument. */
+ * item writes out/lse directly), or for a cascade item (-(cascade unit) - 1,
+ * first page, end page, piece index). Each merge is 4 int32: (unit, first
+ * slot, number of slots, 0). Each cascade unit is 4 int32: (trajectory whose
+ * block-table row is read, member count, first member record, kv-head); each
+ * member record is 2 int32: (trajectory, first partial slot of its unit).
+ * *_copy writes min(count, capacity) records and returns the number written,
+ * or -1 for a NULL argument. */
 int32_t laminar_plan_num_items(const laminar_plan* plan);
 int32_t laminar_plan_num_merges(const laminar_plan* plan);
 int32_t laminar_plan_pages_per_item(const laminar_plan* plan);
@@ -184,6 +214,12 @@ int32_t laminar_plan_items_copy(const laminar_plan* plan, int32_t* dst,
                                 int32_t capacity);
 int32_t laminar_plan_merges_copy(const laminar_plan* plan, int32_t* dst,
                                  int32_t capacity);
+int32_t laminar_plan_num_cascade_units(const laminar_plan* plan);
+int32_t laminar_plan_num_cascade_members(const laminar_plan* plan);
+int32_t laminar_plan_cascade_units_copy(const laminar_plan* plan, int32_t* dst,
+                                        int32_t capacity);
+int32_t laminar_plan_cascade_members_copy(const laminar_plan* plan,
+                                          int32_t* dst, int32_t capacity);
 
 /* Free a plan (NULL is a no-op). Does not free the bound workspace. */
 void laminar_plan_destroy(laminar_plan* plan);

@@ -12,7 +12,10 @@ from ._native import (LaminarAttnDesc, LaminarError, laminar_decode_attn,
                       laminar_hbm_copy, laminar_hbm_read,
                       laminar_hbm_read_sink_floats, laminar_kv_append,
                       laminar_plan_bind_workspace,
-                      laminar_plan_create, laminar_plan_destroy,
+                      laminar_plan_cascade_members_copy,
+                      laminar_plan_cascade_units_copy,
+                      laminar_plan_create, laminar_plan_create_cascade,
+                      laminar_plan_destroy,
                       laminar_plan_items_copy, laminar_plan_merges_copy,
                       laminar_plan_num_items, laminar_plan_num_merges,
                       laminar_plan_pages_per_item, laminar_plan_waves_per_item,

@@ -56,6 +56,10 @@ _LIB = None
 _SIGNATURES = {
     "laminar_plan_create": (c_int32, [POINTER(LaminarAttnDesc), POINTER(c_int32),
                                       c_int32, POINTER(c_void_p)]),
+    "laminar_plan_create_cascade": (c_int32, [POINTER(LaminarAttnDesc),
+                                              POINTER(c_int32), POINTER(c_int32),
+                                              c_int32, POINTER(c_int32), c_int32,
+                                              POINTER(c_void_p)]),
     "laminar_plan_workspace_bytes": (c_size_t, [c_void_p]),
     "laminar_plan_bind_workspace": (c_int32, [c_void_p, c_void_p, c_size_t,
                                               c_void_p]),
@@ -70,6 +74,12 @@ _SIGNATURES = {
     "laminar_plan_waves_per_item": (c_int32, [c_void_p]),
     "laminar_plan_items_copy": (c_int32, [c_void_p, POINTER(c_int32), c_int32]),
     "laminar_plan_merges_copy": (c_int32, [c_void_p, POINTER(c_int32), c_int32]),
+    "laminar_plan_num_cascade_units": (c_int32, [c_void_p]),
+    "laminar_plan_num_cascade_members": (c_int32, [c_void_p]),
+    "laminar_plan_cascade_units_copy": (c_int32, [c_void_p, POINTER(c_int32),
+                                                  c_int32]),
+    "laminar_plan_cascade_members_copy": (c_int32, [c_void_p, POINTER(c_int32),
+                                                    c_int32]),
     "laminar_plan_destroy": (None, [c_void_p]),
     "laminar_status_string": (ctypes.c_char_p, [c_int32]),
     "laminar_hbm_read_sink_floats": (c_int32, []),
@@ -129,6 +139,20 @@ def laminar_plan_create(desc: LaminarAttnDesc, seq_lens_host, num_cus: int):
         ctypes.byref(desc), lens.ctypes.data_as(POINTER(c_int32)),
         int(num_cus), ctypes.byref(out))
     _check(st, "laminar_plan_create")
+    return out.value
+
+
+def laminar_plan_create_cascade(desc: LaminarAttnDesc, seq_lens_host,
+                                group_of_host, group_pages_host, num_cus: int):
+    lens = np.ascontiguousarray(seq_lens_host, dtype=np.int32)
+    grp = np.ascontiguousarray(group_of_host, dtype=np.int32)
+    pages = np.ascontiguousarray(group_pages_host, dtype=np.int32)
+    out = c_void_p()
+    st = lib().laminar_plan_create_cascade(
+        ctypes.byref(desc), lens.ctypes.data_as(POINTER(c_int32)),
+        grp.ctypes.data_as(POINTER(c_int32)), int(pages.size),
+        pages.ctypes.data_as(POINTER(c_int32)), int(num_cus), ctypes.byref(out))
+    _check(st, "laminar_plan_create_cascade")
     return out.value
 
 
@@ -193,6 +217,24 @@ def laminar_plan_merges_copy(plan) -> np.ndarray:
     n = laminar_plan_num_merges(plan)
     buf = np.zeros((max(n, 0), 4), dtype=np.int32)
     got = lib().laminar_plan_merges_copy(
+        plan, buf.ctypes.data_as(POINTER(c_int32)), n)
+    assert got == n
+    return buf
+
+
+def laminar_plan_cascade_units_copy(plan) -> np.ndarray:
+    n = int(lib().laminar_plan_num_cascade_units(plan))
+    buf = np.zeros((max(n, 0), 4), dtype=np.int32)
+    got = lib().laminar_plan_cascade_units_copy(
+        plan, buf.ctypes.data_as(POINTER(c_int32)), n)
+    assert got == n
+    return buf
+
+
+def laminar_plan_cascade_members_copy(plan) -> np.ndarray:
+    n = int(lib().laminar_plan_num_cascade_members(plan))
+    buf = np.zeros((max(n, 0), 2), dtype=np.int32)
+    got = lib().laminar_plan_cascade_members_copy(
         plan, buf.ctypes.data_as(POINTER(c_int32)), n)
     assert got == n
     return buf

@@ -31,7 +31,9 @@ class PagedDecodeAttention:
     """Plan + bound workspace for a batch with fixed trajectory lengths.
 
     ``seq_lens_host`` are the lengths the next calls will see. The plan is
-    reusable by every layer of the decode step.
+    reusable by every layer of the decode step. With ``group_of`` (group
+    index per trajectory, -1 for none) and ``group_pages`` (shared prefix
+    pages per group) the plan decodes each group's shared pages once.
     """
 
     def __init__(self, *, batch: int, num_q_heads: int, num_kv_heads: int,
@@ -40,7 +42,8 @@ class PagedDecodeAttention:
                  k_scale: Optional[torch.Tensor] = None,
                  v_scale: Optional[torch.Tensor] = None,
                  pages_per_item: int = 0, waves_per_item: int = 0,
-                 cus: Optional[int] = None, device="cuda", stream=None):
+                 cus: Optional[int] = None, device="cuda", stream=None,
+                 group_of=None, group_pages=None):
         self.desc = N.LaminarAttnDesc(
             batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
             head_dim=head_dim, page_size=16, num_pages=num_pages,
@@ -53,8 +56,13 @@ class PagedDecodeAttention:
         self._scales = (k_scale, v_scale)        # keep alive
         if cus is None:
             cus = num_cus(self.device) if self.device.type == "cuda" else 256
-        self.plan = N.laminar_plan_create(self.desc,
-                                          np.asarray(seq_lens_host), cus)
+        if group_of is None:
+            self.plan = N.laminar_plan_create(self.desc,
+                                              np.asarray(seq_lens_host), cus)
+        else:
+            self.plan = N.laminar_plan_create_cascade(
+                self.desc, np.asarray(seq_lens_host), group_of, group_pages,
+                cus)
         self.workspace_bytes = N.laminar_plan_workspace_bytes(self.plan)
         self.workspace = None
         if self.device.type == "cuda":

@@ -14,9 +14,16 @@
 //    high part and a bf16 low part, so P keeps about 16 bits of precision.
 //    The page layouts put every operand fragment in 16-byte runs, so no LDS
 //    staging or lane shuffles are needed; LDS is only used to combine the
-//    wavefronts of one item.
-//  * decode_merge: log-sum-exp merge of the partial (out, lse) records of
-//    trajectories whose pages were split over several items.
+//    wavefronts of one item. A cascade item (trajectories sharing a prompt
+//    prefix) instead gives each wavefront the rows of 16/g members and lets
+//    every wavefront walk all shared pages, so the pages are read from HBM
+//    once for all members (the other wavefronts hit L2); each row is masked
+//    at its own member's length.
+//  * decode_merge_rows / decode_merge_heads: log-sum-exp merge of the
+//    partial (out, lse) records of trajectories whose pages were split over
+//    several items (or whose shared prefix was decoded by a cascade item);
+//    one workgroup per record when records have few slots, one per
+//    (record, head) with the slots reduced in parallel otherwise.
 //  * hbm_read / hbm_copy: bandwidth calibration.
 
 #include <hip/hip_runtime.h>
@@ -39,6 +46,11 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
+// Mean partial slots per merge record up to which a workgroup per record
+// merges faster than a workgroup per (record, head): measured 7 against
+// 9 us on the agentic mix (2.2 slots per record) and 11 against 7 us on
+// post-repack (23 slots).
+constexpr int kRowsMergeMaxMeanSlots = 4;
 constexpr double kLn2d = 0.6931471805599453;
 
 struct DecodeArgs {
@@ -55,6 +67,8 @@ struct DecodeArgs {
   float* lse_part;
   const int4* items;
   const int4* merges;
+  const int4* cunits;     // cascade unit headers
+  const int2* cmembers;   // cascade member records
   int32_t hq, hkv, group, max_blocks, num_pages;
   float scale_log2;  // softmax_scale * log2(e)
   float scale;       // softmax_scale
@@ -85,6 +99,7 @@ struct PairRegs {
   u32x4 ka[G::KL], kb[G::KL];
   u32x4 va[G::VL], vb[G::VL];
   int nva, nvb;          // valid tokens in page A / B (0..16)
+  int base;              // token index of slot 0 of page A
   float ksa, ksb, vsa, vsb;
 };
 
@@ -193,15 +208,15 @@ struct ItemCtx {
   int b, kvh, len, p0, npages, slot;
 };
 
-__device__ __forceinline__ ItemCtx read_item(const DecodeArgs& a, int idx) {
-  const int4 it = a.items[idx];
+__device__ __forceinline__ ItemCtx item_ctx(const DecodeArgs& a, int unit,
+                                            int p0, int p1, int slot) {
   ItemCtx c;
-  c.b = it.x / a.hkv;
-  c.kvh = it.x - c.b * a.hkv;
+  c.b = unit / a.hkv;
+  c.kvh = unit - c.b * a.hkv;
   c.len = a.seq_lens[c.b];
-  c.p0 = it.y;
-  c.npages = max(min(it.z, (c.len + 15) >> 4) - c.p0, 0);
-  c.slot = it.w;
+  c.p0 = p0;
+  c.npages = max(min(p1, (c.len + 15) >> 4) - c.p0, 0);
+  c.slot = slot;
   return c;
 }
 
@@ -215,20 +230,19 @@ __device__ __forceinline__ int load_window(const DecodeArgs& a,
              : -1;
 }
 
-// Query fragment (B operand of QK^T): lane holds head r16 of the group,
-// dims (gq*KK + kk)*8 .. +7 for each step kk. Heads beyond the group are 0.
+// Query fragment (B operand of QK^T): lane holds the row of head slot r16
+// (query head h of trajectory b when ok, zero otherwise), dims
+// (gq*KK + kk)*8 .. +7 for each step kk.
 template <int D, bool FP8>
-__device__ __forceinline__ void load_q(const DecodeArgs& a, const ItemCtx& c,
-                                       int r16, int gq,
+__device__ __forceinline__ void load_q(const DecodeArgs& a, int b, int h,
+                                       bool ok, int gq,
                                        bf16x8 (&qf)[Geo<D, FP8>::KK]) {
   using G = Geo<D, FP8>;
-  const bool head_ok = r16 < a.group;
-  const int h = c.kvh * a.group + r16;
   const u32x4* qp = reinterpret_cast<const u32x4*>(
-      a.q + (size_t(c.b) * a.hq + (head_ok ? h : 0)) * D) + gq * G::KK;
+      a.q + (size_t(ok ? b : 0) * a.hq + (ok ? h : 0)) * D) + gq * G::KK;
 #pragma unroll
   for (int kk = 0; kk < G::KK; ++kk) {
-    const u32x4 v = head_ok ? qp[kk] : u4(0, 0, 0, 0);
+    const u32x4 v = ok ? qp[kk] : u4(0, 0, 0, 0);
     qf[kk] = __builtin_bit_cast(bf16x8, v);
   }
 }
@@ -252,6 +266,7 @@ __device__ __forceinline__ void issue_pair(const DecodeArgs& a,
   if (ppb < 0 || ppb >= a.num_pages) { ppb = 0; nvb = 0; }
   pr.nva = nva;
   pr.nvb = nvb;
+  pr.base = base_tok;
   const size_t page_stride = size_t(a.hkv) * G::TILE;
   const uint8_t* kbase = a.k_pages + size_t(c.kvh) * G::TILE;
   const uint8_t* vbase = a.v_pages + size_t(c.kvh) * G::TILE;
@@ -306,7 +321,8 @@ template <int D, bool FP8>
 __device__ __forceinline__ void compute_pair(const DecodeArgs& a,
                                              const bf16x8 (&qf)[Geo<D, FP8>::KK],
                                              PairRegs<D, FP8>& pr, Acc<D>& st,
-                                             int gq) {
+                                             int gq, bool rows,
+                                             const int* row_len_lds) {
   using G = Geo<D, FP8>;
   // Scores S^T[token][head] of both pages: lane holds head r16, tokens
   // 4gq..4gq+3 of page A (sa) and of page B (sb).
@@ -322,14 +338,28 @@ __device__ __forceinline__ void compute_pair(const DecodeArgs& a,
     sa *= pr.ksa;
     sb *= pr.ksb;
   }
-  if (pr.nva < 16 || pr.nvb < 16) {            // uniform: only at the tail
+  // Slots past the page's valid tokens score -inf, and so do slots past
+  // the length of this lane's row when rows belong to different members
+  // (`rows`, a cascade item; the lengths sit in LDS, not in registers).
+  if (rows || pr.nva < 16 || pr.nvb < 16) {    // uniform
+    int la = pr.nva, lb = pr.nvb;
+    if (rows) {
+      // this lane's row: entry (wavefront, head slot) of the LDS table
+      const int rl = __atomic_load_n(&row_len_lds[(threadIdx.x >> 6) * 16 +
+                                                  (threadIdx.x & 15)],
+                                     __ATOMIC_RELAXED) - pr.base;
+      la = min(la, rl);
+      lb = min(lb, rl - 16);
+    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      sa[r] = (4 * gq + r < pr.nva) ? sa[r] : -INFINITY;
-      sb[r] = (4 * gq + r < pr.nvb) ? sb[r] : -INFINITY;
+      sa[r] = (4 * gq + r < la) ? sa[r] : -INFINITY;
+      sb[r] = (4 * gq + r < lb) ? sb[r] : -INFINITY;
     }
-    zero_tail_v<D, FP8>(pr.va, pr.nva, gq);
-    zero_tail_v<D, FP8>(pr.vb, pr.nvb, gq);
+    if (pr.nva < 16 || pr.nvb < 16) {
+      zero_tail_v<D, FP8>(pr.va, pr.nva, gq);
+      zero_tail_v<D, FP8>(pr.vb, pr.nvb, gq);
+    }
   }
   float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])),
                    fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
@@ -394,29 +424,17 @@ __device__ __forceinline__ void compute_pair(const DecodeArgs& a,
   }
 }
 
-// Write the item's result: out/lse directly when the trajectory was not
-// split, else the partial record of its slot. st.l must already hold the
-// full denominator of head r16.
+// Write one query row's result (out or partial row `dst`, lse at `lse_dst`)
+// from lane (head slot, group gq). st.l must already hold the full
+// denominator of the row.
 template <int D, bool FP8>
-__device__ __forceinline__ void write_item(const DecodeArgs& a,
-                                           const ItemCtx& c, const Acc<D>& st,
-                                           int r16, int gq) {
+__device__ __forceinline__ void write_row(float* dst, float* lse_dst,
+                                          const Acc<D>& st, int gq) {
   using G = Geo<D, FP8>;
-  if (r16 >= a.group) return;
-  const int h = c.kvh * a.group + r16;
   const bool empty = !(st.l > 0.f);
   const float inv = empty ? 0.f : 1.0f / st.l;
   const float lse_v =
       empty ? -INFINITY : float(double(st.m) * kLn2d + log(double(st.l)));
-  float* dst;
-  float* lse_dst;
-  if (c.slot < 0) {
-    dst = a.out + (size_t(c.b) * a.hq + h) * D;
-    lse_dst = a.lse + size_t(c.b) * a.hq + h;
-  } else {
-    dst = a.o_part + (size_t(c.slot) * a.group + r16) * D;
-    lse_dst = a.lse_part + size_t(c.slot) * a.group + r16;
-  }
   // Row 4gq + r of tile n is dim vdim(n, 4gq + r): for each load j the lane
   // holds 4*DPL contiguous dims starting at j*16*DPL + 4gq*DPL, ordered
   // (r, e) with n = j*DPL + e.
@@ -437,13 +455,29 @@ __device__ __forceinline__ void write_item(const DecodeArgs& a,
   if (gq == 0) *lse_dst = lse_v;
 }
 
+// Result of an ordinary item: out/lse directly when the trajectory was not
+// split, else the partial record of its slot.
+template <int D, bool FP8>
+__device__ __forceinline__ void write_item(const DecodeArgs& a,
+                                           const ItemCtx& c, const Acc<D>& st,
+                                           int r16, int gq) {
+  if (r16 >= a.group) return;
+  const int h = c.kvh * a.group + r16;
+  if (c.slot < 0)
+    write_row<D, FP8>(a.out + (size_t(c.b) * a.hq + h) * D,
+                      a.lse + size_t(c.b) * a.hq + h, st, gq);
+  else
+    write_row<D, FP8>(a.o_part + (size_t(c.slot) * a.group + r16) * D,
+                      a.lse_part + size_t(c.slot) * a.group + r16, st, gq);
+}
+
 // One workgroup per work item (trajectory, kv-head, page range), in the
 // plan's longest-first order; the hardware dispatcher hands items to CUs as
 // workgroups finish. The WAVES wavefronts share the item's page pairs (wave
 // w takes pairs w, w+WAVES, ...), each keeping the next pair's loads in
 // flight while it computes the current one; the waves are combined through
 // LDS at the end and wave 0 writes the result.
-template <int D, bool FP8, int WAVES>
+template <int D, bool FP8, int WAVES, bool CASCADE>
 __global__ void __launch_bounds__(64 * WAVES)
 __attribute__((amdgpu_waves_per_eu(2)))
 decode_items(const DecodeArgs a) {
@@ -456,10 +490,38 @@ decode_items(const DecodeArgs a) {
     const int r16 = lane & 15, gq = lane >> 4;
     const int koff = gq * G::KL * 16 + r16;                    // u32x4 units
     const int voff = gq * D * G::EB / 4 + r16;                  // u32x4 units
-    const ItemCtx c = read_item(a, k);
-    const int npairs = (c.npages + 1) >> 1;
+    const int4 it = a.items[k];
+    // uniform; plans without cascade items run the CASCADE = false
+    // instantiation, which carries none of the cascade code
+    const bool cascade = CASCADE && it.x < 0;
+    ItemCtx c;
+    int4 cu = make_int4(0, 0, 0, 0);     // cascade unit header
+    // Tokens a cascade row may attend to (its member's length), kept in LDS
+    // rather than a register through the page loop; ordinary rows use c.len.
+    __shared__ int sm_row_len[WAVES * 16];
+    // page pairs of this wavefront: jp0, jp0 + stride, ...
+    int jp0 = wave, stride = WAVES;
     bf16x8 qf[G::KK];
-    load_q<D, FP8>(a, c, r16, gq, qf);
+    if (!cascade) {
+      c = item_ctx(a, it.x, it.y, it.z, it.w);
+      load_q<D, FP8>(a, c.b, c.kvh * a.group + r16, r16 < a.group, gq, qf);
+    } else {
+      // Cascade item: shared pages read through the longest member's table
+      // row; wavefront w holds the rows of members w*mw .. w*mw + mw - 1
+      // (mw = 16 / g), head r16 % g of member w*mw + r16 / g in lane r16.
+      cu = a.cunits[-it.x - 1];
+      c = item_ctx(a, cu.x * a.hkv + cu.w, it.y, it.z, it.w);
+      const int mw = 16 / a.group;
+      if (wave * mw >= cu.y) return;          // no members for this wave
+      const int mi = wave * mw + r16 / a.group;
+      const bool ok = r16 < mw * a.group && mi < cu.y;
+      const int rb = ok ? a.cmembers[cu.z + mi].x : 0;
+      if (gq == 0) sm_row_len[wave * 16 + r16] = ok ? a.seq_lens[rb] : 0;
+      jp0 = 0;
+      stride = 1;
+      load_q<D, FP8>(a, rb, c.kvh * a.group + r16 % a.group, ok, gq, qf);
+    }
+    const int npairs = (c.npages + 1) >> 1;
     Acc<D> st;
     st.reset();
 
@@ -474,23 +536,35 @@ decode_items(const DecodeArgs a) {
     };
 
     PairRegs<D, FP8> buf0, buf1;
-    int jp = wave;
+    int jp = jp0;
     if (jp < npairs) issue(buf0, jp);
     while (jp < npairs) {
-      int jn = jp + WAVES;
+      int jn = jp + stride;
       if (jn < npairs) issue(buf1, jn);
-      compute_pair<D, FP8>(a, qf, buf0, st, gq);
+      compute_pair<D, FP8>(a, qf, buf0, st, gq, cascade, sm_row_len);
       jp = jn;
       if (jp >= npairs) break;
-      jn = jp + WAVES;
+      jn = jp + stride;
       if (jn < npairs) issue(buf0, jn);
-      compute_pair<D, FP8>(a, qf, buf1, st, gq);
+      compute_pair<D, FP8>(a, qf, buf1, st, gq, cascade, sm_row_len);
       jp = jn;
     }
 
     // Full softmax denominator of head r16 over this wave's pages.
     st.l += __shfl_xor(st.l, 16);
     st.l += __shfl_xor(st.l, 32);
+
+    if (cascade) {                 // each wavefront owns its rows: no combine
+      const int mw = 16 / a.group;
+      const int mi = wave * mw + r16 / a.group;
+      if (r16 < mw * a.group && mi < cu.y) {
+        const int slot = a.cmembers[cu.z + mi].y + c.slot;
+        const int i = r16 % a.group;
+        write_row<D, FP8>(a.o_part + (size_t(slot) * a.group + i) * D,
+                          a.lse_part + size_t(slot) * a.group + i, st, gq);
+      }
+      return;
+    }
 
     if constexpr (WAVES > 1) {
       __shared__ float sm_m[WAVES][16];
@@ -549,9 +623,54 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// One workgroup per (split trajectory unit, head of the group).
+// Merge for records with few slots (cascade members: the shared prefix's
+// partial and one or two of their own): one workgroup per merge record;
+// thread (head i, column c) merges the n partial rows of head i for dims
+// 4c..4c+3. The lse values of a head are read by its D/4 threads together
+// (one cache line), and every load's address is known up front, so the
+// loops keep many loads in flight.
 template <int D>
-__global__ void __launch_bounds__(256) decode_merge(const DecodeArgs a) {
+__global__ void __launch_bounds__(256) decode_merge_rows(const DecodeArgs a) {
+  constexpr int C = D / 4;          // float4 columns per row
+  const int4 mg = a.merges[blockIdx.x];
+  const int unit = mg.x, slot0 = mg.y, n = mg.z;
+  const int b = unit / a.hkv;
+  const int kvh = unit - b * a.hkv;
+  for (int t = threadIdx.x; t < a.group * C; t += 256) {
+    const int i = t / C, c = t - i * C;
+    const float* lp = a.lse_part + size_t(slot0) * a.group + i;
+    const float4* op =
+        reinterpret_cast<const float4*>(a.o_part + (size_t(slot0) * a.group + i) * D) + c;
+    const size_t ostride = size_t(a.group) * C;        // float4 per slot
+    float mx = -INFINITY;
+#pragma unroll 4
+    for (int s = 0; s < n; ++s) mx = fmaxf(mx, lp[size_t(s) * a.group]);
+    float sum = 0.f;
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (mx != -INFINITY) {
+#pragma unroll 4
+      for (int s = 0; s < n; ++s) {
+        const float w = expf(lp[size_t(s) * a.group] - mx);   // 0 for -inf
+        const float4 v = op[size_t(s) * ostride];
+        sum += w;
+        o.x = fmaf(w, v.x, o.x); o.y = fmaf(w, v.y, o.y);
+        o.z = fmaf(w, v.z, o.z); o.w = fmaf(w, v.w, o.w);
+      }
+    }
+    const int h = kvh * a.group + i;
+    const float inv = mx == -INFINITY ? 0.f : 1.0f / sum;
+    reinterpret_cast<float4*>(a.out + (size_t(b) * a.hq + h) * D)[c] =
+        make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv);
+    if (c == 0) a.lse[size_t(b) * a.hq + h] = mx == -INFINITY ? -INFINITY
+                                                              : mx + logf(sum);
+  }
+}
+
+// Merge with the slots in parallel, for records with many slots: one
+// workgroup per (merge record, head of the group); 256 / (D/4) partial rows
+// are reduced side by side and combined through LDS.
+template <int D>
+__global__ void __launch_bounds__(256) decode_merge_heads(const DecodeArgs a) {
   constexpr int C = D / 4;          // threads per partial row (float4 each)
   constexpr int SPAR = 256 / C;     // partial rows reduced in parallel
   __shared__ float red[4];
@@ -657,22 +776,32 @@ unsigned calib_grid(size_t n16) {
                                                    : size_t(kReadSinkFloats));
 }
 
-template <int D, bool FP8>
-hipError_t launch_partial(const laminar_plan* p, const DecodeArgs& a,
-                          hipStream_t stream) {
+template <int D, bool FP8, bool CASCADE>
+hipError_t launch_items(const laminar_plan* p, const DecodeArgs& a,
+                        hipStream_t stream) {
   const dim3 grid(p->num_items);
   switch (p->waves) {
     case 1:
-      hipLaunchKernelGGL((decode_items<D, FP8, 1>), grid, dim3(64), 0, stream, a);
+      hipLaunchKernelGGL((decode_items<D, FP8, 1, CASCADE>), grid, dim3(64), 0,
+                         stream, a);
       break;
     case 2:
-      hipLaunchKernelGGL((decode_items<D, FP8, 2>), grid, dim3(128), 0, stream, a);
+      hipLaunchKernelGGL((decode_items<D, FP8, 2, CASCADE>), grid, dim3(128), 0,
+                         stream, a);
       break;
     default:
-      hipLaunchKernelGGL((decode_items<D, FP8, 4>), grid, dim3(256), 0, stream, a);
+      hipLaunchKernelGGL((decode_items<D, FP8, 4, CASCADE>), grid, dim3(256), 0,
+                         stream, a);
       break;
   }
   return hipGetLastError();
+}
+
+template <int D, bool FP8>
+hipError_t launch_partial(const laminar_plan* p, const DecodeArgs& a,
+                          hipStream_t stream) {
+  return p->num_cascade_units > 0 ? launch_items<D, FP8, true>(p, a, stream)
+                                  : launch_items<D, FP8, false>(p, a, stream);
 }
 
 DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
@@ -692,6 +821,8 @@ DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
   a.lse = lse;
   a.items = reinterpret_cast<const int4*>(ws + p->off_items);
   a.merges = reinterpret_cast<const int4*>(ws + p->off_merges);
+  a.cunits = reinterpret_cast<const int4*>(ws + p->off_cunits);
+  a.cmembers = reinterpret_cast<const int2*>(ws + p->off_cmembers);
   a.lse_part = reinterpret_cast<float*>(ws + p->off_lse);
   a.o_part = reinterpret_cast<float*>(ws + p->off_o);
   a.hq = d.num_q_heads;
@@ -728,11 +859,21 @@ laminar_status run_partial(const laminar_plan* p, const DecodeArgs& a,
 laminar_status run_merge(const laminar_plan* p, const DecodeArgs& a,
                          hipStream_t stream) {
   if (p->num_merges == 0) return LAMINAR_OK;
-  const dim3 grid(p->num_merges, p->group);
-  if (p->desc.head_dim == 128)
-    hipLaunchKernelGGL((decode_merge<128>), grid, dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL((decode_merge<64>), grid, dim3(256), 0, stream, a);
+  // Few slots per record: a workgroup per record; many: a workgroup per
+  // (record, head) reducing slots in parallel.
+  const bool rows = p->num_slots <= kRowsMergeMaxMeanSlots * p->num_merges;
+  const dim3 grid = rows ? dim3(p->num_merges) : dim3(p->num_merges, p->group);
+  if (p->desc.head_dim == 128) {
+    if (rows)
+      hipLaunchKernelGGL((decode_merge_rows<128>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_merge_heads<128>), grid, dim3(256), 0, stream, a);
+  } else {
+    if (rows)
+      hipLaunchKernelGGL((decode_merge_rows<64>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_merge_heads<64>), grid, dim3(256), 0, stream, a);
+  }
   return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
 }
 

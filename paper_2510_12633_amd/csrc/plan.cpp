@@ -49,16 +49,53 @@ laminar_status validate(const laminar_attn_desc* d, const int32_t* lens,
   return LAMINAR_OK;
 }
 
-}  // namespace
+laminar_status validate_groups(const laminar_attn_desc* d,
+                               const int32_t* group_of, int32_t num_groups,
+                               const int32_t* group_pages) {
+  if (num_groups < 0) return LAMINAR_ERR_INVALID_ARG;
+  if (num_groups > 0 && (!group_of || !group_pages))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (num_groups == 0) return LAMINAR_OK;
+  for (int32_t b = 0; b < d->batch; ++b)
+    if (group_of[b] < -1 || group_of[b] >= num_groups)
+      return LAMINAR_ERR_INVALID_ARG;
+  for (int32_t g = 0; g < num_groups; ++g)
+    if (group_pages[g] < 0) return LAMINAR_ERR_INVALID_ARG;
+  return LAMINAR_OK;
+}
 
-extern "C" {
+// Near-equal page-aligned cut of `pages` into ceil(pages / cap) pieces, the
+// first pages % n of them one page longer (one empty piece for 0 pages).
+struct Cut {
+  uint32_t n, base, rem;
+  Cut() : n(1), base(0), rem(0) {}
+  Cut(uint32_t pages, uint32_t cap) {
+    n = pages == 0 ? 1 : (pages - 1) / cap + 1;
+    base = pages / n;
+    rem = pages - base * n;
+  }
+  uint32_t size(uint32_t i) const { return base + (i < rem ? 1u : 0u); }
+};
 
-laminar_status laminar_plan_create(const laminar_attn_desc* desc,
-                                   const int32_t* seq_lens_host,
-                                   int32_t num_cus, laminar_plan** out) {
+// One group chunk that is decoded as a cascade: up to waves x (16 / g)
+// members whose first `pages` blocks map to the same physical pages.
+struct Chunk {
+  std::vector<int32_t> members;   // trajectory indices, increasing
+  int32_t row;                    // longest member: its table row is read,
+                                  // its length bounds every row's tokens
+  uint32_t pages;                 // shared pages decoded once
+  Cut cut;
+};
+
+laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
+                     const int32_t* group_of, int32_t num_groups,
+                     const int32_t* group_pages, int32_t num_cus,
+                     laminar_plan** out) {
   if (!out) return LAMINAR_ERR_INVALID_ARG;
   *out = nullptr;
-  laminar_status st = validate(desc, seq_lens_host, num_cus);
+  laminar_status st = validate(desc, lens, num_cus);
+  if (st != LAMINAR_OK) return st;
+  st = validate_groups(desc, group_of, num_groups, group_pages);
   if (st != LAMINAR_OK) return st;
 
   laminar_plan* p = new (std::nothrow) laminar_plan();
@@ -69,13 +106,53 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   p->group = desc->num_q_heads / hkv;
   p->waves = desc->waves_per_item ? desc->waves_per_item
                                   : laminar_detail::kDefaultWaves;
-  int64_t work = 0;                        // (page, kv-head) tiles
-  for (int32_t b = 0; b < B; ++b)
-    work += (int64_t(seq_lens_host[b]) + 15) / 16 * hkv;
-  const int64_t resident = int64_t(num_cus) *
-      std::max(1, laminar_detail::kResidentWavesPerCU / p->waves);
-  const int64_t step = 2 * int64_t(p->waves);   // one page pair per wave
+  const int32_t W = p->waves;
+  std::vector<uint32_t> pages(static_cast<size_t>(B));
+  for (int32_t b = 0; b < B; ++b) pages[size_t(b)] = (uint32_t(lens[b]) + 15) / 16;
 
+  // Cascade chunks. A chunk item gives each of its W wavefronts the rows of
+  // 16 / g members and walks every shared page in each wavefront, so one
+  // item reads the shared pages once for W * (16 / g) members. Chunks of
+  // fewer than two members, or with nothing shared, decode as usual.
+  std::vector<Chunk> chunks;
+  std::vector<uint32_t> first(static_cast<size_t>(B), 0);   // first own page
+  std::vector<int32_t> chunk_of(static_cast<size_t>(B), -1);
+  if (num_groups > 0) {
+    const int32_t cap = W * (16 / p->group);
+    std::vector<std::vector<int32_t>> groups(static_cast<size_t>(num_groups));
+    for (int32_t b = 0; b < B; ++b)
+      if (group_of[b] >= 0) groups[size_t(group_of[b])].push_back(b);
+    for (int32_t g = 0; g < num_groups; ++g) {
+      const auto& m = groups[size_t(g)];
+      for (size_t s = 0; s < m.size(); s += size_t(cap)) {
+        Chunk c;
+        c.members.assign(m.begin() + long(s),
+                         m.begin() + long(std::min(m.size(), s + size_t(cap))));
+        // the member with the most tokens: its length bounds the valid
+        // slots of every shared page, for all rows
+        c.row = c.members[0];
+        for (int32_t b : c.members)
+          if (lens[b] > lens[c.row]) c.row = b;
+        c.pages = std::min(uint32_t(group_pages[g]), pages[size_t(c.row)]);
+        if (c.members.size() < 2 || c.pages == 0) continue;
+        for (int32_t b : c.members) {
+          first[size_t(b)] = std::min(pages[size_t(b)], c.pages);
+          chunk_of[size_t(b)] = int32_t(chunks.size());
+        }
+        chunks.push_back(std::move(c));
+      }
+    }
+  }
+
+  // Split size. Work is counted in wavefront-time: a page of an ordinary
+  // item costs 1 (its W wavefronts share the pages), a page of a cascade
+  // item costs W (each wavefront walks it for its own rows).
+  int64_t work = 0;
+  for (int32_t b = 0; b < B; ++b) work += int64_t(pages[size_t(b)] - first[size_t(b)]) * hkv;
+  for (const Chunk& c : chunks) work += int64_t(c.pages) * hkv * W;
+  const int64_t resident = int64_t(num_cus) *
+      std::max(1, laminar_detail::kResidentWavesPerCU / W);
+  const int64_t step = 2 * int64_t(W);          // one page pair per wave
   int64_t chunk;
   if (desc->pages_per_item > 0) {
     chunk = desc->pages_per_item;
@@ -88,40 +165,52 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
     chunk = (chunk + step - 1) / step * step;
   }
   p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
-
-  // Near-equal page-aligned pieces of every unit (trajectory, kv-head):
-  // n = ceil(pages / chunk) pieces, the first pages % n of them one page
-  // longer; all kv-heads of a trajectory are cut alike. A unit cut into
-  // several pieces gets n consecutive partial slots in page order and one
-  // merge record; a unit in one piece writes out/lse directly.
-  struct Cut { uint32_t n, base, rem; };
-  std::vector<Cut> cuts(static_cast<size_t>(B));
   const uint32_t chunk32 = uint32_t(std::min<int64_t>(chunk, UINT32_MAX));
-  int64_t total = 0, merges = 0, slots = 0;
-  uint32_t longest = 0;
+  // cascade pieces: the same wavefront-time, whole page pairs
+  const uint32_t cchunk =
+      std::max<uint32_t>(2, uint32_t(std::min<int64_t>(chunk / W, UINT32_MAX)) & ~1u);
+  for (Chunk& c : chunks) c.cut = Cut(c.pages, cchunk);
+
+  std::vector<Cut> cuts(static_cast<size_t>(B));
+  int64_t total = 0, merges = 0, slots = 0, members = 0;
+  uint32_t longest = 0;                          // longest item, wave-time
   for (int32_t b = 0; b < B; ++b) {
-    const uint32_t pages = (uint32_t(seq_lens_host[b]) + 15) / 16;  // < 2^27
-    const uint32_t n = pages == 0 ? 1 : (pages - 1) / chunk32 + 1;
-    const uint32_t base = pages / n;
-    const uint32_t rem = pages - base * n;
-    cuts[size_t(b)] = {n, base, rem};
-    total += int64_t(n) * hkv;
-    longest = std::max(longest, base + (rem ? 1 : 0));
-    if (n > 1) {
+    const uint32_t own = pages[size_t(b)] - first[size_t(b)];
+    const bool cas = chunk_of[size_t(b)] >= 0;
+    // a cascade member with nothing of its own has no ordinary item
+    Cut c = (cas && own == 0) ? Cut() : Cut(own, chunk32);
+    if (cas && own == 0) c.n = 0;
+    cuts[size_t(b)] = c;
+    total += int64_t(c.n) * hkv;
+    if (c.n) longest = std::max(longest, c.size(0));
+    const int64_t n_all = c.n + (cas ? chunks[size_t(chunk_of[size_t(b)])].cut.n : 0);
+    if (cas || n_all > 1) {
       merges += hkv;
-      slots += int64_t(n) * hkv;
+      slots += n_all * hkv;
     }
   }
-  if (total > INT32_MAX || slots > INT32_MAX) throw std::length_error("items");
+  for (const Chunk& c : chunks) {
+    total += int64_t(c.cut.n) * hkv;
+    longest = std::max<uint32_t>(longest, uint32_t(W) * c.cut.size(0));
+    members += int64_t(c.members.size()) * hkv;
+  }
+  if (total > INT32_MAX || slots > INT32_MAX || members > INT32_MAX)
+    throw std::length_error("items");
 
   p->num_items = int32_t(total);
   p->num_merges = int32_t(merges);
   p->num_slots = int32_t(slots);
+  p->num_cascade_units = int32_t(chunks.size()) * hkv;
+  p->num_cascade_members = int32_t(members);
   size_t off = 0;
   p->off_items = off;
   off = align256(off + size_t(total) * 16);
   p->off_merges = off;
   off = align256(off + size_t(merges) * 16);
+  p->off_cunits = off;
+  off = align256(off + size_t(p->num_cascade_units) * 16);
+  p->off_cmembers = off;
+  off = align256(off + size_t(members) * 8);
   p->off_lse = off;
   off = align256(off + size_t(slots) * p->group * sizeof(float));
   p->off_o = off;
@@ -129,34 +218,75 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   p->ws_bytes = off;
 
   // The tables are built in place in the byte image of the workspace up to
-  // the partial results (items, then merges, at their section offsets).
+  // the partial results.
   p->tables.assign(p->off_lse / sizeof(int32_t), 0);
   Item* items = reinterpret_cast<Item*>(p->tables.data() + p->off_items / 4);
   Item* mrec = reinterpret_cast<Item*>(p->tables.data() + p->off_merges / 4);
+  Item* cunit = reinterpret_cast<Item*>(p->tables.data() + p->off_cunits / 4);
+  int32_t* cmem = p->tables.data() + p->off_cmembers / 4;
 
-  // Launch order: longest first; equal lengths keep (trajectory, kv-head,
-  // page) order. The hardware dispatcher hands the workgroups to CUs
-  // greedily as earlier ones finish. A stable counting sort on the length.
+  // Launch order: longest (in wavefront-time) first; equal lengths keep
+  // (cascade units, then trajectory, kv-head, page) order. The hardware
+  // dispatcher hands the workgroups to CUs greedily as earlier ones finish.
+  // A stable counting sort on the length.
   std::vector<int64_t> start(size_t(longest) + 2, 0);
+  for (const Chunk& c : chunks)
+    for (uint32_t i = 0; i < c.cut.n; ++i) start[longest - W * c.cut.size(i)] += hkv;
   for (const Cut& c : cuts) {
+    if (c.n == 0) continue;
     start[longest - c.base] += int64_t(c.n - c.rem) * hkv;
     if (c.rem) start[longest - c.base - 1] += int64_t(c.rem) * hkv;
   }
   int64_t acc = 0;
   for (auto& v : start) { const int64_t c = v; v = acc; acc += c; }
+
+  // Slots: every unit of a cascade member, and every other unit cut into
+  // several pieces, gets consecutive partial slots (cascade pieces first,
+  // then its own pieces in page order) and one merge record.
+  std::vector<int32_t> slot0(size_t(B) * hkv, -1);
   int32_t next_slot = 0, m = 0;
   for (int64_t u = 0; u < int64_t(B) * hkv; ++u) {
-    const Cut c = cuts[size_t(u / hkv)];
-    const bool split = c.n > 1;
-    if (split) mrec[m++] = {int32_t(u), next_slot, int32_t(c.n), 0};
-    int32_t pos = 0;
+    const int32_t b = int32_t(u / hkv);
+    const Cut& c = cuts[size_t(b)];
+    const int32_t ci = chunk_of[size_t(b)];
+    const uint32_t ncas = ci >= 0 ? chunks[size_t(ci)].cut.n : 0;
+    const int32_t n_all = int32_t(c.n + ncas);
+    const bool merged = ci >= 0 || n_all > 1;
+    if (merged) {
+      slot0[size_t(u)] = next_slot;
+      mrec[m++] = {int32_t(u), next_slot, n_all, 0};
+    }
+    int32_t pos = int32_t(first[size_t(b)]);
     for (uint32_t i = 0; i < c.n; ++i) {
-      const uint32_t sz = c.base + (i < c.rem ? 1 : 0);
-      items[start[longest - sz]++] = {int32_t(u), pos, pos + int32_t(sz),
-                                      split ? next_slot + int32_t(i) : -1};
+      const uint32_t sz = c.size(i);
+      items[start[longest - sz]++] = {
+          int32_t(u), pos, pos + int32_t(sz),
+          merged ? next_slot + int32_t(ncas + i) : -1};
       pos += int32_t(sz);
     }
-    if (split) next_slot += int32_t(c.n);
+    if (merged) next_slot += n_all;
+  }
+  // Cascade units (chunk, kv-head): header (row, members, first member
+  // record, kv-head) and member records (trajectory, first slot).
+  int32_t mo = 0;
+  for (size_t ci = 0; ci < chunks.size(); ++ci) {
+    const Chunk& c = chunks[ci];
+    for (int32_t h = 0; h < hkv; ++h) {
+      const int32_t cu = int32_t(ci) * hkv + h;
+      cunit[cu] = {c.row, int32_t(c.members.size()), mo, h};
+      for (int32_t b : c.members) {
+        cmem[2 * mo] = b;
+        cmem[2 * mo + 1] = slot0[size_t(b) * hkv + h];
+        ++mo;
+      }
+      int32_t pos = 0;
+      for (uint32_t i = 0; i < c.cut.n; ++i) {
+        const uint32_t sz = c.cut.size(i);
+        items[start[longest - W * sz]++] = {-(cu + 1), pos, pos + int32_t(sz),
+                                            int32_t(i)};
+        pos += int32_t(sz);
+      }
+    }
   }
   } catch (...) {     // host allocation failure or too many items: report
     delete p;
@@ -164,6 +294,26 @@ laminar_status laminar_plan_create(const laminar_attn_desc* desc,
   }
   *out = p;
   return LAMINAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+laminar_status laminar_plan_create(const laminar_attn_desc* desc,
+                                   const int32_t* seq_lens_host,
+                                   int32_t num_cus, laminar_plan** out) {
+  return build(desc, seq_lens_host, nullptr, 0, nullptr, num_cus, out);
+}
+
+laminar_status laminar_plan_create_cascade(const laminar_attn_desc* desc,
+                                           const int32_t* seq_lens_host,
+                                           const int32_t* group_of_host,
+                                           int32_t num_groups,
+                                           const int32_t* group_pages_host,
+                                           int32_t num_cus, laminar_plan** out) {
+  return build(desc, seq_lens_host, group_of_host, num_groups,
+               group_pages_host, num_cus, out);
 }
 
 size_t laminar_plan_workspace_bytes(const laminar_plan* plan) {
@@ -199,6 +349,30 @@ int32_t laminar_plan_merges_copy(const laminar_plan* plan, int32_t* dst,
   if (!plan || !dst || capacity < 0) return -1;
   const int32_t n = std::min(capacity, plan->num_merges);
   std::memcpy(dst, plan->tables.data() + plan->off_merges / 4, size_t(n) * 16);
+  return n;
+}
+
+int32_t laminar_plan_num_cascade_units(const laminar_plan* plan) {
+  return plan ? plan->num_cascade_units : -1;
+}
+
+int32_t laminar_plan_num_cascade_members(const laminar_plan* plan) {
+  return plan ? plan->num_cascade_members : -1;
+}
+
+int32_t laminar_plan_cascade_units_copy(const laminar_plan* plan, int32_t* dst,
+                                        int32_t capacity) {
+  if (!plan || !dst || capacity < 0) return -1;
+  const int32_t n = std::min(capacity, plan->num_cascade_units);
+  std::memcpy(dst, plan->tables.data() + plan->off_cunits / 4, size_t(n) * 16);
+  return n;
+}
+
+int32_t laminar_plan_cascade_members_copy(const laminar_plan* plan,
+                                          int32_t* dst, int32_t capacity) {
+  if (!plan || !dst || capacity < 0) return -1;
+  const int32_t n = std::min(capacity, plan->num_cascade_members);
+  std::memcpy(dst, plan->tables.data() + plan->off_cmembers / 4, size_t(n) * 8);
   return n;
 }
 

@@ -1,7 +1,8 @@
 // Host-planner driver for the address and undefined-behaviour sanitizers.
-// Builds with g++ alone (no HIP): exercises laminar_plan_create over random
-// and edge-case batches, checks that every (trajectory, kv-head, page) is
-// covered exactly once, and frees every plan.
+// Builds with g++ alone (no HIP): exercises laminar_plan_create and
+// laminar_plan_create_cascade over random and edge-case batches, checks that
+// every (trajectory, kv-head, page) is covered exactly once, and frees every
+// plan.
 #include <cstdio>
 #include <cstdlib>
 #include <random>
@@ -14,7 +15,9 @@ static int fail(const char* what) {
   return 1;
 }
 
-static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves) {
+static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves,
+                 const std::vector<int32_t>* group_of = nullptr,
+                 const std::vector<int32_t>* group_pages = nullptr) {
   laminar_attn_desc d = {};
   d.batch = int32_t(lens.size());
   d.num_q_heads = hkv * 4;
@@ -28,8 +31,19 @@ static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves) 
   d.pages_per_item = ppi;
   d.waves_per_item = waves;
   laminar_plan* p = nullptr;
-  if (laminar_plan_create(&d, lens.data(), 256, &p) != LAMINAR_OK || !p)
-    return fail("create");
+  const laminar_status st =
+      group_of ? laminar_plan_create_cascade(
+                     &d, lens.data(), group_of->data(),
+                     int32_t(group_pages->size()), group_pages->data(), 256, &p)
+               : laminar_plan_create(&d, lens.data(), 256, &p);
+  if (st != LAMINAR_OK || !p) return fail("create");
+  const int nc = laminar_plan_num_cascade_units(p);
+  const int nm = laminar_plan_num_cascade_members(p);
+  std::vector<int32_t> cunits(size_t(4) * (nc > 0 ? nc : 1));
+  std::vector<int32_t> cmem(size_t(2) * (nm > 0 ? nm : 1));
+  if (laminar_plan_cascade_units_copy(p, cunits.data(), nc) != nc ||
+      laminar_plan_cascade_members_copy(p, cmem.data(), nm) != nm)
+    return fail("cascade copy");
   const int n = laminar_plan_num_items(p);
   std::vector<int32_t> items(size_t(4) * (n > 0 ? n : 1));
   if (laminar_plan_items_copy(p, items.data(), n) != n) return fail("copy");
@@ -38,7 +52,24 @@ static int check(const std::vector<int32_t>& lens, int hkv, int ppi, int waves) 
     seen[u].assign((lens[u / hkv] + 15) / 16, 0);
   for (int i = 0; i < n; ++i) {
     const int unit = items[4 * i], p0 = items[4 * i + 1], p1 = items[4 * i + 2];
-    if (unit < 0 || size_t(unit) >= seen.size()) return fail("unit");
+    if (unit < 0) {                       // cascade item: every member
+      const int cu = -unit - 1;
+      if (cu >= nc) return fail("cascade unit");
+      const int cnt = cunits[4 * cu + 1], moff = cunits[4 * cu + 2];
+      const int kvh = cunits[4 * cu + 3];
+      if (moff < 0 || moff + cnt > nm || kvh < 0 || kvh >= hkv)
+        return fail("cascade header");
+      for (int j = 0; j < cnt; ++j) {
+        const size_t u = size_t(cmem[2 * (moff + j)]) * hkv + kvh;
+        if (u >= seen.size() || p0 < 0 || p0 > p1) return fail("cascade member");
+        for (int q = p0; q < p1 && q < int(seen[u].size()); ++q) {
+          if (seen[u][q]) return fail("double cover (cascade)");
+          seen[u][q] = 1;
+        }
+      }
+      continue;
+    }
+    if (size_t(unit) >= seen.size()) return fail("unit");
     if (p0 < 0 || p1 > int(seen[unit].size()) || p0 > p1) return fail("range");
     for (int q = p0; q < p1; ++q) {
       if (seen[unit][q]) return fail("double cover");
@@ -70,6 +101,14 @@ int main() {
     const int ppis[] = {0, 1, 2, 7, 64, 1 << 20};
     const int waves[] = {0, 1, 2, 4};
     if (check(lens, hkv, ppis[rng() % 6], waves[rng() % 4])) return 1;
+    // the same batch with random groups sharing random prefixes
+    const int ng = 1 + int(rng() % 40);
+    std::vector<int32_t> group_of(b), group_pages(ng);
+    for (auto& g : group_of) g = int32_t(rng() % (ng + 1)) - 1;
+    for (auto& g : group_pages) g = int32_t(rng() % 200);
+    if (check(lens, hkv, ppis[rng() % 6], waves[rng() % 4], &group_of,
+              &group_pages))
+      return 1;
   }
   // argument errors must not touch the output or leak
   laminar_plan* p = reinterpret_cast<laminar_plan*>(0x1);

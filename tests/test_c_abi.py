@@ -218,6 +218,142 @@ def test_call_errors_before_any_launch():
     assert lib.laminar_plan_workspace_bytes(None) == 0
 
 
+def cascade_tables(d, lens, group_of, group_pages, cus=256):
+    p = N.laminar_plan_create_cascade(d, np.asarray(lens, np.int32),
+                                      np.asarray(group_of, np.int32),
+                                      np.asarray(group_pages, np.int32), cus)
+    try:
+        return (N.laminar_plan_items_copy(p), N.laminar_plan_merges_copy(p),
+                N.laminar_plan_cascade_units_copy(p),
+                N.laminar_plan_cascade_members_copy(p),
+                N.laminar_plan_waves_per_item(p))
+    finally:
+        N.laminar_plan_destroy(p)
+
+
+def check_cascade_plan(lens, hkv, g, group_of, group_pages, items, merges,
+                       cunits, cmembers, waves):
+    """Every (trajectory, kv-head, page) exactly once, by its own item or by
+    a cascade item of a chunk it belongs to; chunk and slot structure."""
+    lens = np.asarray(lens, np.int64)
+    pages = -(-lens // 16)
+    cap = waves * (16 // g)
+    covered = {}
+    slot_of = {}                     # (unit) -> list of (first page, slot)
+    members_of = []
+    for cu, (row, cnt, moff, kvh) in enumerate(cunits):
+        mem = cmembers[moff:moff + cnt]
+        bs = [int(b) for b in mem[:, 0]]
+        assert 2 <= cnt <= cap and bs == sorted(bs)
+        grp = {int(group_of[b]) for b in bs}
+        assert len(grp) == 1 and -1 not in grp
+        # the row read is the member with the most tokens (not just pages)
+        assert int(row) in bs and lens[row] == max(lens[b] for b in bs)
+        members_of.append((bs, mem[:, 1], int(kvh)))
+    cost = []
+    for unit, p0, p1, slot in items:
+        if unit >= 0:
+            b, h = divmod(int(unit), hkv)
+            assert 0 <= p0 <= p1 <= pages[b]
+            for pg in range(p0, p1):
+                assert (b, h, pg) not in covered
+                covered[(b, h, pg)] = True
+            slot_of.setdefault(int(unit), []).append((int(p0), int(slot)))
+            cost.append(int(p1 - p0))
+        else:
+            bs, slot0s, h = members_of[-unit - 1]
+            for b, s0 in zip(bs, slot0s):
+                for pg in range(p0, min(p1, pages[b])):
+                    assert (b, h, pg) not in covered
+                    covered[(b, h, pg)] = True
+                slot_of.setdefault(b * hkv + h, []).append((-1, int(s0 + slot)))
+            cost.append(waves * int(p1 - p0))
+    assert len(covered) == int(pages.sum()) * hkv
+    assert cost == sorted(cost, reverse=True)
+    merged = {int(m[0]): (int(m[1]), int(m[2])) for m in merges}
+    all_slots = []
+    for unit, lst in slot_of.items():
+        if unit in merged:
+            s0, n = merged[unit]
+            assert n == len(lst)
+            # cascade pieces first, then own pieces in page order
+            got = [s for _, s in sorted(lst, key=lambda x: (x[0], x[1]))]
+            assert got == list(range(s0, s0 + n)), (unit, lst, s0, n)
+            all_slots += got
+        else:
+            assert len(lst) == 1 and lst[0][1] == -1
+    assert len(all_slots) == len(set(all_slots))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_cascade_planner_invariants_random(seed):
+    rng = np.random.default_rng(100 + seed)
+    b = int(rng.integers(1, 200))
+    lens = rng.integers(0, 6000, b)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    g = int(rng.choice([1, 2, 5, 7, 8, 16]))
+    n_groups = int(rng.integers(1, 30))
+    group_of = rng.integers(-1, n_groups, b)
+    group_pages = rng.integers(0, 100, n_groups)
+    for ppi, waves in ((0, 0), (1, 1), (6, 2), (64, 4)):
+        d = desc(batch=b, hq=hkv * g, hkv=hkv, ppi=ppi, waves=waves)
+        items, merges, cunits, cmem, w = cascade_tables(d, lens, group_of,
+                                                        group_pages)
+        check_cascade_plan(lens, hkv, g, group_of, group_pages, items, merges,
+                           cunits, cmem, w)
+
+
+def test_cascade_plan_of_the_agentic_shape():
+    """Groups of 8 sharing 64 pages, g = 8, 4 wavefronts: one cascade unit
+    per (group, kv-head) with all 8 members, and no trajectory's own items
+    start before page 64 unless it is shorter than the prefix."""
+    rng = np.random.default_rng(1)
+    b = 64
+    lens = np.where(rng.random(b) < 0.1, rng.integers(32768, 98305, b),
+                    rng.integers(256, 4097, b))
+    group_of = np.arange(b) // 8
+    d = desc(batch=b, hq=64, hkv=8, max_blocks=8192)
+    items, merges, cunits, cmem, w = cascade_tables(d, lens, group_of,
+                                                    np.full(8, 64))
+    assert len(cunits) == 8 * 8 and all(cunits[:, 1] == 8)
+    check_cascade_plan(lens, 8, 8, group_of, np.full(8, 64), items, merges,
+                       cunits, cmem, w)
+    own = items[items[:, 0] >= 0]
+    b_of = own[:, 0] // 8
+    assert np.all(own[:, 1] >= np.minimum(64, -(-lens[b_of] // 16)))
+    # no cascade without sharing, or for lone members
+    items2, _, cu2, _, _ = cascade_tables(d, lens, group_of, np.zeros(8))
+    assert len(cu2) == 0 and np.all(items2[:, 0] >= 0)
+    items3, _, cu3, _, _ = cascade_tables(d, lens, np.arange(b), np.full(b, 64))
+    assert len(cu3) == 0
+
+
+def test_cascade_planner_argument_errors():
+    d = desc(batch=3)
+    lens = np.array([10, 20, 30], np.int32)
+    lib = N.lib()
+    out = ctypes.c_void_p()
+    P = ctypes.POINTER(ctypes.c_int32)
+
+    def st(group_of, n, pages):
+        g = np.asarray(group_of, np.int32)
+        pg = np.asarray(pages, np.int32)
+        return lib.laminar_plan_create_cascade(
+            ctypes.byref(d), lens.ctypes.data_as(P), g.ctypes.data_as(P), n,
+            pg.ctypes.data_as(P), 256, ctypes.byref(out))
+
+    INV = N.LAMINAR_ERR_INVALID_ARG
+    assert st([0, 0, -1], 1, [2]) == N.LAMINAR_OK
+    N.laminar_plan_destroy(out.value)
+    assert st([0, 0, -1], -1, [2]) == INV
+    assert st([0, 2, -1], 2, [2, 2]) == INV          # group out of range
+    assert st([0, -2, -1], 1, [2]) == INV
+    assert st([0, 0, 0], 1, [-1]) == INV
+    assert lib.laminar_plan_create_cascade(ctypes.byref(d), lens.ctypes.data_as(P),
+                                           None, 1, None, 256,
+                                           ctypes.byref(out)) == INV
+
+
 def test_kv_append_errors_before_any_launch():
     lib = N.lib()
     INV, UNS = N.LAMINAR_ERR_INVALID_ARG, N.LAMINAR_ERR_UNSUPPORTED
@@ -267,25 +403,46 @@ def test_planner_under_address_and_ub_sanitizers(tmp_path):
     assert "plan_check OK" in r.stdout
 
 
-def test_attention_kernels_do_not_spill():
-    """The page-pair double buffer fills most of the register file; a spill
-    to scratch in the hot loop costs ~15% of bandwidth, so every attention
-    kernel instantiation must compile without scratch."""
+def test_attention_kernels_do_not_spill_in_the_page_loop():
+    """The page-pair double buffer fills most of the register file. A spill
+    inside the page loop costs ~15% of bandwidth, so no attention kernel
+    instantiation may touch scratch inside a loop; at most one register may
+    be parked across the loop (a store before, a load after), and every
+    instantiation keeps two wavefronts per SIMD."""
     from paper_2510_12633_amd import build as B
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     if not os.path.exists(hipcc):
         pytest.skip("hipcc not available")
     src = os.path.join(B.CSRC, "decode_attn.hip")
-    cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang",
-           "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", B.INCLUDE,
-           "-I", B.CSRC, "-c", src, "-o", os.devnull,
-           "-Rpass-analysis=kernel-resource-usage"]
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    base = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang",
+            "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", B.INCLUDE,
+            "-I", B.CSRC]
+    r = subprocess.run(base + ["-c", src, "-o", os.devnull,
+                               "-Rpass-analysis=kernel-resource-usage"],
+                       capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     names = re.findall(r"Function Name: (\S+)", r.stderr)
     scratch = [int(x) for x in
                re.findall(r"ScratchSize \[bytes/lane\]: (\d+)", r.stderr)]
-    assert len(names) == len(scratch) and names
-    kernels = [(n, sc) for n, sc in zip(names, scratch) if "decode_items" in n]
-    assert len(kernels) == 12          # 2 head dims x 2 dtypes x 3 waves
-    assert all(sc == 0 for _, sc in kernels), kernels
+    occ = [int(x) for x in re.findall(r"Occupancy \[waves/SIMD\]: (\d+)",
+                                      r.stderr)]
+    assert len(names) == len(scratch) == len(occ) and names
+    kernels = [(n, sc, o) for n, sc, o in zip(names, scratch, occ)
+               if "decode_items" in n]
+    assert len(kernels) == 24   # 2 head dims x 2 dtypes x 3 waves x cascade
+    assert all(sc <= 8 and o >= 2 for _, sc, o in kernels), kernels
+    r = subprocess.run(base + ["--cuda-device-only", "-S", src, "-o", "-"],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-2000:]
+    in_loop, fn, bad = False, None, []
+    for line in r.stdout.splitlines():
+        m = re.match(r"^(\w+):", line)
+        if m and "decode_items" in m.group(1):
+            fn, in_loop = m.group(1), False
+        if line.startswith(".LBB") or line.startswith("; %bb."):
+            in_loop = "Loop" in line
+        if fn and in_loop and "scratch_" in line:
+            bad.append((fn, line.strip()))
+        if line.strip() == "s_endpgm":
+            fn = None
+    assert not bad, bad[:4]

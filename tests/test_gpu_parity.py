@@ -11,7 +11,8 @@ import pytest
 import torch
 
 from oracle import decode_attention_from_host
-from workloads import custom_config, get_config, host_arrays, make_workload
+from workloads import (custom_config, get_config, host_arrays, make_workload,
+                       prefix_groups)
 
 pytestmark = pytest.mark.gpu
 
@@ -28,7 +29,7 @@ def _say(msg):
 
 
 def run_gpu(wl, pages_per_item=0, waves_per_item=0, block_table=None,
-            k_pages=None, v_pages=None, two_phase=False):
+            k_pages=None, v_pages=None, two_phase=False, cascade=False):
     from paper_2510_12633_amd.api import PagedDecodeAttention
     c = wl.cfg
     dev = wl.q.device
@@ -42,7 +43,13 @@ def run_gpu(wl, pages_per_item=0, waves_per_item=0, block_table=None,
         max_blocks_per_seq=bt_np.shape[1], seq_lens_host=wl.seq_lens,
         softmax_scale=wl.softmax_scale, kv_dtype=c.kv_dtype,
         k_scale=wl.k_scale, v_scale=wl.v_scale,
-        pages_per_item=pages_per_item, waves_per_item=waves_per_item)
+        pages_per_item=pages_per_item, waves_per_item=waves_per_item,
+        **(dict(zip(("group_of", "group_pages"), prefix_groups(wl)))
+           if cascade else {}))
+    if cascade and (waves_per_item or 4) * (16 // (c.num_q_heads //
+                                                   c.num_kv_heads)) >= 2:
+        # one item holds waves x (16 / g) members; a chunk needs two
+        assert N_cascade_units(att) > 0, "the cascade plan decodes no prefix"
     kp = wl.k_pages if k_pages is None else k_pages
     vp = wl.v_pages if v_pages is None else v_pages
     if two_phase:
@@ -55,6 +62,11 @@ def run_gpu(wl, pages_per_item=0, waves_per_item=0, block_table=None,
     res = out.cpu().numpy(), lse.cpu().numpy()
     att.close()
     return res
+
+
+def N_cascade_units(att):
+    from paper_2510_12633_amd import _native as N
+    return int(N.lib().laminar_plan_num_cascade_units(att.plan))
 
 
 def check(gpu, ref, what, seqs=None):
@@ -86,6 +98,54 @@ CUSTOM = [
                                        kv_dtype="fp8_e4m3fn")),
     ("g8_d64_odd_pages", custom_config([16 * 3, 16 * 5 + 1, 16 * 7 - 1], 8, 1, 64)),
 ]
+
+
+CASCADE = [
+    ("g8_d128_prefix1024", custom_config([10, 400, 1500, 64, 3, 2000, 1100, 90],
+                                         16, 2, 128, prefix_group=4,
+                                         prefix_tokens=1024)),
+    ("g8_d128_16members", custom_config(
+        [0, 5, 511, 512, 513, 1024, 3000, 77, 600, 512, 9000, 1, 256, 700,
+         2048, 40, 1200, 300], 32, 4, 128, prefix_group=16, prefix_tokens=512)),
+    ("g5_d128_fp8", custom_config([100, 257, 3000, 20, 256, 999], 40, 8, 128,
+                                  kv_dtype="fp8_e4m3fn", prefix_group=3,
+                                  prefix_tokens=256)),
+    ("g16_d64", custom_config([64, 300, 31, 800, 2000, 65, 5], 16, 1, 64,
+                              prefix_group=6, prefix_tokens=320)),
+    ("g1_d64_mha", custom_config([50, 700, 130, 129, 128, 1000], 2, 2, 64,
+                                 prefix_group=6, prefix_tokens=128)),
+    ("g7_d128", custom_config([2100, 2048, 100, 5000, 2047, 4000, 2049, 1],
+                              28, 4, 128, prefix_group=8, prefix_tokens=2048)),
+]
+
+
+@pytest.mark.parametrize("name,cfg", CASCADE, ids=[c[0] for c in CASCADE])
+def test_cascade_shapes(name, cfg):
+    """Shared prefixes decoded once per group: members shorter than, equal
+    to and longer than the prefix, empty members, groups larger than one
+    item, prefix pieces split. Against the oracle at the bar, and against
+    the plain plan within 1e-5."""
+    _need_gpu()
+    wl = make_workload(cfg, seed=17, device="cuda")
+    ref = decode_attention_from_host(host_arrays(wl), workers=4)
+    plain = run_gpu(wl)
+    for ppi in (0, 2, 6):
+        for waves in (1, 2, 4):
+            o, l = run_gpu(wl, pages_per_item=ppi, waves_per_item=waves,
+                           cascade=True)
+            check((o, l), ref,
+                  f"{name} cascade waves={waves} pages_per_item={ppi}")
+            fin = np.isfinite(plain[1])
+            assert np.abs(o - plain[0]).max() <= 1e-5
+            assert np.abs(l[fin] - plain[1][fin]).max() <= 1e-5
+
+
+def test_cascade_run_to_run_bitwise():
+    _need_gpu()
+    wl = make_workload(CASCADE[1][1], seed=3, device="cuda")
+    a = run_gpu(wl, cascade=True)
+    b = run_gpu(wl, cascade=True)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
 
 
 def test_tiny_config_all_outputs():
@@ -251,18 +311,20 @@ def _sample(lens, k, seed):
     return sorted(pick)
 
 
-@pytest.mark.parametrize("idx", [2, 3, 4, 5])
-def test_full_size_config_sampled(idx):
+@pytest.mark.parametrize("idx,cascade", [(2, False), (3, False), (4, False),
+                                         (5, False), (5, True)])
+def test_full_size_config_sampled(idx, cascade):
     """Full-size batch in the bench's launch configuration; the oracle checks
     sampled trajectories (shortest, longest, median and random ones)."""
     _need_gpu()
     cfg = get_config(idx)
     _say(f"generating {cfg.name}")
     wl = make_workload(cfg, device="cuda")
-    out, lse = run_gpu(wl)
+    out, lse = run_gpu(wl, cascade=cascade)
     assert np.isfinite(out).all() and np.isfinite(lse).all()
     seqs = _sample(wl.seq_lens, 6 if idx == 5 else 8, idx)
     ref = decode_attention_from_host(host_arrays(wl, seqs), workers=8)
-    check((out, lse), ref, f"{cfg.name} sampled {seqs}", seqs=seqs)
+    check((out, lse), ref, f"{cfg.name}{' cascade' if cascade else ''} "
+          f"sampled {seqs}", seqs=seqs)
     del wl
     torch.cuda.empty_cache()

@@ -261,6 +261,20 @@ def make_workload(cfg, seed: Optional[int] = None, device="cpu",
                     k_logical=k_log, v_logical=v_log)
 
 
+def prefix_groups(wl: Workload):
+    """(group_of [B], group_pages [G]) of a workload with shared prefixes:
+    trajectory b belongs to group b // prefix_group, whose first
+    prefix_tokens / 16 blocks are shared. (None, None) without sharing."""
+    cfg = wl.cfg
+    if not cfg.prefix_group:
+        return None, None
+    b = wl.batch
+    group_of = (np.arange(b) // cfg.prefix_group).astype(np.int32)
+    n_groups = -(-b // cfg.prefix_group)
+    pages = np.full(n_groups, cfg.prefix_tokens // PAGE_SIZE, dtype=np.int32)
+    return group_of, pages
+
+
 def _bits(t: torch.Tensor) -> np.ndarray:
     t = t.detach().cpu()
     if t.dtype == torch.bfloat16:
