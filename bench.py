@@ -146,9 +146,16 @@ def cpu_baseline(wl, budget_s: float):
             sample.append(b)
             tot += int(wl.seq_lens[b])
         arrays = host_arrays(wl, sorted(sample))
-        t0 = time.perf_counter()
-        decode_attention_from_host(arrays, workers=cores)
-        dt = time.perf_counter() - t0
+        # repeat the pass until about budget_s of CPU time (threads x wall)
+        # has been spent, at most 5 passes; report the median pass
+        times = []
+        while True:
+            t0 = time.perf_counter()
+            decode_attention_from_host(arrays, workers=cores)
+            times.append(time.perf_counter() - t0)
+            if len(times) >= 5 or sum(times) * cores >= budget_s:
+                break
+        dt = sorted(times)[len(times) // 2]
     toks = int(wl.seq_lens[sample].sum())
     return {
         "value": toks * per_tok / dt / 1e12,
@@ -157,7 +164,8 @@ def cpu_baseline(wl, budget_s: float):
         "kind": "oracle",
         "sample": f"{len(sample)} of {wl.batch} trajectories ({toks} tokens, "
                   f"{toks * per_tok / 1e9:.3f} GB of KV), fp64 numpy, "
-                  f"{cores} threads over trajectories, BLAS 1 thread each",
+                  f"{cores} threads over trajectories, BLAS 1 thread each; "
+                  f"median of {len(times)} passes",
         "seconds": dt,
         "tokens_per_s": len(sample) / dt,
         "cpu": cpu_model(),
