@@ -57,6 +57,8 @@ def parse_args(argv=None):
                         "the workload has them (auto) or not at all (off)")
     p.add_argument("--no-append", action="store_true",
                    help="skip the KV-append timing")
+    p.add_argument("--no-repack", action="store_true",
+                   help="skip the repack planner and page-migration timing")
     p.add_argument("--fixed-plan", action="store_true",
                    help="plan once outside the timed loop (kernel-only steps)")
     return p.parse_args(argv)
@@ -242,6 +244,71 @@ def measure_append(torch, wl, steps=24):
             "GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
             "bound": "launch/latency (a few hundred bytes per trajectory)",
             "timed_calls": len(times)}
+
+
+def measure_repack(torch, N, wl, n_rollouts=256, reps=50):
+    """Repack legs: the consolidation planner's host time for n_rollouts
+    rollout states, and the page migration kernel moving this workload's
+    whole pool (K, V and any scales) into a second pool in a random page
+    order."""
+    import ctypes
+    import numpy as np
+    rng = np.random.default_rng(5)
+    used = rng.integers(100, 60000, n_rollouts)
+    states = (N.LaminarRolloutState * n_rollouts)()
+    for i in range(n_rollouts):
+        states[i].kv_used = int(used[i])
+        states[i].kv_prev = int(used[i] + rng.integers(-500, 3000))
+        states[i].num_reqs = int(rng.integers(1, 300))
+    src = (ctypes.c_int32 * n_rollouts)()
+    dst = (ctypes.c_int32 * n_rollouts)()
+    k = ctypes.c_int32()
+    lib = N.lib()
+    best = float("inf")
+    for _ in range(reps):
+        t0 = time.perf_counter_ns()
+        st = lib.laminar_repack_plan(states, n_rollouts, 65536, 256, src, dst,
+                                     ctypes.byref(k))
+        best = min(best, time.perf_counter_ns() - t0)
+        assert st == N.LAMINAR_OK
+
+    pools = [t for t in (wl.k_pages, wl.v_pages, wl.k_scale, wl.v_scale)
+             if t is not None]
+    n = pools[0].shape[0]
+    dev = pools[0].device
+    perm = torch.randperm(n, generator=torch.Generator().manual_seed(1))
+    pairs = torch.stack([torch.arange(n), perm], dim=1).to(torch.int32).to(dev)
+    dsts = [torch.empty_like(t) for t in pools]
+    stream = torch.cuda.current_stream()
+    h = stream.cuda_stream
+
+    def run():
+        for s_, d_ in zip(pools, dsts):
+            N.laminar_migrate_pages(s_, n, d_, n, s_[0].numel() * s_.element_size(),
+                                    pairs, n, h)
+
+    run()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    iters = 5
+    e0.record(stream)
+    for _ in range(iters):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    nbytes = 2 * sum(t.numel() * t.element_size() for t in pools)   # read + write
+    for s_, d_ in zip(pools, dsts):
+        assert torch.equal(d_[pairs[:, 1].long()], s_)
+    del dsts
+    torch.cuda.empty_cache()
+    return {"plan_us": round(best / 1e3, 2), "rollouts": n_rollouts,
+            "pairs_planned": k.value,
+            "migrate": {"kernel": "migrate_kernel16", "pages": n,
+                        "bytes_read_plus_written": nbytes,
+                        "ms": round(ms, 4),
+                        "GBps": round(nbytes / (ms / 1e3) / 1e9, 1),
+                        "frac_of_hbm_peak": round(nbytes / (ms / 1e3) / 1e9
+                                                  / HBM_PEAK_GBPS, 4)}}
 
 
 def main(argv=None):
@@ -437,6 +504,8 @@ def main(argv=None):
         app = measure_append(torch, wl)
         if app is not None:
             result["kv_append"] = app
+    if not args.no_repack:
+        result["repack"] = measure_repack(torch, N, wl)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget_s)
     N.laminar_plan_destroy(plan0)

@@ -1,7 +1,7 @@
 """MI355X-native paged grouped-query decode attention (HIP, gfx950).
 
 The C ABI is declared in include/laminar_decode_attn.h and
-include/laminar_kv_append.h; ``_native`` binds it
+include/laminar_kv_append.h and include/laminar_repack.h; ``_native`` binds it
 with ctypes under the same names and ``api.PagedDecodeAttention`` owns a plan
 and its device workspace. Every step of the computation runs in the HIP
 library; there is no CPU fallback.
@@ -20,4 +20,6 @@ from ._native import (LaminarAttnDesc, LaminarError, laminar_decode_attn,
                       laminar_plan_num_items, laminar_plan_num_merges,
                       laminar_plan_pages_per_item, laminar_plan_waves_per_item,
                       laminar_plan_workspace_bytes, laminar_status_string)
-from .api import PagedDecodeAttention, kv_append
+from ._native import (LaminarRolloutState, laminar_migrate_pages,
+                      laminar_migration_pairs, laminar_repack_plan)
+from .api import PagedDecodeAttention, kv_append, migrate

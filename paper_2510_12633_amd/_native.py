@@ -1,5 +1,5 @@
-"""ctypes binding of the C ABI in include/laminar_decode_attn.h and
-include/laminar_kv_append.h.
+"""ctypes binding of the C ABI in include/laminar_decode_attn.h,
+include/laminar_kv_append.h and include/laminar_repack.h.
 
 Argument marshalling only: every step of the computation runs in the HIP
 library. Importing this module does not touch the GPU; loading fails loudly
@@ -41,6 +41,11 @@ class LaminarAttnDesc(ctypes.Structure):
         ("pages_per_item", c_int32),
         ("waves_per_item", c_int32),
     ]
+
+
+class LaminarRolloutState(ctypes.Structure):
+    _fields_ = [("kv_used", ctypes.c_int64), ("kv_prev", ctypes.c_int64),
+                ("num_reqs", c_int32), ("reserved", c_int32)]
 
 
 class LaminarError(RuntimeError):
@@ -87,6 +92,17 @@ _SIGNATURES = {
     "laminar_hbm_copy": (c_int32, [c_void_p, c_void_p, c_size_t, c_void_p]),
     "laminar_kv_append": (c_int32, [POINTER(LaminarAttnDesc)] + [c_void_p] * 8
                           + [c_void_p]),
+    "laminar_repack_plan": (c_int32, [POINTER(LaminarRolloutState), c_int32,
+                                      ctypes.c_int64, c_int32, POINTER(c_int32),
+                                      POINTER(c_int32), POINTER(c_int32)]),
+    "laminar_migration_pairs": (c_int32, [POINTER(c_int32), POINTER(c_int32),
+                                          c_int32, c_int32, POINTER(c_int32),
+                                          c_int32, POINTER(c_int32), c_int32,
+                                          POINTER(c_int32), c_int32,
+                                          POINTER(c_int32), POINTER(c_int32)]),
+    "laminar_migrate_pages": (c_int32, [c_void_p, ctypes.c_int64, c_void_p,
+                                        ctypes.c_int64, c_size_t, c_void_p,
+                                        c_int32, c_void_p]),
 }
 
 
@@ -250,6 +266,53 @@ def laminar_kv_append(desc: LaminarAttnDesc, k_new, v_new, block_table,
         ctypes.byref(desc), _ptr(k_new), _ptr(v_new), _ptr(block_table),
         _ptr(seq_lens), _ptr(k_pages), _ptr(v_pages), _ptr(k_scale),
         _ptr(v_scale), _ptr(stream)), "laminar_kv_append")
+
+
+def _i32p(a):
+    return a.ctypes.data_as(POINTER(c_int32))
+
+
+def laminar_repack_plan(kv_used, kv_prev, num_reqs, kv_max: int,
+                        batch_max: int):
+    """(source, destination) rollout pairs of the consolidation plan."""
+    n = len(kv_used)
+    states = (LaminarRolloutState * max(n, 1))()
+    for i in range(n):
+        states[i].kv_used = int(kv_used[i])
+        states[i].kv_prev = int(kv_prev[i])
+        states[i].num_reqs = int(num_reqs[i])
+    src = np.zeros(max(n, 1), np.int32)
+    dst = np.zeros(max(n, 1), np.int32)
+    k = c_int32(0)
+    _check(lib().laminar_repack_plan(states, n, int(kv_max), int(batch_max),
+                                     _i32p(src), _i32p(dst), ctypes.byref(k)),
+           "laminar_repack_plan")
+    return [(int(a), int(b)) for a, b in zip(src[:k.value], dst[:k.value])]
+
+
+def laminar_migration_pairs(src_table, lens, dst_free, dst_width: int):
+    """(dst_table [n, dst_width], pairs [k, 2], free pages used)."""
+    src_table = np.ascontiguousarray(src_table, dtype=np.int32)
+    lens = np.ascontiguousarray(lens, dtype=np.int32)
+    dst_free = np.ascontiguousarray(dst_free, dtype=np.int32)
+    n, width = src_table.shape
+    dst_table = np.full((n, dst_width), -1, np.int32)
+    cap = int(np.sum((lens.astype(np.int64) + 15) // 16))
+    pairs = np.zeros((max(cap, 1), 2), np.int32)
+    k, used = c_int32(0), c_int32(0)
+    _check(lib().laminar_migration_pairs(
+        _i32p(src_table), _i32p(lens), n, width, _i32p(dst_free),
+        dst_free.size, _i32p(dst_table), dst_width, _i32p(pairs), cap,
+        ctypes.byref(k), ctypes.byref(used)), "laminar_migration_pairs")
+    return dst_table, pairs[:k.value].copy(), used.value
+
+
+def laminar_migrate_pages(src_pool, src_pages: int, dst_pool, dst_pages: int,
+                          page_bytes: int, pairs, num_pairs: int, stream):
+    _check(lib().laminar_migrate_pages(
+        _ptr(src_pool), int(src_pages), _ptr(dst_pool), int(dst_pages),
+        int(page_bytes), _ptr(pairs), int(num_pairs), _ptr(stream)),
+        "laminar_migrate_pages")
 
 
 def laminar_hbm_read_sink_floats() -> int:

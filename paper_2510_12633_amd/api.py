@@ -153,3 +153,16 @@ def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages,
         v_scale=None, pages_per_item=0, waves_per_item=0)
     N.laminar_kv_append(desc, k_new, v_new, block_table, seq_lens, k_pages,
                         v_pages, k_scale, v_scale, _stream_handle(stream))
+
+
+def migrate(src_pools, dst_pools, pairs, stream=None):
+    """Copy the pages listed in ``pairs`` (device int32 [n, 2]: source page,
+    destination page) between matching pools of two rollouts, e.g.
+    (k_pages, v_pages) or (k_pages, v_pages, k_scale, v_scale)."""
+    n = int(pairs.shape[0])
+    for s, d in zip(src_pools, dst_pools):
+        if s is None:
+            continue
+        page_bytes = s[0].numel() * s.element_size()
+        N.laminar_migrate_pages(s, s.shape[0], d, d.shape[0], page_bytes,
+                                pairs, n, _stream_handle(stream))

@@ -19,7 +19,8 @@ LIB_NAME = "liblaminar_decode_attn.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 
 SOURCES = [os.path.join(CSRC, "decode_attn.hip"),
-           os.path.join(CSRC, "kv_append.hip"), os.path.join(CSRC, "plan.cpp")]
+           os.path.join(CSRC, "kv_append.hip"), os.path.join(CSRC, "migrate.hip"),
+           os.path.join(CSRC, "plan.cpp"), os.path.join(CSRC, "repack.cpp")]
 
 # Packed fp32 VALU forms are switched off for all device code.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
