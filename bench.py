@@ -57,6 +57,13 @@ def parse_args(argv=None):
                         "the workload has them (auto) or not at all (off)")
     p.add_argument("--no-append", action="store_true",
                    help="skip the KV-append timing")
+    p.add_argument("--latency-curve", action="store_true",
+                   help="also time full Qwen2.5-7B-shaped decode steps over "
+                        "batch sizes (the latency-versus-batch curve)")
+    p.add_argument("--curve-batches", default="",
+                   help="comma-separated batch sizes for --latency-curve")
+    p.add_argument("--curve-contexts", default="",
+                   help="comma-separated cached-token counts for --latency-curve")
     p.add_argument("--no-repack", action="store_true",
                    help="skip the repack planner and page-migration timing")
     p.add_argument("--fixed-plan", action="store_true",
@@ -313,6 +320,129 @@ def measure_repack(torch, N, wl, n_rollouts=256, reps=50):
                                                   / HBM_PEAK_GBPS, 4)}}
 
 
+def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
+                                     512, 768, 1024),
+                  contexts=(16, 2048), reps=5):
+    """One decode step of a Qwen2.5-7B-shaped decoder (28 layers, random
+    bf16 weights; per layer RMS pre-norms, the QKV, O, gate+up and down
+    projections as library GEMMs, this library's KV append and paged
+    attention, SwiGLU and residuals; then the LM head) captured in a HIP
+    graph and timed at each batch size, next to the roofline model's step
+    time and batch bound. Every replay is checked bit for bit against the
+    eager step. Every trajectory holds `context` cached tokens; one KV pool
+    serves all layers (the bytes read per layer are those of a real step).
+    Rotary embedding and biases are left out."""
+    import numpy as np
+    from paper_2510_12633_amd.api import PagedDecodeAttention, kv_append
+    L, h, hq, hkv, d, inter, vocab = 28, 3584, 28, 4, 128, 18944, 152064
+    shape = N.LaminarModelShape(layers=L, hidden=h, q_heads=hq, kv_heads=hkv,
+                                head_dim=d, intermediate=inter, vocab=vocab,
+                                weight_bytes=2, act_bytes=2, kv_bytes=2)
+    peak_f, peak_bw = 2_500_000_000_000_000, 8_000_000_000_000
+    bound = N.laminar_roofline_batch_bound(shape, peak_f, peak_bw)
+    gen = torch.Generator(device="cuda").manual_seed(3)
+    bf = torch.bfloat16
+
+    def w(k, n):
+        return (torch.randn((k, n), generator=gen, device="cuda", dtype=bf)
+                * (1.0 / k ** 0.5))
+
+    layers = [(w(h, (hq + 2 * hkv) * d), w(hq * d, h), w(h, 2 * inter),
+               w(inter, h)) for _ in range(L)]
+    lm_head = w(h, vocab)
+    stream = torch.cuda.current_stream()
+    curves = []
+    for ctx in contexts:
+        points = []
+        for m in batches:
+            n_tok = ctx + 1                       # cached tokens + the new one
+            pages = -(-n_tok // 16)
+            kp = torch.randn((m * pages, hkv, 16 * d), generator=gen,
+                             device="cuda", dtype=bf)
+            vp = torch.randn_like(kp)
+            table = torch.arange(m * pages, dtype=torch.int32,
+                                 device="cuda").view(m, pages)
+            lens_host = np.full(m, n_tok, np.int32)
+            lens = torch.as_tensor(lens_host, device="cuda")
+            att = PagedDecodeAttention(
+                batch=m, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                num_pages=m * pages, max_blocks_per_seq=pages,
+                seq_lens_host=lens_host, softmax_scale=d ** -0.5)
+            out, lse = att.outputs()
+            x0 = torch.randn((m, h), generator=gen, device="cuda", dtype=bf)
+
+            def step():
+                cur = torch.cuda.current_stream()
+                x = x0
+
+                def rms(t):                       # pre-norm, keeps x finite
+                    tf = t.float()
+                    return (tf * torch.rsqrt(tf.pow(2).mean(-1, keepdim=True)
+                                             + 1e-6)).to(bf)
+
+                for wqkv, wo, wgu, wd in layers:
+                    qkv = rms(x) @ wqkv
+                    q = qkv[:, :hq * d].reshape(m, hq, d).contiguous()
+                    k_new = qkv[:, hq * d:(hq + hkv) * d].reshape(m, hkv, d).contiguous()
+                    v_new = qkv[:, (hq + hkv) * d:].reshape(m, hkv, d).contiguous()
+                    kv_append(k_new, v_new, table, lens, kp, vp, stream=cur)
+                    att(q, kp, vp, table, lens, out, lse, stream=cur)
+                    x = x + out.view(m, hq * d).to(bf) @ wo
+                    gu = rms(x) @ wgu
+                    x = x + (torch.nn.functional.silu(gu[:, :inter])
+                             * gu[:, inter:]) @ wd
+                return rms(x) @ lm_head
+
+            # The step is ~400 launches: capture it in a HIP graph so the
+            # curve shows the GPU's time, not the host's launch rate.
+            side = torch.cuda.Stream()
+            side.wait_stream(stream)
+            with torch.cuda.stream(side):
+                eager = step()
+            stream.wait_stream(side)
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                logits = step()
+            graph.replay()
+            torch.cuda.synchronize()
+            first = logits.clone()
+            graph.replay()
+            torch.cuda.synchronize()
+            # every replay must reproduce the eager step bit for bit
+            bits = lambda t: t.view(torch.int16)
+            assert bool(torch.isfinite(eager).all()), "non-finite logits"
+            assert torch.equal(bits(first), bits(eager)), "graph replay differs"
+            assert torch.equal(bits(logits), bits(eager)), "graph replays differ"
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                graph.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            del graph, logits, eager, first
+            model_ms = 1e3 * N.laminar_roofline_step_seconds(shape, m, ctx,
+                                                             peak_f, peak_bw)
+            points.append({"batch": m, "ms": round(ms, 3),
+                           "roofline_ms": round(model_ms, 3)})
+            print(f"[latency] context {ctx} batch {m}: {ms:.3f} ms "
+                  f"(roofline {model_ms:.3f} ms)", file=sys.stderr, flush=True)
+            att.close()
+            del kp, vp, att
+            torch.cuda.empty_cache()
+        base = points[0]["ms"]
+        knee = next((p["batch"] for p in points if p["ms"] > 1.1 * base), None)
+        curves.append({"context": ctx, "points": points,
+                       "first_batch_10pct_slower_than_batch_1": knee})
+    del layers, lm_head
+    torch.cuda.empty_cache()
+    return {"model": "Qwen2.5-7B shapes, random bf16 weights, 28 layers + LM head",
+            "roofline_batch_bound": bound, "peak_flops": peak_f,
+            "peak_bw": peak_bw, "curves": curves}
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.gpus != 1:
@@ -508,6 +638,13 @@ def main(argv=None):
             result["kv_append"] = app
     if not args.no_repack:
         result["repack"] = measure_repack(torch, N, wl)
+    if args.latency_curve:
+        kw = {}
+        if args.curve_batches:
+            kw["batches"] = tuple(int(x) for x in args.curve_batches.split(","))
+        if args.curve_contexts:
+            kw["contexts"] = tuple(int(x) for x in args.curve_contexts.split(","))
+        result["latency_curve"] = latency_curve(torch, N, **kw)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget_s)
     N.laminar_plan_destroy(plan0)

@@ -91,6 +91,44 @@ laminar_status laminar_migrate_pages(const void* src_pool, int64_t src_pages,
                                      size_t page_bytes, const int32_t* pairs,
                                      int32_t num_pairs, hipStream_t stream);
 
+/* Dense decoder shape for the roofline batch bound (host struct). */
+typedef struct {
+  int32_t layers, hidden, q_heads, kv_heads, head_dim, intermediate, vocab;
+  int32_t weight_bytes;   /* bytes per weight element (2 for bf16)        */
+  int32_t act_bytes;      /* bytes per activation element (2 for bf16)    */
+  int32_t kv_bytes;       /* bytes per KV element (2 bf16, 1 fp8)         */
+} laminar_model_shape;
+
+/*
+ * Roofline batch bound B of Algorithm 1 (§6.2): the smallest decode batch
+ * at which one step's projections (per layer QKV, O, gate+up and down, and
+ * the LM head; a [M, K] x [K, N] product does 2 M N K flops and moves
+ * weight_bytes N K + act_bytes M (K + N) bytes) are compute-bound at peak
+ * compute peak_flops (FLOP/s) and bandwidth peak_bw (B/s):
+ *   B = min { M >= 1 : sum 2 M N K / F >= sum (wb N K + ab M (K + N)) / BW }.
+ * Attention is memory-bound at every batch (its intensity is
+ * q_heads / (kv_heads kv_bytes) flops per byte) and adds a cost per
+ * trajectory, not a transition. Exact integer arithmetic. *bound = 0 when
+ * no batch is compute-bound (activation traffic outweighs the gain).
+ * Errors: INVALID_ARG (NULL pointers, non-positive sizes or peaks).
+ */
+laminar_status laminar_roofline_batch_bound(const laminar_model_shape* shape,
+                                            uint64_t peak_flops,
+                                            uint64_t peak_bw, int32_t* bound);
+
+/*
+ * Roofline time of one decode step of `batch` trajectories holding
+ * `context` cached tokens each: every projection at max(flops / F,
+ * bytes / BW), plus per layer attention at max(4 M c Hq D / F,
+ * kv_bytes 2 Hkv D M (c + 1) / BW). Written to *seconds.
+ * Errors: INVALID_ARG (NULL pointers, non-positive sizes or peaks,
+ * negative batch or context).
+ */
+laminar_status laminar_roofline_step_seconds(const laminar_model_shape* shape,
+                                             int64_t batch, int64_t context,
+                                             uint64_t peak_flops,
+                                             uint64_t peak_bw, double* seconds);
+
 #ifdef __cplusplus
 }
 #endif

@@ -20,6 +20,8 @@ from ._native import (LaminarAttnDesc, LaminarError, laminar_decode_attn,
                       laminar_plan_num_items, laminar_plan_num_merges,
                       laminar_plan_pages_per_item, laminar_plan_waves_per_item,
                       laminar_plan_workspace_bytes, laminar_status_string)
-from ._native import (LaminarRolloutState, laminar_migrate_pages,
-                      laminar_migration_pairs, laminar_repack_plan)
+from ._native import (LaminarModelShape, LaminarRolloutState,
+                      laminar_migrate_pages, laminar_migration_pairs,
+                      laminar_repack_plan, laminar_roofline_batch_bound,
+                      laminar_roofline_step_seconds)
 from .api import PagedDecodeAttention, kv_append, migrate

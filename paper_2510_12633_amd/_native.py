@@ -48,6 +48,12 @@ class LaminarRolloutState(ctypes.Structure):
                 ("num_reqs", c_int32), ("reserved", c_int32)]
 
 
+class LaminarModelShape(ctypes.Structure):
+    _fields_ = [(n, c_int32) for n in (
+        "layers", "hidden", "q_heads", "kv_heads", "head_dim", "intermediate",
+        "vocab", "weight_bytes", "act_bytes", "kv_bytes")]
+
+
 class LaminarError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = int(status)
@@ -100,6 +106,13 @@ _SIGNATURES = {
                                           c_int32, POINTER(c_int32), c_int32,
                                           POINTER(c_int32), c_int32,
                                           POINTER(c_int32), POINTER(c_int32)]),
+    "laminar_roofline_batch_bound": (c_int32, [POINTER(LaminarModelShape),
+                                               ctypes.c_uint64, ctypes.c_uint64,
+                                               POINTER(c_int32)]),
+    "laminar_roofline_step_seconds": (c_int32, [POINTER(LaminarModelShape),
+                                                ctypes.c_int64, ctypes.c_int64,
+                                                ctypes.c_uint64, ctypes.c_uint64,
+                                                POINTER(ctypes.c_double)]),
     "laminar_migrate_pages": (c_int32, [c_void_p, ctypes.c_int64, c_void_p,
                                         ctypes.c_int64, c_size_t, c_void_p,
                                         c_int32, c_void_p]),
@@ -288,6 +301,27 @@ def laminar_repack_plan(kv_used, kv_prev, num_reqs, kv_max: int,
                                      _i32p(src), _i32p(dst), ctypes.byref(k)),
            "laminar_repack_plan")
     return [(int(a), int(b)) for a, b in zip(src[:k.value], dst[:k.value])]
+
+
+def laminar_roofline_batch_bound(shape: LaminarModelShape, peak_flops: int,
+                                 peak_bw: int) -> int:
+    """Roofline batch bound B (0: no batch is compute-bound)."""
+    out = c_int32()
+    _check(lib().laminar_roofline_batch_bound(ctypes.byref(shape),
+                                              int(peak_flops), int(peak_bw),
+                                              ctypes.byref(out)),
+           "laminar_roofline_batch_bound")
+    return out.value
+
+
+def laminar_roofline_step_seconds(shape: LaminarModelShape, batch: int,
+                                  context: int, peak_flops: int,
+                                  peak_bw: int) -> float:
+    out = ctypes.c_double()
+    _check(lib().laminar_roofline_step_seconds(
+        ctypes.byref(shape), int(batch), int(context), int(peak_flops),
+        int(peak_bw), ctypes.byref(out)), "laminar_roofline_step_seconds")
+    return out.value
 
 
 def laminar_migration_pairs(src_table, lens, dst_free, dst_width: int):

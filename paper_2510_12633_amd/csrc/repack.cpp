@@ -1,5 +1,6 @@
-// Trajectory repacking, host side: the best-fit consolidation plan and the
-// page assignment of a migration. Pure host C++: no HIP call.
+// Trajectory repacking, host side: the best-fit consolidation plan, the
+// page assignment of a migration, and the roofline batch bound B that the
+// plan takes as input. Pure host C++: no HIP call.
 //
 // The plan follows the paper's Algorithm 1 (§6.2): candidates are the
 // rollouts whose KV usage is falling and below the limit and that run fewer
@@ -16,6 +17,30 @@
 #include <vector>
 
 #include "laminar_repack.h"
+
+namespace {
+
+bool shape_ok(const laminar_model_shape* m) {
+  return m && m->layers > 0 && m->hidden > 0 && m->q_heads > 0 &&
+         m->kv_heads > 0 && m->head_dim > 0 && m->intermediate > 0 &&
+         m->vocab > 0 && m->weight_bytes > 0 && m->act_bytes >= 0 &&
+         m->kv_bytes > 0;
+}
+
+// (K, N) of every projection of one decode step; calls f(K, N).
+template <class F>
+void for_each_projection(const laminar_model_shape* m, F f) {
+  const int64_t h = m->hidden, d = m->head_dim;
+  for (int32_t l = 0; l < m->layers; ++l) {
+    f(h, (int64_t(m->q_heads) + 2 * m->kv_heads) * d);
+    f(int64_t(m->q_heads) * d, h);
+    f(h, 2 * int64_t(m->intermediate));
+    f(int64_t(m->intermediate), h);
+  }
+  f(h, int64_t(m->vocab));
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -124,6 +149,55 @@ laminar_status laminar_migration_pairs(const int32_t* src_table,
   } catch (...) {
     return LAMINAR_ERR_INVALID_ARG;
   }
+  return LAMINAR_OK;
+}
+
+
+laminar_status laminar_roofline_batch_bound(const laminar_model_shape* m,
+                                            uint64_t peak_flops,
+                                            uint64_t peak_bw, int32_t* bound) {
+  if (!bound || !shape_ok(m) || peak_flops == 0 || peak_bw == 0)
+    return LAMINAR_ERR_INVALID_ARG;
+  // sum N K and sum (K + N) over the projections
+  __int128 nk = 0, kn = 0;
+  for_each_projection(m, [&](int64_t k, int64_t n) {
+    nk += __int128(k) * n;
+    kn += k + n;
+  });
+  // compute-bound at M  <=>  M (2 nk BW - ab kn F) >= wb nk F
+  const __int128 F = peak_flops, BW = peak_bw;
+  const __int128 den = 2 * nk * BW - __int128(m->act_bytes) * kn * F;
+  if (den <= 0) {
+    *bound = 0;
+    return LAMINAR_OK;
+  }
+  const __int128 num = __int128(m->weight_bytes) * nk * F;
+  __int128 b = (num + den - 1) / den;
+  if (b < 1) b = 1;
+  *bound = b > INT32_MAX ? INT32_MAX : int32_t(b);
+  return LAMINAR_OK;
+}
+
+laminar_status laminar_roofline_step_seconds(const laminar_model_shape* m,
+                                             int64_t batch, int64_t context,
+                                             uint64_t peak_flops,
+                                             uint64_t peak_bw, double* seconds) {
+  if (!seconds || !shape_ok(m) || peak_flops == 0 || peak_bw == 0 ||
+      batch < 0 || context < 0)
+    return LAMINAR_ERR_INVALID_ARG;
+  const long double F = peak_flops, BW = peak_bw, M = batch;
+  long double t = 0;
+  for_each_projection(m, [&](int64_t k, int64_t n) {
+    const long double flops = 2 * M * k * n;
+    const long double bytes = (long double)(m->weight_bytes) * k * n +
+                              (long double)(m->act_bytes) * M * (k + n);
+    t += std::max(flops / F, bytes / BW);
+  });
+  const long double att_f = 4 * M * context * m->q_heads * m->head_dim;
+  const long double att_b = (long double)(m->kv_bytes) * 2 * m->kv_heads *
+                            m->head_dim * M * (context + 1);
+  t += m->layers * std::max(att_f / F, att_b / BW);
+  *seconds = double(t);
   return LAMINAR_OK;
 }
 

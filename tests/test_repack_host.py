@@ -97,3 +97,49 @@ def test_migrate_pages_errors_before_any_launch():
     assert lib.laminar_migrate_pages(16, 4, 40, 4, 16, 64, 1, None) == INV  # align
     assert lib.laminar_migrate_pages(16, 4, 32, 4, 16, 68, 1, None) == INV  # pairs
     assert lib.laminar_migrate_pages(16, -1, 32, 4, 16, 64, 1, None) == INV
+
+
+def _shape(m):
+    return N.LaminarModelShape(
+        layers=m.layers, hidden=m.hidden, q_heads=m.q_heads,
+        kv_heads=m.kv_heads, head_dim=m.head_dim, intermediate=m.intermediate,
+        vocab=m.vocab, weight_bytes=m.weight_bytes, act_bytes=m.act_bytes,
+        kv_bytes=m.kv_bytes)
+
+
+def test_roofline_bound_matches_oracle():
+    from oracle.roofline import QWEN25_7B, QWEN25_32B, ModelShape, batch_bound
+    peaks = [(2_500_000_000_000_000, 8_000_000_000_000),
+             (5_000_000_000_000_000, 8_000_000_000_000),
+             (989_000_000_000_000, 3_350_000_000_000), (10 ** 12, 10 ** 12)]
+    shapes = [QWEN25_7B, QWEN25_32B, ModelShape(2, 64, 4, 2, 16, 128, 100),
+              ModelShape(1, 2, 1, 1, 2, 2, 2, 2, 64, 2),
+              ModelShape(28, 3584, 28, 4, 128, 18944, 152064, 1, 2, 1)]
+    for m in shapes:
+        for f, bw in peaks:
+            want = batch_bound(m, f, bw)
+            got = N.laminar_roofline_batch_bound(_shape(m), f, bw)
+            assert got == (0 if want is None else want), (m, f, bw)
+
+
+def test_roofline_step_time_matches_oracle():
+    from oracle.roofline import QWEN25_7B, QWEN25_32B, step_time
+    f, bw = 2_500_000_000_000_000, 8_000_000_000_000
+    for m in (QWEN25_7B, QWEN25_32B):
+        for batch in (1, 7, 64, 350, 1024):
+            for c in (0, 1, 2048, 98304):
+                want = float(step_time(m, batch, c, f, bw))
+                got = N.laminar_roofline_step_seconds(_shape(m), batch, c, f, bw)
+                assert abs(got - want) <= 1e-12 * want
+
+
+def test_roofline_argument_errors():
+    from oracle.roofline import QWEN25_7B
+    s = _shape(QWEN25_7B)
+    with pytest.raises(N.LaminarError):
+        N.laminar_roofline_batch_bound(s, 0, 10)
+    s.layers = 0
+    with pytest.raises(N.LaminarError):
+        N.laminar_roofline_batch_bound(s, 10, 10)
+    with pytest.raises(N.LaminarError):
+        N.laminar_roofline_step_seconds(_shape(QWEN25_7B), -1, 0, 10, 10)
