@@ -60,6 +60,8 @@ def parse_args(argv=None):
     p.add_argument("--latency-curve", action="store_true",
                    help="also time full Qwen2.5-7B-shaped decode steps over "
                         "batch sizes (the latency-versus-batch curve)")
+    p.add_argument("--no-projections", action="store_true",
+                   help="skip the skinny projection kernel timing")
     p.add_argument("--curve-batches", default="",
                    help="comma-separated batch sizes for --latency-curve")
     p.add_argument("--curve-contexts", default="",
@@ -320,14 +322,58 @@ def measure_repack(torch, N, wl, n_rollouts=256, reps=50):
                                                   / HBM_PEAK_GBPS, 4)}}
 
 
+QWEN7B_PROJECTIONS = {"qkv": (4608, 3584), "o": (3584, 3584),
+                      "gate_up": (37888, 3584), "down": (3584, 18944),
+                      "lm_head": (152064, 3584)}
+
+
+def measure_projections(torch, N, batches=(1, 16, 64), reps=20):
+    """The skinny projection kernel on Qwen2.5-7B's projection shapes (w
+    [N, K] bf16), HIP-event time per call and weight bytes / time, next to
+    the library GEMM (torch.matmul) on the same operands."""
+    from paper_2510_12633_amd.api import SkinnyLinear
+    gen = torch.Generator(device="cuda").manual_seed(9)
+    stream = torch.cuda.current_stream()
+    rows = []
+    for name, (n, k) in QWEN7B_PROJECTIONS.items():
+        w = torch.randn((n, k), generator=gen, device="cuda").to(torch.bfloat16)
+        wt = w.t().contiguous()                    # [K, N] for x @ wt
+        lin = SkinnyLinear(w)
+        for m in batches:
+            x = torch.randn((m, k), generator=gen, device="cuda").to(torch.bfloat16)
+            out = torch.empty((m, n), device="cuda")
+            for fn_name, fn in (("laminar_linear", lambda: lin(x, out=out)),
+                                ("library_gemm", lambda: x @ wt)):
+                fn()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(reps):
+                    fn()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                us = 1e3 * e0.elapsed_time(e1) / reps
+                wbytes = 2 * n * k
+                rows.append({"proj": name, "n": n, "k": k, "m": m,
+                             "impl": fn_name, "us": round(us, 2),
+                             "weight_GBps": round(wbytes / (us * 1e-6) / 1e9, 1),
+                             "frac_hbm_peak": round(wbytes / (us * 1e-6) / 1e9
+                                                    / HBM_PEAK_GBPS, 4)})
+        del w, wt, lin
+    torch.cuda.empty_cache()
+    return rows
+
+
 def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                                      512, 768, 1024),
                   contexts=(16, 2048), reps=5):
     """One decode step of a Qwen2.5-7B-shaped decoder (28 layers, random
     bf16 weights; per layer RMS pre-norms, the QKV, O, gate+up and down
-    projections as library GEMMs, this library's KV append and paged
-    attention, SwiGLU and residuals; then the LM head) captured in a HIP
-    graph and timed at each batch size, next to the roofline model's step
+    projections, this library's KV append and paged attention, SwiGLU and
+    residuals; then the LM head) captured in a HIP graph and timed at each
+    batch size. Each projection kind runs the faster of this library's
+    skinny kernel (batches up to 64) and the library GEMM, timed first at
+    that batch; next to the roofline model's step
     time and batch bound. Every replay is checked bit for bit against the
     eager step. Every trajectory holds `context` cached tokens; one KV pool
     serves all layers (the bytes read per layer are those of a real step).
@@ -343,18 +389,63 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     gen = torch.Generator(device="cuda").manual_seed(3)
     bf = torch.bfloat16
 
-    def w(k, n):
-        return (torch.randn((k, n), generator=gen, device="cuda", dtype=bf)
-                * (1.0 / k ** 0.5))
+    from paper_2510_12633_amd.api import SkinnyLinear
 
-    layers = [(w(h, (hq + 2 * hkv) * d), w(hq * d, h), w(h, 2 * inter),
-               w(inter, h)) for _ in range(L)]
-    lm_head = w(h, vocab)
+    class Proj:
+        """One projection's weight in both layouts: [N, K] for this
+        library's skinny kernel, [K, N] for the library GEMM (x @ w)."""
+
+        def __init__(self, k, n):
+            self.nk = (torch.randn((n, k), generator=gen, device="cuda",
+                                   dtype=bf) * (1.0 / k ** 0.5))
+            self.kn = self.nk.t().contiguous()
+            self.skinny = SkinnyLinear(self.nk)
+            self.use_skinny = False
+
+        def __call__(self, x):
+            if self.use_skinny:
+                return self.skinny(x).to(bf)
+            return x @ self.kn
+
+    layers = [(Proj(h, (hq + 2 * hkv) * d), Proj(hq * d, h),
+               Proj(h, 2 * inter), Proj(inter, h)) for _ in range(L)]
+    lm_head = Proj(h, vocab)
+
+    def choose(m):
+        """Per projection kind, the faster of the skinny kernel and the
+        library GEMM at this batch (timed on layer 0's weights)."""
+        picks = {}
+        for i, kind in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
+            p0 = lm_head if kind == "lm_head" else layers[0][i]
+            x = torch.randn((m, p0.nk.shape[1]), generator=gen, device="cuda",
+                            dtype=bf)
+            times = {}
+            for use in (False, True):
+                if use and m > 64:
+                    continue
+                p0.use_skinny = use
+                p0(x)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(5):
+                    p0(x)
+                e1.record()
+                torch.cuda.synchronize()
+                times[use] = e0.elapsed_time(e1)
+            best = min(times, key=times.get)
+            for lay in ([lm_head] if kind == "lm_head" else
+                        [layer[i] for layer in layers]):
+                lay.use_skinny = best
+            picks[kind] = "laminar_linear" if best else "library_gemm"
+        return picks
+
     stream = torch.cuda.current_stream()
     curves = []
     for ctx in contexts:
         points = []
         for m in batches:
+            picks = choose(m)
             n_tok = ctx + 1                       # cached tokens + the new one
             pages = -(-n_tok // 16)
             kp = torch.randn((m * pages, hkv, 16 * d), generator=gen,
@@ -381,17 +472,17 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                                              + 1e-6)).to(bf)
 
                 for wqkv, wo, wgu, wd in layers:
-                    qkv = rms(x) @ wqkv
+                    qkv = wqkv(rms(x))
                     q = qkv[:, :hq * d].reshape(m, hq, d).contiguous()
                     k_new = qkv[:, hq * d:(hq + hkv) * d].reshape(m, hkv, d).contiguous()
                     v_new = qkv[:, (hq + hkv) * d:].reshape(m, hkv, d).contiguous()
                     kv_append(k_new, v_new, table, lens, kp, vp, stream=cur)
                     att(q, kp, vp, table, lens, out, lse, stream=cur)
-                    x = x + out.view(m, hq * d).to(bf) @ wo
-                    gu = rms(x) @ wgu
-                    x = x + (torch.nn.functional.silu(gu[:, :inter])
-                             * gu[:, inter:]) @ wd
-                return rms(x) @ lm_head
+                    x = x + wo(out.view(m, hq * d).to(bf))
+                    gu = wgu(rms(x))
+                    x = x + wd(torch.nn.functional.silu(gu[:, :inter])
+                               * gu[:, inter:])
+                return lm_head(rms(x))
 
             # The step is ~400 launches: capture it in a HIP graph so the
             # curve shows the GPU's time, not the host's launch rate.
@@ -426,7 +517,8 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             model_ms = 1e3 * N.laminar_roofline_step_seconds(shape, m, ctx,
                                                              peak_f, peak_bw)
             points.append({"batch": m, "ms": round(ms, 3),
-                           "roofline_ms": round(model_ms, 3)})
+                           "roofline_ms": round(model_ms, 3),
+                           "projections": picks})
             print(f"[latency] context {ctx} batch {m}: {ms:.3f} ms "
                   f"(roofline {model_ms:.3f} ms)", file=sys.stderr, flush=True)
             att.close()
@@ -436,7 +528,7 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
         knee = next((p["batch"] for p in points if p["ms"] > 1.1 * base), None)
         curves.append({"context": ctx, "points": points,
                        "first_batch_10pct_slower_than_batch_1": knee})
-    del layers, lm_head
+    del layers, lm_head, Proj
     torch.cuda.empty_cache()
     return {"model": "Qwen2.5-7B shapes, random bf16 weights, 28 layers + LM head",
             "roofline_batch_bound": bound, "peak_flops": peak_f,
@@ -638,6 +730,8 @@ def main(argv=None):
             result["kv_append"] = app
     if not args.no_repack:
         result["repack"] = measure_repack(torch, N, wl)
+    if not args.no_projections:
+        result["projections"] = measure_projections(torch, N)
     if args.latency_curve:
         kw = {}
         if args.curve_batches:

@@ -1,7 +1,8 @@
 """MI355X-native paged grouped-query decode attention (HIP, gfx950).
 
 The C ABI is declared in include/laminar_decode_attn.h and
-include/laminar_kv_append.h and include/laminar_repack.h; ``_native`` binds it
+include/laminar_kv_append.h, include/laminar_repack.h and
+include/laminar_linear.h; ``_native`` binds it
 with ctypes under the same names and ``api.PagedDecodeAttention`` owns a plan
 and its device workspace. Every step of the computation runs in the HIP
 library; there is no CPU fallback.
@@ -24,4 +25,6 @@ from ._native import (LaminarModelShape, LaminarRolloutState,
                       laminar_migrate_pages, laminar_migration_pairs,
                       laminar_repack_plan, laminar_roofline_batch_bound,
                       laminar_roofline_step_seconds)
-from .api import PagedDecodeAttention, kv_append, migrate
+from ._native import (laminar_linear, laminar_linear_splits,
+                      laminar_linear_workspace_bytes)
+from .api import PagedDecodeAttention, SkinnyLinear, kv_append, migrate

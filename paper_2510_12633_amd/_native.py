@@ -1,5 +1,6 @@
 """ctypes binding of the C ABI in include/laminar_decode_attn.h,
-include/laminar_kv_append.h and include/laminar_repack.h.
+include/laminar_kv_append.h, include/laminar_repack.h and
+include/laminar_linear.h.
 
 Argument marshalling only: every step of the computation runs in the HIP
 library. Importing this module does not touch the GPU; loading fails loudly
@@ -113,6 +114,10 @@ _SIGNATURES = {
                                                 ctypes.c_int64, ctypes.c_int64,
                                                 ctypes.c_uint64, ctypes.c_uint64,
                                                 POINTER(ctypes.c_double)]),
+    "laminar_linear_splits": (c_int32, [c_int32, c_int32, c_int32]),
+    "laminar_linear_workspace_bytes": (c_size_t, [c_int32, c_int32, c_int32]),
+    "laminar_linear": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32, c_int32,
+                                 c_int32, c_void_p, c_size_t, c_void_p]),
     "laminar_migrate_pages": (c_int32, [c_void_p, ctypes.c_int64, c_void_p,
                                         ctypes.c_int64, c_size_t, c_void_p,
                                         c_int32, c_void_p]),
@@ -347,6 +352,21 @@ def laminar_migrate_pages(src_pool, src_pages: int, dst_pool, dst_pages: int,
         _ptr(src_pool), int(src_pages), _ptr(dst_pool), int(dst_pages),
         int(page_bytes), _ptr(pairs), int(num_pairs), _ptr(stream)),
         "laminar_migrate_pages")
+
+
+def laminar_linear_splits(m: int, n: int, k: int) -> int:
+    return int(lib().laminar_linear_splits(int(m), int(n), int(k)))
+
+
+def laminar_linear_workspace_bytes(m: int, n: int, k: int) -> int:
+    return int(lib().laminar_linear_workspace_bytes(int(m), int(n), int(k)))
+
+
+def laminar_linear(x, w, y, m: int, n: int, k: int, workspace,
+                   workspace_bytes: int, stream):
+    _check(lib().laminar_linear(_ptr(x), _ptr(w), _ptr(y), int(m), int(n),
+                                int(k), _ptr(workspace), int(workspace_bytes),
+                                _ptr(stream)), "laminar_linear")
 
 
 def laminar_hbm_read_sink_floats() -> int:

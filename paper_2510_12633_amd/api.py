@@ -166,3 +166,24 @@ def migrate(src_pools, dst_pools, pairs, stream=None):
         page_bytes = s[0].numel() * s.element_size()
         N.laminar_migrate_pages(s, s.shape[0], d, d.shape[0], page_bytes,
                                 pairs, n, _stream_handle(stream))
+
+
+class SkinnyLinear:
+    """y = x w^T for decode batches (M <= 64): w [N, K] bf16 on the device;
+    owns the K-split workspace for up to max_m rows."""
+
+    def __init__(self, weight, max_m: int = 64):
+        self.w = weight
+        self.n, self.k = weight.shape
+        self.ws_bytes = max(N.laminar_linear_workspace_bytes(m, self.n, self.k)
+                            for m in range(1, max_m + 1))
+        self.ws = (torch.empty(self.ws_bytes, dtype=torch.uint8,
+                               device=weight.device) if self.ws_bytes else None)
+
+    def __call__(self, x, out=None, stream=None):
+        m = x.shape[0]
+        if out is None:
+            out = torch.empty((m, self.n), dtype=torch.float32, device=x.device)
+        N.laminar_linear(x, self.w, out, m, self.n, self.k, self.ws,
+                         self.ws_bytes, _stream_handle(stream))
+        return out

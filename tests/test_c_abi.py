@@ -382,6 +382,27 @@ def test_kv_append_errors_before_any_launch():
     assert call(fp8, vs=None) == INV
 
 
+def test_linear_errors_before_any_launch():
+    lib = N.lib()
+    INV, UNS = N.LAMINAR_ERR_INVALID_ARG, N.LAMINAR_ERR_UNSUPPORTED
+    assert lib.laminar_linear(None, 16, 16, 1, 16, 128, None, 0, None) == INV
+    assert lib.laminar_linear(16, 24, 16, 1, 16, 128, None, 0, None) == INV
+    assert lib.laminar_linear(16, 16, 16, 0, 16, 128, None, 0, None) == UNS
+    assert lib.laminar_linear(16, 16, 16, 65, 16, 128, None, 0, None) == UNS
+    assert lib.laminar_linear(16, 16, 16, 1, 24, 128, None, 0, None) == UNS
+    assert lib.laminar_linear(16, 16, 16, 1, 16, 100, None, 0, None) == UNS
+    # a K split needs a workspace
+    assert N.laminar_linear_splits(64, 3584, 18944) > 1
+    need = N.laminar_linear_workspace_bytes(64, 3584, 18944)
+    assert need >= 64 * 3584 * 4 * 2
+    assert lib.laminar_linear(16, 16, 16, 64, 3584, 18944, None, 0, None) == INV
+    assert lib.laminar_linear(16, 16, 16, 64, 3584, 18944, 256, need - 1,
+                              None) == INV
+    assert N.laminar_linear_splits(1, 152064, 3584) == 1
+    assert N.laminar_linear_workspace_bytes(1, 152064, 3584) == 0
+    assert N.laminar_linear_splits(0, 16, 128) == 0
+
+
 def test_planner_under_address_and_ub_sanitizers(tmp_path):
     gxx = shutil.which("g++")
     if not gxx:

@@ -1,0 +1,73 @@
+"""GPU parity of the skinny projection kernel against the fp64 oracle.
+
+Bar: |y - y_ref| <= 4 (K/32 + 32) 2^-24 sum_k |x w| per output (fp32
+accumulation of exact bf16 products, one rounding per matrix-core step of
+32 and per accumulation), plus determinism and untouched padding rows."""
+import numpy as np
+import pytest
+import torch
+
+from oracle.linear import linear, linear_abs
+
+pytestmark = pytest.mark.gpu
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+
+
+def bits(t):
+    return t.detach().cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+SHAPES = [(1, 16, 128), (7, 48, 256), (16, 4608, 3584), (17, 3584, 3584),
+          (33, 256, 1024), (64, 3584, 18944), (2, 37888, 3584),
+          (1, 152064, 3584), (48, 96, 640)]
+
+
+@pytest.mark.parametrize("m,n,k", SHAPES)
+def test_linear_matches_oracle(m, n, k):
+    from paper_2510_12633_amd.api import SkinnyLinear
+    _need_gpu()
+    print(f"[gpu-linear] m={m} n={n} k={k}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(m * 1000 + n + k)
+    x = torch.randn((m, k), generator=g, device="cuda").to(torch.bfloat16)
+    w = (torch.randn((n, k), generator=g, device="cuda") / k ** 0.5).to(torch.bfloat16)
+    lin = SkinnyLinear(w)
+    y = torch.full((m + 3, n), float("nan"), device="cuda")
+    lin(x, out=y[:m])
+    y2 = lin(x)
+    torch.cuda.synchronize()
+    got = y[:m].cpu().numpy().astype(np.float64)
+    # sample rows of w for the oracle on the big shapes
+    cols = np.arange(n) if n <= 8192 else np.random.default_rng(0).choice(n, 4096, replace=False)
+    xb, wb = bits(x), bits(w)[cols]
+    ref = linear(xb, wb)
+    bound = 4 * (k / 32 + 32) * 2.0 ** -24 * linear_abs(xb, wb)
+    err = np.abs(got[:, cols] - ref)
+    print(f"[gpu-linear] max err {err.max():.2e}, max err/bound {(err / bound).max():.3f}",
+          flush=True)
+    assert np.all(err <= bound)
+    assert torch.equal(y[:m], y2)                          # deterministic
+    assert torch.isnan(y[m:]).all()                        # padding untouched
+
+
+def test_linear_errors():
+    from paper_2510_12633_amd import _native as N
+    _need_gpu()
+    x = torch.zeros((4, 256), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((32, 256), dtype=torch.bfloat16, device="cuda")
+    y = torch.zeros((4, 32), device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_linear(x, w, y, 65, 32, 256, None, 0, s)
+    assert e.value.status == N.LAMINAR_ERR_UNSUPPORTED
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_linear(x, w, y, 4, 32, 200, None, 0, s)
+    assert e.value.status == N.LAMINAR_ERR_UNSUPPORTED
+    need = N.laminar_linear_workspace_bytes(4, 32, 256)
+    N.laminar_linear(x, w, y, 4, 32, 256,
+                     torch.empty(max(need, 1), dtype=torch.uint8, device="cuda"),
+                     need, s)
+    torch.cuda.synchronize()
