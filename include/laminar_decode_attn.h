@@ -166,8 +166,11 @@ laminar_status laminar_plan_bind_workspace(laminar_plan* plan, void* workspace,
  * page pools, block_table, seq_lens, out and lse are device pointers in the
  * layouts above; seq_lens must hold the lengths the plan was created from
  * (longer device lengths are clipped to the plan's page ranges). Block-table
- * entries outside [0, num_pages) contribute nothing. Errors: INVALID_ARG
- * (NULL plan or pointer), WORKSPACE (no workspace bound), HIP.
+ * entries outside [0, num_pages) contribute nothing. Calls with one plan
+ * share its workspace (partial results and the counter that hands out the
+ * dynamic tail items) and must therefore be ordered on one stream.
+ * Errors: INVALID_ARG (NULL plan or pointer), WORKSPACE (no workspace
+ * bound), HIP.
  */
 laminar_status laminar_decode_attn(const laminar_plan* plan, const void* q,
                                    const void* k_pages, const void* v_pages,
@@ -214,6 +217,10 @@ int32_t laminar_plan_items_copy(const laminar_plan* plan, int32_t* dst,
                                 int32_t capacity);
 int32_t laminar_plan_merges_copy(const laminar_plan* plan, int32_t* dst,
                                  int32_t capacity);
+/* Items at the end of the list that are handed out dynamically (the
+ * smallest ones; workgroups past the bound items take the next of them when
+ * they start, so XCDs that run ahead take more). */
+int32_t laminar_plan_num_dynamic_items(const laminar_plan* plan);
 int32_t laminar_plan_num_cascade_units(const laminar_plan* plan);
 int32_t laminar_plan_num_cascade_members(const laminar_plan* plan);
 int32_t laminar_plan_cascade_units_copy(const laminar_plan* plan, int32_t* dst,

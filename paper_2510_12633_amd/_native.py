@@ -86,6 +86,7 @@ _SIGNATURES = {
     "laminar_plan_waves_per_item": (c_int32, [c_void_p]),
     "laminar_plan_items_copy": (c_int32, [c_void_p, POINTER(c_int32), c_int32]),
     "laminar_plan_merges_copy": (c_int32, [c_void_p, POINTER(c_int32), c_int32]),
+    "laminar_plan_num_dynamic_items": (c_int32, [c_void_p]),
     "laminar_plan_num_cascade_units": (c_int32, [c_void_p]),
     "laminar_plan_num_cascade_members": (c_int32, [c_void_p]),
     "laminar_plan_cascade_units_copy": (c_int32, [c_void_p, POINTER(c_int32),

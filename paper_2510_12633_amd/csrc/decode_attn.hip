@@ -67,6 +67,8 @@ struct DecodeArgs {
   float* lse_part;
   const int4* items;
   const int4* merges;
+  int* tail_counter;      // dynamic tail: next tail item to hand out
+  int32_t num_main, num_tail;
   const int4* cunits;     // cascade unit headers
   const int2* cmembers;   // cascade member records
   int32_t hq, hkv, group, max_blocks, num_pages;
@@ -473,7 +475,8 @@ __device__ __forceinline__ void write_item(const DecodeArgs& a,
 
 // One workgroup per work item (trajectory, kv-head, page range), in the
 // plan's longest-first order; the hardware dispatcher hands items to CUs as
-// workgroups finish. The WAVES wavefronts share the item's page pairs (wave
+// workgroups finish, and the plan's smallest items (the dynamic tail) go to
+// whichever workgroup starts next. The WAVES wavefronts share the item's page pairs (wave
 // w takes pairs w, w+WAVES, ...), each keeping the next pair's loads in
 // flight while it computes the current one; the waves are combined through
 // LDS at the end and wave 0 writes the result.
@@ -484,7 +487,25 @@ decode_items(const DecodeArgs a) {
   using G = Geo<D, FP8>;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int k = blockIdx.x;
+  int k = blockIdx.x;
+  if (!CASCADE && k >= a.num_main) {
+    // Dynamic tail: this workgroup takes the next tail item (longest
+    // first) when the hardware starts it, on whichever XCD has room. Every
+    // tail workgroup pulls once; the pull that gets the last index resets
+    // the counter for the next launch.
+    __shared__ int s_idx;
+    if (threadIdx.x == 0) {
+      const int t = __hip_atomic_fetch_add(a.tail_counter, 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+      if (t == a.num_tail - 1)
+        __hip_atomic_store(a.tail_counter, 0, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      s_idx = t;
+    }
+    __syncthreads();
+    if (s_idx >= a.num_tail) return;     // not expected; keeps k in range
+    k = a.num_main + s_idx;
+  }
   {
     using G = Geo<D, FP8>;
     const int r16 = lane & 15, gq = lane >> 4;
@@ -821,6 +842,9 @@ DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
   a.lse = lse;
   a.items = reinterpret_cast<const int4*>(ws + p->off_items);
   a.merges = reinterpret_cast<const int4*>(ws + p->off_merges);
+  a.tail_counter = reinterpret_cast<int*>(ws + p->off_tail);
+  a.num_main = p->num_main;
+  a.num_tail = p->num_items - p->num_main;
   a.cunits = reinterpret_cast<const int4*>(ws + p->off_cunits);
   a.cmembers = reinterpret_cast<const int2*>(ws + p->off_cmembers);
   a.lse_part = reinterpret_cast<float*>(ws + p->off_lse);

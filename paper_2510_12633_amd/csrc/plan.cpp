@@ -211,6 +211,8 @@ laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
   off = align256(off + size_t(p->num_cascade_units) * 16);
   p->off_cmembers = off;
   off = align256(off + size_t(members) * 8);
+  p->off_tail = off;
+  off = align256(off + sizeof(int32_t));
   p->off_lse = off;
   off = align256(off + size_t(slots) * p->group * sizeof(float));
   p->off_o = off;
@@ -288,6 +290,29 @@ laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
       }
     }
   }
+  // Dynamic tail. Workgroups are dealt to the eight XCDs round-robin by
+  // index and the XCDs stream at rates up to ~10% apart, so a fixed
+  // assignment ends when the slowest XCD ends. The smallest items (at most
+  // half the size of the largest, together at most half the work) are
+  // therefore not bound to an index: each workgroup past num_main takes
+  // the next of them from a counter when the hardware starts it, so XCDs
+  // that run ahead take more of the tail. Plans with cascade items, or
+  // whose items are all about equal (nothing to rebalance, only the
+  // counter's latency to pay), keep every item bound to its index.
+  p->num_main = int32_t(total);
+  if (chunks.empty() && total > 0) {
+    int64_t all = 0;
+    for (int64_t i = 0; i < total; ++i) all += items[i].p1 - items[i].p0;
+    const int32_t small = (items[0].p1 - items[0].p0) / 2;
+    int64_t acc = 0, i = total;
+    while (i > 0) {
+      const int32_t sz = items[i - 1].p1 - items[i - 1].p0;
+      if (sz > small || 2 * (acc + sz) > all) break;
+      acc += sz;
+      --i;
+    }
+    p->num_main = int32_t(i);
+  }
   } catch (...) {     // host allocation failure or too many items: report
     delete p;
     return LAMINAR_ERR_INVALID_ARG;
@@ -350,6 +375,10 @@ int32_t laminar_plan_merges_copy(const laminar_plan* plan, int32_t* dst,
   const int32_t n = std::min(capacity, plan->num_merges);
   std::memcpy(dst, plan->tables.data() + plan->off_merges / 4, size_t(n) * 16);
   return n;
+}
+
+int32_t laminar_plan_num_dynamic_items(const laminar_plan* plan) {
+  return plan ? plan->num_items - plan->num_main : -1;
 }
 
 int32_t laminar_plan_num_cascade_units(const laminar_plan* plan) {

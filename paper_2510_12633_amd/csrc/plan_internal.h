@@ -16,16 +16,21 @@ struct laminar_plan {
   int32_t num_items = 0;
   int32_t num_merges = 0;
   int32_t num_slots = 0;       // partial (out, lse) records
+  // Items [num_main, num_items) are the dynamic tail: workgroups with those
+  // indices take the next of them from a counter at off_tail instead.
+  int32_t num_main = 0;
   int32_t num_cascade_units = 0;  // (shared-prefix chunk, kv-head) units
   int32_t num_cascade_members = 0;  // member records over all those units
   // Host image of workspace bytes [0, off_lse): the work items (4 int32
   // each, in launch order) at off_items, the merge records at off_merges,
   // the cascade unit headers (4 int32: longest member, member count, first
   // member record, kv-head) at off_cunits and the cascade member records
-  // (2 int32: trajectory, first partial slot) at off_cmembers.
+  // (2 int32: trajectory, first partial slot) at off_cmembers, and the
+  // dynamic-tail counter (0) at off_tail.
   std::vector<int32_t> tables;
   // Workspace layout (byte offsets, 256-byte aligned sections).
   size_t off_items = 0, off_merges = 0, off_cunits = 0, off_cmembers = 0;
+  size_t off_tail = 0;         // int32 tail counter, 0 between launches
   size_t off_lse = 0, off_o = 0;
   size_t ws_bytes = 0;
   // Bound workspace (device memory owned by the caller).

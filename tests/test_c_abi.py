@@ -132,6 +132,43 @@ def test_planner_auto_split_fills_the_gpu():
     check_plan(lens, 4, items, merges, chosen)
 
 
+def test_dynamic_tail_is_the_small_end_of_the_list():
+    """Items at most half the largest, together at most half the work, are
+    handed out dynamically; equal-sized items and cascade plans keep every
+    item bound to its workgroup index."""
+    rng = np.random.default_rng(3)
+    lens = np.minimum(np.exp(rng.normal(np.log(2048), 1.0, 256)).astype(np.int64),
+                      32768)
+    d = desc(batch=256)
+    p = N.laminar_plan_create(d, lens.astype(np.int32), 256)
+    try:
+        items = N.laminar_plan_items_copy(p)
+        dyn = int(N.lib().laminar_plan_num_dynamic_items(p))
+    finally:
+        N.laminar_plan_destroy(p)
+    sizes = items[:, 2] - items[:, 1]
+    assert 0 < dyn < len(items)
+    tail = sizes[len(items) - dyn:]
+    assert tail.max() <= sizes[0] // 2 and 2 * tail.sum() <= sizes.sum()
+    # the next larger item would break one of the two limits
+    nxt = sizes[len(items) - dyn - 1]
+    assert nxt > sizes[0] // 2 or 2 * (tail.sum() + nxt) > sizes.sum()
+    # equal pieces: nothing to rebalance
+    p = N.laminar_plan_create(desc(batch=8), np.full(8, 40000, np.int32), 256)
+    try:
+        assert N.lib().laminar_plan_num_dynamic_items(p) == 0
+    finally:
+        N.laminar_plan_destroy(p)
+    # cascade plans keep every item bound
+    p = N.laminar_plan_create_cascade(d, lens.astype(np.int32),
+                                      np.arange(256, dtype=np.int32) // 8,
+                                      np.full(32, 8, np.int32), 256)
+    try:
+        assert N.lib().laminar_plan_num_dynamic_items(p) == 0
+    finally:
+        N.laminar_plan_destroy(p)
+
+
 def test_planner_edge_lengths():
     for lens in ([0], [1], [16], [17], [0, 0, 0], [98304], [1, 98304, 0, 15]):
         d = desc(batch=len(lens), hq=64, hkv=8)

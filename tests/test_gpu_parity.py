@@ -148,6 +148,37 @@ def test_cascade_run_to_run_bitwise():
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
 
 
+def test_dynamic_tail_repeated_launches_bitwise():
+    """One plan launched five times: the tail counter is reset by each
+    launch's last pull, so every launch computes every item once and the
+    results are bitwise identical (the items' arithmetic does not depend on
+    which workgroup runs them)."""
+    from paper_2510_12633_amd import _native as N
+    from paper_2510_12633_amd.api import PagedDecodeAttention
+    _need_gpu()
+    wl = make_workload(get_config(2), device="cuda")
+    c = wl.cfg
+    att = PagedDecodeAttention(
+        batch=wl.batch, num_q_heads=c.num_q_heads, num_kv_heads=c.num_kv_heads,
+        head_dim=c.head_dim, num_pages=wl.num_pages,
+        max_blocks_per_seq=wl.block_table.shape[1], seq_lens_host=wl.seq_lens,
+        softmax_scale=wl.softmax_scale)
+    assert N.lib().laminar_plan_num_dynamic_items(att.plan) > 0
+    bt = torch.as_tensor(wl.block_table, device="cuda")
+    lens = torch.as_tensor(wl.seq_lens, device="cuda")
+    runs = []
+    for _ in range(5):
+        out, lse = att(wl.q, wl.k_pages, wl.v_pages, bt, lens)
+        torch.cuda.synchronize()
+        runs.append((out.cpu().numpy(), lse.cpu().numpy()))
+    for o, l in runs[1:]:
+        assert np.array_equal(o, runs[0][0]) and np.array_equal(l, runs[0][1])
+    seqs = _sample(wl.seq_lens, 6, 2)
+    ref = decode_attention_from_host(host_arrays(wl, seqs), workers=8)
+    check(runs[-1], ref, "7b_pre_repack dynamic tail, 5th launch", seqs=seqs)
+    att.close()
+
+
 def test_tiny_config_all_outputs():
     _need_gpu()
     wl = make_workload(1, device="cuda")
