@@ -329,38 +329,48 @@ QWEN7B_PROJECTIONS = {"qkv": (4608, 3584), "o": (3584, 3584),
 
 def measure_projections(torch, N, batches=(1, 16, 64), reps=20):
     """The skinny projection kernel on Qwen2.5-7B's projection shapes (w
-    [N, K] bf16), HIP-event time per call and weight bytes / time, next to
-    the library GEMM (torch.matmul) on the same operands."""
+    [N, K] bf16, packed once), HIP-event time per call and weight bytes /
+    time, next to the library GEMM (torch.matmul) on the same operands.
+    Calls cycle over enough copies of each weight (at least 512 MB) that
+    the 256 MB Infinity Cache cannot serve them, as in a decode step that
+    runs every layer once."""
     from paper_2510_12633_amd.api import SkinnyLinear
     gen = torch.Generator(device="cuda").manual_seed(9)
     stream = torch.cuda.current_stream()
     rows = []
     for name, (n, k) in QWEN7B_PROJECTIONS.items():
-        w = torch.randn((n, k), generator=gen, device="cuda").to(torch.bfloat16)
-        wt = w.t().contiguous()                    # [K, N] for x @ wt
-        lin = SkinnyLinear(w)
+        wbytes = 2 * n * k
+        copies = max(1, -(-(512 << 20) // wbytes))
+        lins, wts = [], []
+        for _ in range(copies):
+            w = torch.randn((n, k), generator=gen, device="cuda").to(torch.bfloat16)
+            wts.append(w.t().contiguous())         # [K, N] for x @ wt
+            lins.append(SkinnyLinear(w))
+            del w
+        calls = max(reps, 2 * copies)
         for m in batches:
             x = torch.randn((m, k), generator=gen, device="cuda").to(torch.bfloat16)
             out = torch.empty((m, n), device="cuda")
-            for fn_name, fn in (("laminar_linear", lambda: lin(x, out=out)),
-                                ("library_gemm", lambda: x @ wt)):
-                fn()
+            for fn_name, fn in (("laminar_linear", lambda i: lins[i % copies](x, out=out)),
+                                ("library_gemm", lambda i: x @ wts[i % copies])):
+                for i in range(copies):
+                    fn(i)
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
-                for _ in range(reps):
-                    fn()
+                for i in range(calls):
+                    fn(i)
                 e1.record(stream)
                 torch.cuda.synchronize()
-                us = 1e3 * e0.elapsed_time(e1) / reps
-                wbytes = 2 * n * k
+                us = 1e3 * e0.elapsed_time(e1) / calls
                 rows.append({"proj": name, "n": n, "k": k, "m": m,
                              "impl": fn_name, "us": round(us, 2),
+                             "weight_copies": copies,
                              "weight_GBps": round(wbytes / (us * 1e-6) / 1e9, 1),
                              "frac_hbm_peak": round(wbytes / (us * 1e-6) / 1e9
                                                     / HBM_PEAK_GBPS, 4)})
-        del w, wt, lin
-    torch.cuda.empty_cache()
+        del lins, wts
+        torch.cuda.empty_cache()
     return rows
 
 
@@ -392,14 +402,16 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     from paper_2510_12633_amd.api import SkinnyLinear
 
     class Proj:
-        """One projection's weight in both layouts: [N, K] for this
-        library's skinny kernel, [K, N] for the library GEMM (x @ w)."""
+        """One projection's weight in two layouts: packed by this library's
+        skinny kernel, and [K, N] for the library GEMM (x @ w)."""
 
         def __init__(self, k, n):
-            self.nk = (torch.randn((n, k), generator=gen, device="cuda",
-                                   dtype=bf) * (1.0 / k ** 0.5))
-            self.kn = self.nk.t().contiguous()
-            self.skinny = SkinnyLinear(self.nk)
+            nk = (torch.randn((n, k), generator=gen, device="cuda",
+                              dtype=bf) * (1.0 / k ** 0.5))
+            self.k = k
+            self.kn = nk.t().contiguous()
+            self.skinny = SkinnyLinear(nk)
+            del nk
             self.use_skinny = False
 
         def __call__(self, x):
@@ -413,30 +425,32 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
 
     def choose(m):
         """Per projection kind, the faster of the skinny kernel and the
-        library GEMM at this batch (timed on layer 0's weights)."""
+        library GEMM at this batch, timed over every layer's weights in turn
+        (as in a step, so the 256 MB Infinity Cache does not hold them)."""
         picks = {}
         for i, kind in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
-            p0 = lm_head if kind == "lm_head" else layers[0][i]
-            x = torch.randn((m, p0.nk.shape[1]), generator=gen, device="cuda",
+            projs = ([lm_head] * 4 if kind == "lm_head" else
+                     [layer[i] for layer in layers])
+            x = torch.randn((m, projs[0].k), generator=gen, device="cuda",
                             dtype=bf)
             times = {}
             for use in (False, True):
                 if use and m > 64:
                     continue
-                p0.use_skinny = use
-                p0(x)
+                for p in projs:
+                    p.use_skinny = use
+                projs[0](x)
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record()
-                for _ in range(5):
-                    p0(x)
+                for p in projs:
+                    p(x)
                 e1.record()
                 torch.cuda.synchronize()
                 times[use] = e0.elapsed_time(e1)
             best = min(times, key=times.get)
-            for lay in ([lm_head] if kind == "lm_head" else
-                        [layer[i] for layer in layers]):
-                lay.use_skinny = best
+            for p in projs:
+                p.use_skinny = best
             picks[kind] = "laminar_linear" if best else "library_gemm"
         return picks
 

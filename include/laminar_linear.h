@@ -18,15 +18,25 @@
  * accumulated in fp32 on the matrix cores; with several K splits the
  * partial sums are added in a fixed order, so results are deterministic.
  *
- * Limits: 1 <= M <= 64, N a multiple of 16, K a multiple of 128; larger
- * batches are compute-bound and belong to a general GEMM.
+ * Packed weights. laminar_linear reads w in a packed layout made once per
+ * weight by laminar_linear_pack: 16-row tiles, and within a tile 16-byte
+ * chunks (8 consecutive k of one row) ordered (k / 8, row):
+ *
+ *     packed[((n / 16) * (K / 8) + k / 8) * 16 + n % 16][k % 8] = w[n][k]
+ *
+ * (same size as w). The 16 rows x 32 k that one matrix-core step consumes
+ * are then 1 KB of contiguous bytes, which one wavefront load reads whole.
+ *
+ * Limits: 1 <= M <= 64, N a multiple of 16, K a multiple of 128 and at most
+ * 2^24; larger batches are compute-bound and belong to a general GEMM.
  * Workspace: laminar_linear_workspace_bytes(M, N, K) bytes of device
  * memory (0 when no K split is used), 256-byte aligned, owned by the
  * caller; calls that share a workspace must be ordered on one stream.
- * Pointers: x, w 16-byte aligned; y 16-byte aligned.
- * Errors: INVALID_ARG (NULL pointers, misalignment, a workspace smaller
- * than required), UNSUPPORTED (M, N or K outside the limits), HIP (launch
- * failure).
+ * Pointers: x, w, w_packed and y 16-byte aligned; the caller owns every
+ * buffer.
+ * Errors: INVALID_ARG (NULL pointers, misalignment, w_packed equal to w, a
+ * workspace smaller than required), UNSUPPORTED (M, N or K outside the
+ * limits), HIP (launch failure).
  */
 #ifndef LAMINAR_LINEAR_H
 #define LAMINAR_LINEAR_H
@@ -37,13 +47,20 @@
 extern "C" {
 #endif
 
+/* Writes the packed layout of w [N, K] bf16 to w_packed (same size, not
+ * overlapping w). Enqueued on `stream`; a pure permutation of 16-byte
+ * chunks. */
+laminar_status laminar_linear_pack(const void* w, void* w_packed, int32_t n,
+                                   int32_t k, hipStream_t stream);
+
 /* Number of K splits the call will use (1: none). 0 outside the limits. */
 int32_t laminar_linear_splits(int32_t m, int32_t n, int32_t k);
 
 /* Device workspace bytes for the K splits (0 when there are none). */
 size_t laminar_linear_workspace_bytes(int32_t m, int32_t n, int32_t k);
 
-laminar_status laminar_linear(const void* x, const void* w, float* y,
+/* y = x w^T with w given in the packed layout. */
+laminar_status laminar_linear(const void* x, const void* w_packed, float* y,
                               int32_t m, int32_t n, int32_t k,
                               void* workspace, size_t workspace_bytes,
                               hipStream_t stream);

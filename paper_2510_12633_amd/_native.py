@@ -115,6 +115,8 @@ _SIGNATURES = {
                                                 ctypes.c_int64, ctypes.c_int64,
                                                 ctypes.c_uint64, ctypes.c_uint64,
                                                 POINTER(ctypes.c_double)]),
+    "laminar_linear_pack": (c_int32, [c_void_p, c_void_p, c_int32, c_int32,
+                                      c_void_p]),
     "laminar_linear_splits": (c_int32, [c_int32, c_int32, c_int32]),
     "laminar_linear_workspace_bytes": (c_size_t, [c_int32, c_int32, c_int32]),
     "laminar_linear": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32, c_int32,
@@ -355,6 +357,11 @@ def laminar_migrate_pages(src_pool, src_pages: int, dst_pool, dst_pages: int,
         "laminar_migrate_pages")
 
 
+def laminar_linear_pack(w, w_packed, n: int, k: int, stream):
+    _check(lib().laminar_linear_pack(_ptr(w), _ptr(w_packed), int(n), int(k),
+                                     _ptr(stream)), "laminar_linear_pack")
+
+
 def laminar_linear_splits(m: int, n: int, k: int) -> int:
     return int(lib().laminar_linear_splits(int(m), int(n), int(k)))
 
@@ -363,9 +370,9 @@ def laminar_linear_workspace_bytes(m: int, n: int, k: int) -> int:
     return int(lib().laminar_linear_workspace_bytes(int(m), int(n), int(k)))
 
 
-def laminar_linear(x, w, y, m: int, n: int, k: int, workspace,
+def laminar_linear(x, w_packed, y, m: int, n: int, k: int, workspace,
                    workspace_bytes: int, stream):
-    _check(lib().laminar_linear(_ptr(x), _ptr(w), _ptr(y), int(m), int(n),
+    _check(lib().laminar_linear(_ptr(x), _ptr(w_packed), _ptr(y), int(m), int(n),
                                 int(k), _ptr(workspace), int(workspace_bytes),
                                 _ptr(stream)), "laminar_linear")
 

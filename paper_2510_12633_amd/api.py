@@ -169,12 +169,15 @@ def migrate(src_pools, dst_pools, pairs, stream=None):
 
 
 class SkinnyLinear:
-    """y = x w^T for decode batches (M <= 64): w [N, K] bf16 on the device;
-    owns the K-split workspace for up to max_m rows."""
+    """y = x w^T for decode batches (M <= 64): w [N, K] bf16 on the device is
+    packed once into the kernel's tiled layout (a copy of the same size);
+    owns that copy and the K-split workspace for up to max_m rows."""
 
-    def __init__(self, weight, max_m: int = 64):
-        self.w = weight
+    def __init__(self, weight, max_m: int = 64, stream=None):
         self.n, self.k = weight.shape
+        self.w_packed = torch.empty_like(weight)
+        N.laminar_linear_pack(weight, self.w_packed, self.n, self.k,
+                              _stream_handle(stream))
         self.ws_bytes = max(N.laminar_linear_workspace_bytes(m, self.n, self.k)
                             for m in range(1, max_m + 1))
         self.ws = (torch.empty(self.ws_bytes, dtype=torch.uint8,
@@ -184,6 +187,6 @@ class SkinnyLinear:
         m = x.shape[0]
         if out is None:
             out = torch.empty((m, self.n), dtype=torch.float32, device=x.device)
-        N.laminar_linear(x, self.w, out, m, self.n, self.k, self.ws,
+        N.laminar_linear(x, self.w_packed, out, m, self.n, self.k, self.ws,
                          self.ws_bytes, _stream_handle(stream))
         return out

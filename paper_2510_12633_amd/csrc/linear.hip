@@ -2,16 +2,25 @@
 // MI355X (gfx950).
 //
 // At decode batch sizes the product streams the whole weight matrix w
-// [N, K] for a few rows of x, so it is bound by HBM bandwidth. Each
-// wavefront owns 16 rows of w (16 output features) over a range of K and
-// runs v_mfma_f32_16x16x32_bf16 with the weights as the A operand and the
-// batch (padded to 16 per tile) as B, so each weight byte is read once and
-// used for all M rows. Within a step of 128 k values, matrix-core step j
-// takes k = 32j .. 32j+31, lane group q holding k = 32j + 8q .. +7 of its
-// row: each load instruction reads 64 contiguous bytes of each of 16 rows.
-// Loads run NB steps ahead of the step being computed (plain loads:
-// measured 10-25% faster here than non-temporal ones). When
-// N alone gives too few wavefronts to keep HBM busy, K is split and a
+// [N, K] for a few rows of x, so it is bound by HBM bandwidth. The weights
+// are packed once (laminar_linear_pack) into tiles of 16 rows whose 16-byte
+// chunks (8 consecutive k of one row) are ordered (tile, k / 8, row): the
+// 16 rows x 32 k that one v_mfma_f32_16x16x32_bf16 takes as its A operand
+// are then 1 KB of contiguous bytes, and one load instruction of a
+// wavefront reads exactly that.
+//
+// A workgroup is four wavefronts on four consecutive tiles (64 output
+// features) over one range of K. Per pipeline step of 128 k, each wavefront
+// loads its tile's 4 KB of weights (non-temporal: they are read once) and
+// the workgroup loads the batch's x [16 MT rows, 128 k] once and stages it
+// in LDS, from where every wavefront reads its B operand; so x is fetched
+// once per four tiles instead of once per tile (at M = 64 it would
+// otherwise be four times the weight traffic). NB steps of loads are in
+// flight. All loads are buffer loads whose range check returns zeros: rows
+// of x past M, the steps that pad the last group of NB, and a wavefront
+// past the last tile read zeros without touching memory, so no load is
+// conditional and the compiler keeps exact counts of the loads in flight.
+// When N alone gives too few wavefronts to keep HBM busy, K is split and a
 // second kernel adds the partial sums in a fixed order.
 
 #include <hip/hip_runtime.h>
@@ -28,99 +37,117 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kStepK = 128;          // k values per pipeline step
 constexpr int kMaxM = 64;
-constexpr int kTargetWaves = 2048;   // 2 per SIMD: ~16 MB of weights in flight
+constexpr int kMaxK = 1 << 24;       // keeps every buffer offset in 31 bits
+constexpr int kTargetWaves = 2048;   // 2 per SIMD: ~32 MB of weights in flight
+constexpr int kNB = 4;               // steps in flight
+constexpr int kOob = 0x40000000;     // past every buffer: reads as zero
+constexpr int kBufFlags = 0x00020000;
 
 struct LinearArgs {
   const uint16_t* x;     // [M, K]
-  const uint16_t* w;     // [N, K]
+  const uint16_t* w;     // packed [N/16][K/8][16][8]
   float* y;              // [M, N]
   float* part;           // [splits, M, N] when split
   int32_t m, n, k;
   int32_t n_tiles, splits, steps_per_split;
 };
 
-template <int MT>
-struct StepRegs {
-  u32x4 w[4];
-  u32x4 x[MT][4];
-};
-
-template <int MT>
-__device__ __forceinline__ void load_step(const LinearArgs& a, int row_n,
-                                          int kb, int q, int r16,
-                                          StepRegs<MT>& s) {
-  // load j of lane group q: k = kb + 32 j + 8 q .. +7, so each load
-  // instruction reads 64 contiguous bytes of each of the 16 rows
-  const u32x4* wp = reinterpret_cast<const u32x4*>(
-      a.w + size_t(row_n) * a.k + kb + 8 * q);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) s.w[j] = wp[4 * j];
-#pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    const int m = 16 * t + r16;
-    const bool ok = m < a.m;
-    const u32x4* xp = reinterpret_cast<const u32x4*>(
-        a.x + size_t(ok ? m : 0) * a.k + kb + 8 * q);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) s.x[t][j] = ok ? xp[4 * j] : u32x4{0, 0, 0, 0};
-  }
-}
-
-template <int MT>
-__device__ __forceinline__ void mma_step(const StepRegs<MT>& s,
-                                         f32x4 (&acc)[MT]) {
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const bf16x8 av = __builtin_bit_cast(bf16x8, s.w[j]);
-#pragma unroll
-    for (int t = 0; t < MT; ++t)
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-          av, __builtin_bit_cast(bf16x8, s.x[t][j]), acc[t], 0, 0, 0);
-  }
+// Waits for this wavefront's LDS writes, then for the whole workgroup; the
+// loads in flight are not waited for (a plain __syncthreads would drain
+// them). The empty asm statements keep the compiler from moving LDS
+// accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0); vmcnt, expcnt free
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 template <int MT>
 __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int gw = blockIdx.x * 4 + wave;                // global wavefront
-  if (gw >= a.n_tiles * a.splits) return;
-  const int tile = gw % a.n_tiles, split = gw / a.n_tiles;
+  // x of one step, double-buffered: chunk (t, k/8 = c, row r) at
+  // t * 256 + c * 16 + r, so the 64 lanes of a wavefront read 1 KB of
+  // consecutive chunks for each matrix-core step
+  __shared__ u32x4 xs[2][MT * 256];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tile = blockIdx.x * 4 + wave;
+  const bool has_tile = tile < a.n_tiles;
+  const int split = blockIdx.y;
   const int r16 = lane & 15, q = lane >> 4;
-  const int n0 = tile * 16;
   const int total_steps = a.k / kStepK;
   const int s0 = split * a.steps_per_split;
   const int s1 = min(total_steps, s0 + a.steps_per_split);
+  // this thread stages chunk (t, c = tid / 16, row tid % 16) of every step
+  const int x_row = tid & 15, x_chunk = tid >> 4;
+
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.w) + size_t(has_tile ? tile : 0) * 16 * a.k, 0,
+      has_tile ? a.k * 32 : 0, kBufFlags);
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.x), 0, a.m * a.k * 2, kBufFlags);
+  // lane (q, r16) of matrix-core step j holds row r16, k chunk 4 j + q
+  const int w_lane = (q * 16 + r16) * 16;
+
+  u32x4 wb[kNB][4];
+  u32x4 xb[kNB][MT];
+  auto load = [&](int s, int i) {
+    const bool in = s < s1;
+    const int kb = s * kStepK;
+    const int wo = in ? kb * 32 + w_lane : kOob;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      wb[i][j] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(wr, wo + 1024 * j, 0,
+                                                       /*nt*/ 2));
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      const int xo = in ? ((16 * t + x_row) * a.k + kb + 8 * x_chunk) * 2 : kOob;
+      xb[i][t] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xo, 0, 0));
+    }
+  };
 
   f32x4 acc[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // NB steps in flight: a ring of register buffers, refilled NB steps
-  // ahead of the step being computed
-  constexpr int NB = MT == 1 ? 4 : 2;
-  StepRegs<MT> buf[NB];
 #pragma unroll
-  for (int i = 0; i < NB; ++i)
-    if (s0 + i < s1) load_step<MT>(a, n0 + r16, (s0 + i) * kStepK, q, r16, buf[i]);
-  for (int st = s0; st < s1; st += NB) {
+  for (int i = 0; i < kNB; ++i) load(s0 + i, i);
+  // Steps past s1 (the last group padded to kNB steps) load zeros and add
+  // nothing, so every step runs the same code.
+  for (int st = s0; st < s1; st += kNB) {
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      if (st + i < s1) {
-        mma_step<MT>(buf[i], acc);
-        if (st + i + NB < s1)
-          load_step<MT>(a, n0 + r16, (st + i + NB) * kStepK, q, r16, buf[i]);
+    for (int i = 0; i < kNB; ++i) {
+      const int s = st + i;
+      u32x4* buf = xs[s & 1];
+#pragma unroll
+      for (int t = 0; t < MT; ++t) buf[t * 256 + tid] = xb[i][t];
+      // The buffer written here was last read two steps ago, before every
+      // wavefront passed the previous step's barrier.
+      lds_barrier();
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bf16x8 av = __builtin_bit_cast(bf16x8, wb[i][j]);
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              av, __builtin_bit_cast(bf16x8, buf[t * 256 + 64 * j + lane]),
+              acc[t], 0, 0, 0);
       }
+      load(s + kNB, i);
     }
   }
+  if (!has_tile) return;
 
-  // lane (group q, column r16) holds D[n0 + 4q + r][m = 16t + r16]
+  // lane (group q, column r16) holds D[16 tile + 4q + r][m = 16t + r16]
   float* dst = a.splits > 1 ? a.part + size_t(split) * a.m * a.n : a.y;
 #pragma unroll
   for (int t = 0; t < MT; ++t) {
     const int m = 16 * t + r16;
     if (m < a.m)
-      *reinterpret_cast<f32x4*>(dst + size_t(m) * a.n + n0 + 4 * q) = acc[t];
+      *reinterpret_cast<f32x4*>(dst + size_t(m) * a.n + tile * 16 + 4 * q) =
+          acc[t];
   }
 }
 
@@ -135,9 +162,26 @@ __global__ void __launch_bounds__(256) linear_reduce(const LinearArgs a) {
   reinterpret_cast<f32x4*>(a.y)[i] = s;
 }
 
+// w [N, K] -> packed [N/16][K/8][16][8]: one 16-byte chunk per thread,
+// indexed by its destination.
+__global__ void __launch_bounds__(256)
+pack_kernel(const u32x4* __restrict__ w, u32x4* __restrict__ out, int32_t n,
+            int32_t k) {
+  const size_t i = size_t(blockIdx.x) * 256 + threadIdx.x;
+  const size_t chunks = size_t(k) / 8;
+  if (i >= size_t(n) * chunks) return;
+  const size_t row = i & 15, rest = i >> 4;
+  const size_t c = rest % chunks, tile = rest / chunks;
+  out[i] = w[(tile * 16 + row) * chunks + c];
+}
+
+bool shape_ok(int32_t n, int32_t k) {
+  return n >= 16 && n % 16 == 0 && k >= kStepK && k % kStepK == 0 &&
+         k <= kMaxK;
+}
+
 bool shape_ok(int32_t m, int32_t n, int32_t k) {
-  return m >= 1 && m <= kMaxM && n >= 16 && n % 16 == 0 && k >= kStepK &&
-         k % kStepK == 0;
+  return m >= 1 && m <= kMaxM && shape_ok(n, k);
 }
 
 void split_plan(int32_t n, int32_t k, int32_t* splits, int32_t* per) {
@@ -149,9 +193,25 @@ void split_plan(int32_t n, int32_t k, int32_t* splits, int32_t* per) {
   *splits = (steps + *per - 1) / *per;
 }
 
+bool misaligned16(const void* p) {
+  return reinterpret_cast<uintptr_t>(p) & 15;
+}
+
 }  // namespace
 
 extern "C" {
+
+laminar_status laminar_linear_pack(const void* w, void* w_packed, int32_t n,
+                                   int32_t k, hipStream_t stream) {
+  if (!w || !w_packed || w == w_packed) return LAMINAR_ERR_INVALID_ARG;
+  if (misaligned16(w) || misaligned16(w_packed)) return LAMINAR_ERR_INVALID_ARG;
+  if (!shape_ok(n, k)) return LAMINAR_ERR_UNSUPPORTED;
+  const size_t chunks = size_t(n) * k / 8;
+  hipLaunchKernelGGL(pack_kernel, dim3(unsigned((chunks + 255) / 256)),
+                     dim3(256), 0, stream, static_cast<const u32x4*>(w),
+                     static_cast<u32x4*>(w_packed), n, k);
+  return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+}
 
 int32_t laminar_linear_splits(int32_t m, int32_t n, int32_t k) {
   if (!shape_ok(m, n, k)) return 0;
@@ -165,17 +225,16 @@ size_t laminar_linear_workspace_bytes(int32_t m, int32_t n, int32_t k) {
   return s > 1 ? (size_t(s) * m * n * sizeof(float) + 255) & ~size_t(255) : 0;
 }
 
-laminar_status laminar_linear(const void* x, const void* w, float* y,
+laminar_status laminar_linear(const void* x, const void* w_packed, float* y,
                               int32_t m, int32_t n, int32_t k, void* workspace,
                               size_t workspace_bytes, hipStream_t stream) {
-  if (!x || !w || !y) return LAMINAR_ERR_INVALID_ARG;
-  if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(w) |
-       reinterpret_cast<uintptr_t>(y)) & 15)
+  if (!x || !w_packed || !y) return LAMINAR_ERR_INVALID_ARG;
+  if (misaligned16(x) || misaligned16(w_packed) || misaligned16(y))
     return LAMINAR_ERR_INVALID_ARG;
   if (!shape_ok(m, n, k)) return LAMINAR_ERR_UNSUPPORTED;
   LinearArgs a;
   a.x = static_cast<const uint16_t*>(x);
-  a.w = static_cast<const uint16_t*>(w);
+  a.w = static_cast<const uint16_t*>(w_packed);
   a.y = y;
   a.m = m;
   a.n = n;
@@ -190,13 +249,11 @@ laminar_status laminar_linear(const void* x, const void* w, float* y,
       return LAMINAR_ERR_INVALID_ARG;
     a.part = static_cast<float*>(workspace);
   }
-  const int waves = a.n_tiles * a.splits;
-  const dim3 grid((waves + 3) / 4);
+  const dim3 grid((a.n_tiles + 3) / 4, a.splits);
   const int mt = (m + 15) / 16;
   switch (mt) {
     case 1: hipLaunchKernelGGL(linear_kernel<1>, grid, dim3(256), 0, stream, a); break;
     case 2: hipLaunchKernelGGL(linear_kernel<2>, grid, dim3(256), 0, stream, a); break;
-    case 3: hipLaunchKernelGGL(linear_kernel<3>, grid, dim3(256), 0, stream, a); break;
     default: hipLaunchKernelGGL(linear_kernel<4>, grid, dim3(256), 0, stream, a); break;
   }
   if (hipGetLastError() != hipSuccess) return LAMINAR_ERR_HIP;

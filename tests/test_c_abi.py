@@ -428,6 +428,14 @@ def test_linear_errors_before_any_launch():
     assert lib.laminar_linear(16, 16, 16, 65, 16, 128, None, 0, None) == UNS
     assert lib.laminar_linear(16, 16, 16, 1, 24, 128, None, 0, None) == UNS
     assert lib.laminar_linear(16, 16, 16, 1, 16, 100, None, 0, None) == UNS
+    assert lib.laminar_linear(16, 16, 16, 1, 16, (1 << 24) + 128, None, 0,
+                              None) == UNS
+    # packing: NULL, in place, misaligned, shapes
+    assert lib.laminar_linear_pack(None, 16, 16, 128, None) == INV
+    assert lib.laminar_linear_pack(16, 16, 16, 128, None) == INV
+    assert lib.laminar_linear_pack(16, 40, 16, 128, None) == INV
+    assert lib.laminar_linear_pack(16, 32, 24, 128, None) == UNS
+    assert lib.laminar_linear_pack(16, 32, 16, 100, None) == UNS
     # a K split needs a workspace
     assert N.laminar_linear_splits(64, 3584, 18944) > 1
     need = N.laminar_linear_workspace_bytes(64, 3584, 18944)
@@ -504,3 +512,29 @@ def test_attention_kernels_do_not_spill_in_the_page_loop():
         if line.strip() == "s_endpgm":
             fn = None
     assert not bad, bad[:4]
+
+
+def test_linear_kernels_use_no_scratch():
+    """The projection kernels keep every pipeline buffer in registers: no
+    scratch at all, and at least two wavefronts per SIMD."""
+    from paper_2510_12633_amd import build as B
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    src = os.path.join(B.CSRC, "linear.hip")
+    r = subprocess.run([hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17",
+                        "-Xclang", "-target-feature", "-Xclang",
+                        "-packed-fp32-ops", "-I", B.INCLUDE, "-I", B.CSRC,
+                        "-c", src, "-o", os.devnull,
+                        "-Rpass-analysis=kernel-resource-usage"],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-2000:]
+    names = re.findall(r"Function Name: (\S+)", r.stderr)
+    scratch = [int(x) for x in
+               re.findall(r"ScratchSize \[bytes/lane\]: (\d+)", r.stderr)]
+    occ = [int(x) for x in re.findall(r"Occupancy \[waves/SIMD\]: (\d+)",
+                                      r.stderr)]
+    kernels = [(n, sc, o) for n, sc, o in zip(names, scratch, occ)
+               if "linear_kernel" in n]
+    assert len(kernels) == 3, kernels      # 16, 32 and 64 batch rows
+    assert all(sc == 0 and o >= 2 for _, sc, o in kernels), kernels

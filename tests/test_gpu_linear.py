@@ -53,6 +53,22 @@ def test_linear_matches_oracle(m, n, k):
     assert torch.isnan(y[m:]).all()                        # padding untouched
 
 
+@pytest.mark.parametrize("n,k", [(16, 128), (48, 384), (4608, 3584)])
+def test_pack_is_the_documented_permutation(n, k):
+    """packed[((n/16)(K/8) + k/8) 16 + n%16][k%8] = w[n][k], bit for bit."""
+    from paper_2510_12633_amd import _native as N
+    _need_gpu()
+    g = torch.Generator(device="cuda").manual_seed(n + k)
+    w = torch.randint(-2 ** 15, 2 ** 15, (n, k), generator=g, device="cuda",
+                      dtype=torch.int32).to(torch.int16)
+    p = torch.empty_like(w)
+    N.laminar_linear_pack(w, p, n, k, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    ref = (w.cpu().numpy().reshape(n // 16, 16, k // 8, 8)
+           .transpose(0, 2, 1, 3).reshape(n, k))
+    assert np.array_equal(p.cpu().numpy(), ref)
+
+
 def test_linear_errors():
     from paper_2510_12633_amd import _native as N
     _need_gpu()
@@ -65,6 +81,12 @@ def test_linear_errors():
     assert e.value.status == N.LAMINAR_ERR_UNSUPPORTED
     with pytest.raises(N.LaminarError) as e:
         N.laminar_linear(x, w, y, 4, 32, 200, None, 0, s)
+    assert e.value.status == N.LAMINAR_ERR_UNSUPPORTED
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_linear_pack(w, w, 32, 256, s)
+    assert e.value.status == N.LAMINAR_ERR_INVALID_ARG
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_linear_pack(w, y, 24, 256, s)
     assert e.value.status == N.LAMINAR_ERR_UNSUPPORTED
     need = N.laminar_linear_workspace_bytes(4, 32, 256)
     N.laminar_linear(x, w, y, 4, 32, 256,
