@@ -726,6 +726,8 @@ def main(argv=None):
         "algorithmic_bytes": alg_bytes,
         "kernel_ms": {"decode_items": round(k1_ms, 5),
                       "decode_merge": round(k2_ms, 5)},
+        "kernel_ms_median": {"decode_items": round(sorted(k1)[len(k1) // 2], 5),
+                             "decode_merge": round(sorted(k2)[len(k2) // 2], 5)},
         "plan_host_ms": round(sum(plan_ns) / max(len(plan_ns), 1) / 1e6, 5)
         if plan_ns else None,
         "wall_s_timed": round(wall, 4),

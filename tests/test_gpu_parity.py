@@ -343,7 +343,8 @@ def _sample(lens, k, seed):
 
 
 @pytest.mark.parametrize("idx,cascade", [(2, False), (3, False), (4, False),
-                                         (5, False), (5, True)])
+                                         (5, False), (5, True), (6, False),
+                                         (7, True)])
 def test_full_size_config_sampled(idx, cascade):
     """Full-size batch in the bench's launch configuration; the oracle checks
     sampled trajectories (shortest, longest, median and random ones)."""
@@ -353,7 +354,7 @@ def test_full_size_config_sampled(idx, cascade):
     wl = make_workload(cfg, device="cuda")
     out, lse = run_gpu(wl, cascade=cascade)
     assert np.isfinite(out).all() and np.isfinite(lse).all()
-    seqs = _sample(wl.seq_lens, 6 if idx == 5 else 8, idx)
+    seqs = _sample(wl.seq_lens, 6 if idx in (5, 7) else 8, idx)
     ref = decode_attention_from_host(host_arrays(wl, seqs), workers=8)
     check((out, lse), ref, f"{cfg.name}{' cascade' if cascade else ''} "
           f"sampled {seqs}", seqs=seqs)

@@ -34,6 +34,17 @@ def test_length_models_match_config_text():
     assert l5[long_].max() <= 98304
 
 
+def test_tensor_parallel_shares_keep_the_batch():
+    """A TP share is the parent's batch with 1/TP of its heads."""
+    for share, parent, tp in (("32b_fp8_tp4", 4, 4), ("agentic_mix_tp8", 5, 8)):
+        s, p = get_config(share), get_config(parent)
+        assert np.array_equal(_layout(s)[1], _layout(p)[1])
+        assert (s.num_q_heads * tp, s.num_kv_heads * tp) == (p.num_q_heads,
+                                                            p.num_kv_heads)
+        assert (s.kv_dtype, s.prefix_group, s.prefix_tokens) == (
+            p.kv_dtype, p.prefix_group, p.prefix_tokens)
+
+
 def test_page_counts_and_pool_occupancy():
     for idx in (1, 2, 3, 4):
         cfg, lens, (num_pages, table, valid) = _layout(idx)

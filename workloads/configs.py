@@ -62,6 +62,7 @@ class WorkloadConfig:
     prefix_tokens: int = 0     # shared prompt tokens per group
     pool_pages: Optional[int] = None   # fixed pool size; None: 1.0625 x needed
     description: str = ""
+    seed_of: int = 0           # draw with this workload's seed (0: own index)
 
     @property
     def group_size(self) -> int:
@@ -73,7 +74,7 @@ class WorkloadConfig:
 
     @property
     def default_seed(self) -> int:
-        return 1000 + self.index
+        return 1000 + (self.seed_of or self.index)
 
     @property
     def kv_elem_bytes(self) -> int:
@@ -120,7 +121,29 @@ CONFIGS = (
                     "1024-token prompt prefix; 64q/8kv, bf16 KV"),
 )
 
-BY_NAME = {c.name: c for c in CONFIGS}
+# One GPU's share of the two larger models under the tensor parallelism the
+# paper rolls them out with (appendix, hyperparameter details: TP 4 for 32B,
+# TP 8 for 72B, whose head counts the agentic mix uses): the same
+# trajectories and lengths, the kv-heads split across GPUs with their query
+# heads. Attention needs no exchange between the shares, so one GPU's call
+# is exactly this.
+TP_SHARES = (
+    WorkloadConfig(
+        name="32b_fp8_tp4", index=6, batch=128, num_q_heads=10,
+        num_kv_heads=2, head_dim=128, kv_dtype="fp8_e4m3fn",
+        lengths=CONFIGS[3].lengths, seed_of=4,
+        description="32b_fp8 on one GPU of four: 10q/2kv heads, the same "
+                    "trajectory lengths"),
+    WorkloadConfig(
+        name="agentic_mix_tp8", index=7, batch=512, num_q_heads=8,
+        num_kv_heads=1, head_dim=128, kv_dtype="bf16",
+        lengths=CONFIGS[4].lengths, prefix_group=8, prefix_tokens=1024,
+        seed_of=5,
+        description="agentic_mix on one GPU of eight: 8q/1kv heads, the "
+                    "same trajectory lengths and shared prefixes"),
+)
+
+BY_NAME = {c.name: c for c in CONFIGS + TP_SHARES}
 
 
 def get_config(key) -> WorkloadConfig:
@@ -128,5 +151,5 @@ def get_config(key) -> WorkloadConfig:
     if isinstance(key, WorkloadConfig):
         return key
     if isinstance(key, int) or (isinstance(key, str) and key.isdigit()):
-        return CONFIGS[int(key) - 1]
+        return (CONFIGS + TP_SHARES)[int(key) - 1]
     return BY_NAME[key]
