@@ -222,16 +222,6 @@ __device__ __forceinline__ ItemCtx item_ctx(const DecodeArgs& a, int unit,
   return c;
 }
 
-// Block-table entries of pages w*64 .. w*64+63 of the item, one per lane
-// (-1 beyond the item).
-__device__ __forceinline__ int load_window(const DecodeArgs& a,
-                                           const ItemCtx& c, int w, int lane) {
-  const int j = w * 64 + lane;
-  return j < c.npages
-             ? a.block_table[size_t(c.b) * a.max_blocks + c.p0 + j]
-             : -1;
-}
-
 // Query fragment (B operand of QK^T): lane holds the row of head slot r16
 // (query head h of trajectory b when ok, zero otherwise), dims
 // (gq*KK + kk)*8 .. +7 for each step kk.
@@ -249,52 +239,74 @@ __device__ __forceinline__ void load_q(const DecodeArgs& a, int b, int h,
   }
 }
 
-// Issue the loads of pages ja and ja+1 of the item (ja even; btv is the
-// block-table window holding them). Pages past the item, or whose table
-// entry lies outside the pool, get no valid tokens and read page 0.
+// Issue the loads of pages ja and ja+1 of the item (ja even). The two
+// block-table entries are read through the scalar cache (the index is
+// wave-uniform), and each page is read through a buffer resource whose size
+// is the tile for a valid page and zero otherwise: pages past the item
+// (including the whole pair after the last one, issued unconditionally),
+// table entries outside the pool and the second page of an odd tail read
+// zeros without touching memory. No load is conditional, so the compiler
+// counts the loads in flight exactly and the next pair's loads overlap the
+// current pair's arithmetic.
+typedef const __attribute__((address_space(4))) int32_t* ConstI32;
+typedef const __attribute__((address_space(4))) float* ConstF32;
+constexpr int kBufFlags = 0x00020000;
+
 template <int D, bool FP8>
 __device__ __forceinline__ void issue_pair(const DecodeArgs& a,
-                                           const ItemCtx& c, int ja, int btv,
+                                           const ItemCtx& c, int ja,
                                            int koff, int voff,
                                            PairRegs<D, FP8>& pr) {
   using G = Geo<D, FP8>;
-  const bool has_b = ja + 1 < c.npages;
-  int ppa = __builtin_amdgcn_readlane(btv, ja & 63);
-  int ppb = has_b ? __builtin_amdgcn_readlane(btv, (ja + 1) & 63) : ppa;
+  const ConstI32 row =
+      (ConstI32)(a.block_table + size_t(c.b) * a.max_blocks + c.p0);
+  const int last = max(c.npages - 1, 0);
+  int ppa = row[min(ja, last)];
+  int ppb = row[min(ja + 1, last)];
   const int base_tok = (c.p0 + ja) * 16;
-  int nva = min(16, c.len - base_tok);
-  int nvb = has_b ? min(16, c.len - base_tok - 16) : 0;
+  int nva = ja < c.npages ? min(16, c.len - base_tok) : 0;
+  int nvb = ja + 1 < c.npages ? min(16, c.len - base_tok - 16) : 0;
   if (ppa < 0 || ppa >= a.num_pages) { ppa = 0; nva = 0; }
   if (ppb < 0 || ppb >= a.num_pages) { ppb = 0; nvb = 0; }
   pr.nva = nva;
   pr.nvb = nvb;
   pr.base = base_tok;
   const size_t page_stride = size_t(a.hkv) * G::TILE;
-  const uint8_t* kbase = a.k_pages + size_t(c.kvh) * G::TILE;
-  const uint8_t* vbase = a.v_pages + size_t(c.kvh) * G::TILE;
-  const u32x4* ka = reinterpret_cast<const u32x4*>(kbase + size_t(ppa) * page_stride);
-  const u32x4* kb = reinterpret_cast<const u32x4*>(kbase + size_t(ppb) * page_stride);
-  const u32x4* va = reinterpret_cast<const u32x4*>(vbase + size_t(ppa) * page_stride);
-  const u32x4* vb = reinterpret_cast<const u32x4*>(vbase + size_t(ppb) * page_stride);
+  uint8_t* kbase = const_cast<uint8_t*>(a.k_pages) + size_t(c.kvh) * G::TILE;
+  uint8_t* vbase = const_cast<uint8_t*>(a.v_pages) + size_t(c.kvh) * G::TILE;
+  const __amdgpu_buffer_rsrc_t kra = __builtin_amdgcn_make_buffer_rsrc(
+      kbase + size_t(ppa) * page_stride, 0, nva > 0 ? G::TILE : 0, kBufFlags);
+  const __amdgpu_buffer_rsrc_t krb = __builtin_amdgcn_make_buffer_rsrc(
+      kbase + size_t(ppb) * page_stride, 0, nvb > 0 ? G::TILE : 0, kBufFlags);
+  const __amdgpu_buffer_rsrc_t vra = __builtin_amdgcn_make_buffer_rsrc(
+      vbase + size_t(ppa) * page_stride, 0, nva > 0 ? G::TILE : 0, kBufFlags);
+  const __amdgpu_buffer_rsrc_t vrb = __builtin_amdgcn_make_buffer_rsrc(
+      vbase + size_t(ppb) * page_stride, 0, nvb > 0 ? G::TILE : 0, kBufFlags);
   // KV pages are streamed once per call: non-temporal loads keep them from
   // displacing reusable lines in L2 and the Infinity Cache.
 #pragma unroll
   for (int j = 0; j < G::KL; ++j)
-    pr.ka[j] = __builtin_nontemporal_load(&ka[koff + j * 16]);
+    pr.ka[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+        kra, (koff + j * 16) * 16, 0, 2));
 #pragma unroll
   for (int j = 0; j < G::KL; ++j)
-    pr.kb[j] = __builtin_nontemporal_load(&kb[koff + j * 16]);
+    pr.kb[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+        krb, (koff + j * 16) * 16, 0, 2));
 #pragma unroll
   for (int j = 0; j < G::VL; ++j)
-    pr.va[j] = __builtin_nontemporal_load(&va[voff + j * 16]);
+    pr.va[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+        vra, (voff + j * 16) * 16, 0, 2));
 #pragma unroll
   for (int j = 0; j < G::VL; ++j)
-    pr.vb[j] = __builtin_nontemporal_load(&vb[voff + j * 16]);
+    pr.vb[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+        vrb, (voff + j * 16) * 16, 0, 2));
   if constexpr (FP8) {
-    pr.ksa = a.k_scale[size_t(ppa) * a.hkv + c.kvh];
-    pr.ksb = a.k_scale[size_t(ppb) * a.hkv + c.kvh];
-    pr.vsa = a.v_scale[size_t(ppa) * a.hkv + c.kvh];
-    pr.vsb = a.v_scale[size_t(ppb) * a.hkv + c.kvh];
+    const ConstF32 ks = (ConstF32)(a.k_scale);
+    const ConstF32 vs = (ConstF32)(a.v_scale);
+    pr.ksa = ks[size_t(ppa) * a.hkv + c.kvh];
+    pr.ksb = ks[size_t(ppb) * a.hkv + c.kvh];
+    pr.vsa = vs[size_t(ppa) * a.hkv + c.kvh];
+    pr.vsb = vs[size_t(ppb) * a.hkv + c.kvh];
   }
 }
 
@@ -546,27 +558,19 @@ decode_items(const DecodeArgs a) {
     Acc<D> st;
     st.reset();
 
-    int win = -1, btv = -1;
-    auto issue = [&](PairRegs<D, FP8>& pr, int jp) {
-      const int ja = 2 * jp;
-      if ((ja >> 6) != win) {
-        win = ja >> 6;
-        btv = load_window(a, c, win, lane);
-      }
-      issue_pair<D, FP8>(a, c, ja, btv, koff, voff, pr);
-    };
-
     PairRegs<D, FP8> buf0, buf1;
     int jp = jp0;
-    if (jp < npairs) issue(buf0, jp);
+    issue_pair<D, FP8>(a, c, 2 * jp, koff, voff, buf0);
     while (jp < npairs) {
       int jn = jp + stride;
-      if (jn < npairs) issue(buf1, jn);
+      issue_pair<D, FP8>(a, c, 2 * jn, koff, voff, buf1);
+      __builtin_amdgcn_sched_barrier(0);   // next pair's loads go out first
       compute_pair<D, FP8>(a, qf, buf0, st, gq, cascade, sm_row_len);
       jp = jn;
       if (jp >= npairs) break;
       jn = jp + stride;
-      if (jn < npairs) issue(buf0, jn);
+      issue_pair<D, FP8>(a, c, 2 * jn, koff, voff, buf0);
+      __builtin_amdgcn_sched_barrier(0);
       compute_pair<D, FP8>(a, qf, buf1, st, gq, cascade, sm_row_len);
       jp = jn;
     }
