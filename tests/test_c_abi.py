@@ -472,9 +472,9 @@ def test_planner_under_address_and_ub_sanitizers(tmp_path):
 def test_attention_kernels_do_not_spill_in_the_page_loop():
     """The page-pair double buffer fills most of the register file. A spill
     inside the page loop costs ~15% of bandwidth, so no attention kernel
-    instantiation may touch scratch inside a loop; at most one register may
-    be parked across the loop (a store before, a load after), and every
-    instantiation keeps two wavefronts per SIMD."""
+    instantiation may use scratch at all (the loop check below names the
+    offending lines if one ever does), and every instantiation keeps two
+    wavefronts per SIMD."""
     from paper_2510_12633_amd import build as B
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     if not os.path.exists(hipcc):
@@ -496,7 +496,7 @@ def test_attention_kernels_do_not_spill_in_the_page_loop():
     kernels = [(n, sc, o) for n, sc, o in zip(names, scratch, occ)
                if "decode_items" in n]
     assert len(kernels) == 24   # 2 head dims x 2 dtypes x 3 waves x cascade
-    assert all(sc <= 8 and o >= 2 for _, sc, o in kernels), kernels
+    assert all(sc == 0 and o >= 2 for _, sc, o in kernels), kernels
     r = subprocess.run(base + ["--cuda-device-only", "-S", src, "-o", "-"],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
