@@ -58,8 +58,10 @@ def parse_args(argv=None):
     p.add_argument("--no-append", action="store_true",
                    help="skip the KV-append timing")
     p.add_argument("--latency-curve", action="store_true",
-                   help="also time full Qwen2.5-7B-shaped decode steps over "
+                   help="also time full Qwen2.5-shaped decode steps over "
                         "batch sizes (the latency-versus-batch curve)")
+    p.add_argument("--curve-model", choices=sorted(CURVE_MODELS),
+                   default="qwen7b", help="decoder shape for --latency-curve")
     p.add_argument("--no-projections", action="store_true",
                    help="skip the skinny projection kernel timing")
     p.add_argument("--curve-batches", default="",
@@ -374,10 +376,18 @@ def measure_projections(torch, N, batches=(1, 16, 64), reps=20):
     return rows
 
 
+CURVE_MODELS = {
+    # layers, hidden, q heads, kv heads, head dim, intermediate, vocab
+    "qwen7b": ("Qwen2.5-7B", (28, 3584, 28, 4, 128, 18944, 152064)),
+    "qwen32b": ("Qwen2.5-32B", (64, 5120, 40, 8, 128, 27648, 152064)),
+}
+
+
 def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                                      512, 768, 1024),
-                  contexts=(16, 2048), reps=5):
-    """One decode step of a Qwen2.5-7B-shaped decoder (28 layers, random
+                  contexts=(16, 2048), reps=5, model="qwen7b"):
+    """One decode step of a Qwen2.5-7B- or 32B-shaped decoder (28 or 64
+    layers, all on this one GPU, random
     bf16 weights; per layer RMS pre-norms, the QKV, O, gate+up and down
     projections, this library's KV append and paged attention, SwiGLU and
     residuals; then the LM head) captured in a HIP graph and timed at each
@@ -390,7 +400,7 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     Rotary embedding and biases are left out."""
     import numpy as np
     from paper_2510_12633_amd.api import PagedDecodeAttention, kv_append
-    L, h, hq, hkv, d, inter, vocab = 28, 3584, 28, 4, 128, 18944, 152064
+    model_name, (L, h, hq, hkv, d, inter, vocab) = CURVE_MODELS[model]
     shape = N.LaminarModelShape(layers=L, hidden=h, q_heads=hq, kv_heads=hkv,
                                 head_dim=d, intermediate=inter, vocab=vocab,
                                 weight_bytes=2, act_bytes=2, kv_bytes=2)
@@ -544,7 +554,8 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                        "first_batch_10pct_slower_than_batch_1": knee})
     del layers, lm_head, Proj
     torch.cuda.empty_cache()
-    return {"model": "Qwen2.5-7B shapes, random bf16 weights, 28 layers + LM head",
+    return {"model": f"{model_name} shapes, random bf16 weights, {L} layers "
+                     "+ LM head",
             "roofline_batch_bound": bound, "peak_flops": peak_f,
             "peak_bw": peak_bw, "curves": curves}
 
@@ -749,7 +760,7 @@ def main(argv=None):
     if not args.no_projections:
         result["projections"] = measure_projections(torch, N)
     if args.latency_curve:
-        kw = {}
+        kw = {"model": args.curve_model}
         if args.curve_batches:
             kw["batches"] = tuple(int(x) for x in args.curve_batches.split(","))
         if args.curve_contexts:
