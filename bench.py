@@ -387,11 +387,11 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                                      512, 768, 1024),
                   contexts=(16, 2048), reps=5, model="qwen7b"):
     """One decode step of a Qwen2.5-7B- or 32B-shaped decoder (28 or 64
-    layers, all on this one GPU, random
-    bf16 weights; per layer RMS pre-norms, the QKV, O, gate+up and down
-    projections, this library's KV append and paged attention, SwiGLU and
-    residuals; then the LM head) captured in a HIP graph and timed at each
-    batch size. Each projection kind runs the faster of this library's
+    layers, all on this one GPU, random bf16 weights; per layer this
+    library's RMS pre-norms, the QKV, O, gate+up and down projections (the
+    O and down ones adding the residual stream), its KV append, paged
+    attention and SwiGLU; then the LM head) captured in a HIP graph and
+    timed at each batch size. Each projection kind runs the faster of this library's
     skinny kernel (batches up to 64) and the library GEMM, timed first at
     that batch; next to the roofline model's step
     time and batch bound. Every replay is checked bit for bit against the
@@ -409,7 +409,7 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     gen = torch.Generator(device="cuda").manual_seed(3)
     bf = torch.bfloat16
 
-    from paper_2510_12633_amd.api import SkinnyLinear
+    from paper_2510_12633_amd.api import SkinnyLinear, rmsnorm, silu_mul
 
     class Proj:
         """One projection's weight in two layouts: packed by this library's
@@ -424,10 +424,14 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             del nk
             self.use_skinny = False
 
-        def __call__(self, x):
+        def __call__(self, x, residual=None):
+            """bf16(x w^T), plus residual when given (in place into it on
+            the skinny path)."""
             if self.use_skinny:
-                return self.skinny(x).to(bf)
-            return x @ self.kn
+                return self.skinny.bf16(x, out=residual, residual=residual)
+            if residual is None:
+                return x @ self.kn
+            return torch.addmm(residual, x, self.kn)
 
     layers = [(Proj(h, (hq + 2 * hkv) * d), Proj(hq * d, h),
                Proj(h, 2 * inter), Proj(inter, h)) for _ in range(L)]
@@ -488,25 +492,19 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
 
             def step():
                 cur = torch.cuda.current_stream()
-                x = x0
-
-                def rms(t):                       # pre-norm, keeps x finite
-                    tf = t.float()
-                    return (tf * torch.rsqrt(tf.pow(2).mean(-1, keepdim=True)
-                                             + 1e-6)).to(bf)
+                x = x0.clone()                    # the residual stream
 
                 for wqkv, wo, wgu, wd in layers:
-                    qkv = wqkv(rms(x))
+                    qkv = wqkv(rmsnorm(x, stream=cur))
                     q = qkv[:, :hq * d].reshape(m, hq, d).contiguous()
                     k_new = qkv[:, hq * d:(hq + hkv) * d].reshape(m, hkv, d).contiguous()
                     v_new = qkv[:, (hq + hkv) * d:].reshape(m, hkv, d).contiguous()
                     kv_append(k_new, v_new, table, lens, kp, vp, stream=cur)
                     att(q, kp, vp, table, lens, out, lse, stream=cur)
-                    x = x + wo(out.view(m, hq * d).to(bf))
-                    gu = wgu(rms(x))
-                    x = x + wd(torch.nn.functional.silu(gu[:, :inter])
-                               * gu[:, inter:])
-                return lm_head(rms(x))
+                    x = wo(out.view(m, hq * d).to(bf), residual=x)
+                    gu = wgu(rmsnorm(x, stream=cur))
+                    x = wd(silu_mul(gu, stream=cur), residual=x)
+                return lm_head(rmsnorm(x, stream=cur))
 
             # The step is ~400 launches: capture it in a HIP graph so the
             # curve shows the GPU's time, not the host's launch rate.

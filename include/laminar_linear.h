@@ -65,6 +65,17 @@ laminar_status laminar_linear(const void* x, const void* w_packed, float* y,
                               void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/* The same product with a bf16 output: y[m, n] = bf16(sum_k x[m, k] w[n, k]
+ * + residual[m, n]), the fp32 sum (and the bf16 residual, if not NULL)
+ * rounded once to nearest even. y and residual are [M, N] bf16, 16-byte
+ * aligned, and may be the same buffer (an in-place residual add); the
+ * decode step uses it for the projections whose outputs feed the next
+ * bf16 operation, with the residual for O and down. */
+laminar_status laminar_linear_bf16(const void* x, const void* w_packed,
+                                   void* y, const void* residual, int32_t m,
+                                   int32_t n, int32_t k, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -27,4 +27,5 @@ from ._native import (LaminarModelShape, LaminarRolloutState,
                       laminar_roofline_step_seconds)
 from ._native import (laminar_linear, laminar_linear_pack, laminar_linear_splits,
                       laminar_linear_workspace_bytes)
-from .api import PagedDecodeAttention, SkinnyLinear, kv_append, migrate
+from .api import (PagedDecodeAttention, SkinnyLinear, kv_append, migrate,
+                  rmsnorm, silu_mul)

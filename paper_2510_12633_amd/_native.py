@@ -117,6 +117,13 @@ _SIGNATURES = {
                                                 POINTER(ctypes.c_double)]),
     "laminar_linear_pack": (c_int32, [c_void_p, c_void_p, c_int32, c_int32,
                                       c_void_p]),
+    "laminar_linear_bf16": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p,
+                                      c_int32, c_int32, c_int32, c_void_p,
+                                      c_size_t, c_void_p]),
+    "laminar_rmsnorm": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32,
+                                  c_int32, ctypes.c_float, c_void_p]),
+    "laminar_silu_mul": (c_int32, [c_void_p, c_void_p, c_int32, c_int32,
+                                   c_void_p]),
     "laminar_linear_splits": (c_int32, [c_int32, c_int32, c_int32]),
     "laminar_linear_workspace_bytes": (c_size_t, [c_int32, c_int32, c_int32]),
     "laminar_linear": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32, c_int32,
@@ -375,6 +382,24 @@ def laminar_linear(x, w_packed, y, m: int, n: int, k: int, workspace,
     _check(lib().laminar_linear(_ptr(x), _ptr(w_packed), _ptr(y), int(m), int(n),
                                 int(k), _ptr(workspace), int(workspace_bytes),
                                 _ptr(stream)), "laminar_linear")
+
+
+def laminar_linear_bf16(x, w_packed, y, residual, m: int, n: int, k: int,
+                        workspace, workspace_bytes: int, stream):
+    _check(lib().laminar_linear_bf16(_ptr(x), _ptr(w_packed), _ptr(y),
+                                     _ptr(residual), int(m), int(n), int(k),
+                                     _ptr(workspace), int(workspace_bytes),
+                                     _ptr(stream)), "laminar_linear_bf16")
+
+
+def laminar_rmsnorm(x, weight, y, m: int, n: int, eps: float, stream):
+    _check(lib().laminar_rmsnorm(_ptr(x), _ptr(weight), _ptr(y), int(m), int(n),
+                                 float(eps), _ptr(stream)), "laminar_rmsnorm")
+
+
+def laminar_silu_mul(gu, y, m: int, inter: int, stream):
+    _check(lib().laminar_silu_mul(_ptr(gu), _ptr(y), int(m), int(inter),
+                                  _ptr(stream)), "laminar_silu_mul")
 
 
 def laminar_hbm_read_sink_floats() -> int:

@@ -190,3 +190,31 @@ class SkinnyLinear:
         N.laminar_linear(x, self.w_packed, out, m, self.n, self.k, self.ws,
                          self.ws_bytes, _stream_handle(stream))
         return out
+
+    def bf16(self, x, out=None, residual=None, stream=None):
+        """bf16(x w^T + residual) [M, N]; out may be the residual itself."""
+        m = x.shape[0]
+        if out is None:
+            out = torch.empty((m, self.n), dtype=torch.bfloat16, device=x.device)
+        N.laminar_linear_bf16(x, self.w_packed, out, residual, m, self.n,
+                              self.k, self.ws, self.ws_bytes,
+                              _stream_handle(stream))
+        return out
+
+
+def rmsnorm(x, weight=None, eps: float = 1e-6, out=None, stream=None):
+    """Row-wise RMS norm of bf16 x [M, N] (times weight [N]) -> bf16."""
+    m, n = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    N.laminar_rmsnorm(x, weight, out, m, n, eps, _stream_handle(stream))
+    return out
+
+
+def silu_mul(gu, out=None, stream=None):
+    """silu(gate) * up for bf16 gu [M, 2I] (gate then up) -> bf16 [M, I]."""
+    m, two_i = gu.shape
+    if out is None:
+        out = torch.empty((m, two_i // 2), dtype=gu.dtype, device=gu.device)
+    N.laminar_silu_mul(gu, out, m, two_i // 2, _stream_handle(stream))
+    return out

@@ -1,0 +1,102 @@
+// Element-wise operations of a decode step on MI355X (gfx950): the RMS
+// pre-norm and the SwiGLU activation, one fused kernel each. Both are a few
+// kilobytes per token, so what matters at decode batch sizes is one launch
+// instead of the five or six that the unfused operations take.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "laminar_decode_step.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// One workgroup per row: sum of squares over 16-byte chunks, a workgroup
+// reduction, then a second pass (served by L2) that scales and rounds.
+__global__ void __launch_bounds__(256)
+rmsnorm_kernel(const bf16x8* __restrict__ x, const bf16x8* __restrict__ w,
+               bf16x8* __restrict__ y, int chunks, float inv_n, float eps) {
+  __shared__ float part[4];
+  const bf16x8* xr = x + size_t(blockIdx.x) * chunks;
+  bf16x8* yr = y + size_t(blockIdx.x) * chunks;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < chunks; c += 256) {
+    const bf16x8 v = xr[c];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss = fmaf(float(v[e]), float(v[e]), ss);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float total = (part[0] + part[1]) + (part[2] + part[3]);
+  const float r = 1.0f / sqrtf(total * inv_n + eps);
+  for (int c = threadIdx.x; c < chunks; c += 256) {
+    const bf16x8 v = xr[c];
+    bf16x8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float s = float(v[e]) * r;
+      o[e] = (__bf16)(w ? s * float(w[c][e]) : s);
+    }
+    yr[c] = o;
+  }
+}
+
+// Eight outputs per thread: y[m, i..i+7] from gate gu[m, i..] and up
+// gu[m, I + i..].
+__global__ void __launch_bounds__(256)
+silu_mul_kernel(const bf16x8* __restrict__ gu, bf16x8* __restrict__ y,
+                int rows, int chunks) {
+  const size_t t = size_t(blockIdx.x) * 256 + threadIdx.x;
+  if (t >= size_t(rows) * chunks) return;
+  const size_t m = t / chunks, c = t - m * chunks;
+  const bf16x8 g = gu[m * 2 * chunks + c];
+  const bf16x8 u = gu[m * 2 * chunks + chunks + c];
+  bf16x8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float gf = float(g[e]);
+    o[e] = (__bf16)(gf / (1.0f + expf(-gf)) * float(u[e]));
+  }
+  y[t] = o;
+}
+
+bool misaligned16(const void* p) {
+  return reinterpret_cast<uintptr_t>(p) & 15;
+}
+
+}  // namespace
+
+extern "C" {
+
+laminar_status laminar_rmsnorm(const void* x, const void* weight, void* y,
+                               int32_t m, int32_t n, float eps,
+                               hipStream_t stream) {
+  if (!x || !y || misaligned16(x) || misaligned16(y) || misaligned16(weight))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (m < 1 || n < 8 || n % 8 || !(eps >= 0.f) || !std::isfinite(eps))
+    return LAMINAR_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(unsigned(m)), dim3(256), 0, stream,
+                     static_cast<const bf16x8*>(x),
+                     static_cast<const bf16x8*>(weight),
+                     static_cast<bf16x8*>(y), n / 8, 1.0f / float(n), eps);
+  return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+}
+
+laminar_status laminar_silu_mul(const void* gu, void* y, int32_t m,
+                                int32_t inter, hipStream_t stream) {
+  if (!gu || !y || misaligned16(gu) || misaligned16(y))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (m < 1 || inter < 8 || inter % 8) return LAMINAR_ERR_INVALID_ARG;
+  const size_t total = size_t(m) * (inter / 8);
+  hipLaunchKernelGGL(silu_mul_kernel, dim3(unsigned((total + 255) / 256)),
+                     dim3(256), 0, stream, static_cast<const bf16x8*>(gu),
+                     static_cast<bf16x8*>(y), m, inter / 8);
+  return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+}
+
+}  // extern "C"

@@ -46,11 +46,29 @@ constexpr int kBufFlags = 0x00020000;
 struct LinearArgs {
   const uint16_t* x;     // [M, K]
   const uint16_t* w;     // packed [N/16][K/8][16][8]
-  float* y;              // [M, N]
+  float* y;              // [M, N] fp32 output, or NULL when yb is set
+  uint16_t* yb;          // [M, N] bf16 output (rounded to nearest even)
+  const uint16_t* res;   // [M, N] bf16 residual added before rounding, or NULL
   float* part;           // [splits, M, N] when split
   int32_t m, n, k;
   int32_t n_tiles, splits, steps_per_split;
 };
+
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// Final values of y[m, n .. n+3]: fp32, or bf16 of (value + residual).
+__device__ __forceinline__ void store4(const LinearArgs& a, size_t off, f32x4 v) {
+  if (!a.yb) {
+    *reinterpret_cast<f32x4*>(a.y + off) = v;
+    return;
+  }
+  if (a.res) {
+    const bf16x4 r = *reinterpret_cast<const bf16x4*>(a.res + off);
+    v += f32x4{float(r[0]), float(r[1]), float(r[2]), float(r[3])};
+  }
+  *reinterpret_cast<bf16x4*>(a.yb + off) =
+      bf16x4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+}
 
 // Waits for this wavefront's LDS writes, then for the whole workgroup; the
 // loads in flight are not waited for (a plain __syncthreads would drain
@@ -141,17 +159,20 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
   if (!has_tile) return;
 
   // lane (group q, column r16) holds D[16 tile + 4q + r][m = 16t + r16]
-  float* dst = a.splits > 1 ? a.part + size_t(split) * a.m * a.n : a.y;
 #pragma unroll
   for (int t = 0; t < MT; ++t) {
     const int m = 16 * t + r16;
-    if (m < a.m)
-      *reinterpret_cast<f32x4*>(dst + size_t(m) * a.n + tile * 16 + 4 * q) =
-          acc[t];
+    if (m >= a.m) continue;
+    const size_t off = size_t(m) * a.n + tile * 16 + 4 * q;
+    if (a.splits > 1)
+      *reinterpret_cast<f32x4*>(a.part + size_t(split) * a.m * a.n + off) = acc[t];
+    else
+      store4(a, off, acc[t]);
   }
 }
 
-// y[m, n] = sum over splits s (in order) of part[s, m, n]; four n per thread.
+// y[m, n] = sum over splits s (in order) of part[s, m, n], then the output
+// epilogue; four n per thread.
 __global__ void __launch_bounds__(256) linear_reduce(const LinearArgs a) {
   const size_t i = size_t(blockIdx.x) * 256 + threadIdx.x;    // float4 index
   const size_t total = size_t(a.m) * a.n / 4;
@@ -159,7 +180,7 @@ __global__ void __launch_bounds__(256) linear_reduce(const LinearArgs a) {
   const f32x4* p = reinterpret_cast<const f32x4*>(a.part);
   f32x4 s = p[i];
   for (int k = 1; k < a.splits; ++k) s += p[size_t(k) * total + i];
-  reinterpret_cast<f32x4*>(a.y)[i] = s;
+  store4(a, 4 * i, s);
 }
 
 // w [N, K] -> packed [N/16][K/8][16][8]: one 16-byte chunk per thread,
@@ -199,6 +220,55 @@ bool misaligned16(const void* p) {
 
 }  // namespace
 
+namespace {
+
+laminar_status linear_impl(const void* x, const void* w_packed, float* y,
+                           void* yb, const void* res, int32_t m, int32_t n,
+                           int32_t k, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream) {
+  if (!x || !w_packed || (!y && !yb)) return LAMINAR_ERR_INVALID_ARG;
+  if (misaligned16(x) || misaligned16(w_packed) || misaligned16(y) ||
+      misaligned16(yb) || misaligned16(res))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (!shape_ok(m, n, k)) return LAMINAR_ERR_UNSUPPORTED;
+  LinearArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.w = static_cast<const uint16_t*>(w_packed);
+  a.y = y;
+  a.yb = static_cast<uint16_t*>(yb);
+  a.res = static_cast<const uint16_t*>(res);
+  a.m = m;
+  a.n = n;
+  a.k = k;
+  a.n_tiles = n / 16;
+  split_plan(n, k, &a.splits, &a.steps_per_split);
+  a.part = nullptr;
+  if (a.splits > 1) {
+    const size_t need = laminar_linear_workspace_bytes(m, n, k);
+    if (!workspace || workspace_bytes < need ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255))
+      return LAMINAR_ERR_INVALID_ARG;
+    a.part = static_cast<float*>(workspace);
+  }
+  const dim3 grid((a.n_tiles + 3) / 4, a.splits);
+  const int mt = (m + 15) / 16;
+  switch (mt) {
+    case 1: hipLaunchKernelGGL(linear_kernel<1>, grid, dim3(256), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL(linear_kernel<2>, grid, dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL(linear_kernel<4>, grid, dim3(256), 0, stream, a); break;
+  }
+  if (hipGetLastError() != hipSuccess) return LAMINAR_ERR_HIP;
+  if (a.splits > 1) {
+    const size_t total = size_t(m) * n / 4;
+    hipLaunchKernelGGL(linear_reduce, dim3(unsigned((total + 255) / 256)),
+                       dim3(256), 0, stream, a);
+    if (hipGetLastError() != hipSuccess) return LAMINAR_ERR_HIP;
+  }
+  return LAMINAR_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 laminar_status laminar_linear_pack(const void* w, void* w_packed, int32_t n,
@@ -228,42 +298,18 @@ size_t laminar_linear_workspace_bytes(int32_t m, int32_t n, int32_t k) {
 laminar_status laminar_linear(const void* x, const void* w_packed, float* y,
                               int32_t m, int32_t n, int32_t k, void* workspace,
                               size_t workspace_bytes, hipStream_t stream) {
-  if (!x || !w_packed || !y) return LAMINAR_ERR_INVALID_ARG;
-  if (misaligned16(x) || misaligned16(w_packed) || misaligned16(y))
-    return LAMINAR_ERR_INVALID_ARG;
-  if (!shape_ok(m, n, k)) return LAMINAR_ERR_UNSUPPORTED;
-  LinearArgs a;
-  a.x = static_cast<const uint16_t*>(x);
-  a.w = static_cast<const uint16_t*>(w_packed);
-  a.y = y;
-  a.m = m;
-  a.n = n;
-  a.k = k;
-  a.n_tiles = n / 16;
-  split_plan(n, k, &a.splits, &a.steps_per_split);
-  a.part = nullptr;
-  if (a.splits > 1) {
-    const size_t need = laminar_linear_workspace_bytes(m, n, k);
-    if (!workspace || workspace_bytes < need ||
-        (reinterpret_cast<uintptr_t>(workspace) & 255))
-      return LAMINAR_ERR_INVALID_ARG;
-    a.part = static_cast<float*>(workspace);
-  }
-  const dim3 grid((a.n_tiles + 3) / 4, a.splits);
-  const int mt = (m + 15) / 16;
-  switch (mt) {
-    case 1: hipLaunchKernelGGL(linear_kernel<1>, grid, dim3(256), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL(linear_kernel<2>, grid, dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL(linear_kernel<4>, grid, dim3(256), 0, stream, a); break;
-  }
-  if (hipGetLastError() != hipSuccess) return LAMINAR_ERR_HIP;
-  if (a.splits > 1) {
-    const size_t total = size_t(m) * n / 4;
-    hipLaunchKernelGGL(linear_reduce, dim3(unsigned((total + 255) / 256)),
-                       dim3(256), 0, stream, a);
-    if (hipGetLastError() != hipSuccess) return LAMINAR_ERR_HIP;
-  }
-  return LAMINAR_OK;
+  if (!y) return LAMINAR_ERR_INVALID_ARG;
+  return linear_impl(x, w_packed, y, nullptr, nullptr, m, n, k, workspace,
+                     workspace_bytes, stream);
+}
+
+laminar_status laminar_linear_bf16(const void* x, const void* w_packed,
+                                   void* y, const void* residual, int32_t m,
+                                   int32_t n, int32_t k, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
+  if (!y) return LAMINAR_ERR_INVALID_ARG;
+  return linear_impl(x, w_packed, nullptr, y, residual, m, n, k, workspace,
+                     workspace_bytes, stream);
 }
 
 }  // extern "C"

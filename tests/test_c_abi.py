@@ -430,6 +430,13 @@ def test_linear_errors_before_any_launch():
     assert lib.laminar_linear(16, 16, 16, 1, 16, 100, None, 0, None) == UNS
     assert lib.laminar_linear(16, 16, 16, 1, 16, (1 << 24) + 128, None, 0,
                               None) == UNS
+    # bf16 output: NULL output, misaligned residual, shapes
+    assert lib.laminar_linear_bf16(16, 16, None, None, 1, 16, 128, None, 0,
+                                   None) == INV
+    assert lib.laminar_linear_bf16(16, 16, 16, 24, 1, 16, 128, None, 0,
+                                   None) == INV
+    assert lib.laminar_linear_bf16(16, 16, 16, None, 65, 16, 128, None, 0,
+                                   None) == UNS
     # packing: NULL, in place, misaligned, shapes
     assert lib.laminar_linear_pack(None, 16, 16, 128, None) == INV
     assert lib.laminar_linear_pack(16, 16, 16, 128, None) == INV
@@ -512,6 +519,23 @@ def test_attention_kernels_do_not_spill_in_the_page_loop():
         if line.strip() == "s_endpgm":
             fn = None
     assert not bad, bad[:4]
+
+
+def test_decode_step_errors_before_any_launch():
+    lib = N.lib()
+    INV = N.LAMINAR_ERR_INVALID_ARG
+    f = ctypes.c_float
+    assert lib.laminar_rmsnorm(None, None, 16, 1, 64, f(1e-6), None) == INV
+    assert lib.laminar_rmsnorm(16, None, 24, 1, 64, f(1e-6), None) == INV
+    assert lib.laminar_rmsnorm(16, 8, 32, 1, 64, f(1e-6), None) == INV
+    assert lib.laminar_rmsnorm(16, None, 32, 1, 60, f(1e-6), None) == INV
+    assert lib.laminar_rmsnorm(16, None, 32, 0, 64, f(1e-6), None) == INV
+    assert lib.laminar_rmsnorm(16, None, 32, 1, 64, f(-1.0), None) == INV
+    assert lib.laminar_rmsnorm(16, None, 32, 1, 64, f(float("nan")), None) == INV
+    assert lib.laminar_silu_mul(None, 16, 1, 64, None) == INV
+    assert lib.laminar_silu_mul(16, 40, 1, 64, None) == INV
+    assert lib.laminar_silu_mul(16, 32, 1, 12, None) == INV
+    assert lib.laminar_silu_mul(16, 32, 0, 64, None) == INV
 
 
 def test_linear_kernels_use_no_scratch():

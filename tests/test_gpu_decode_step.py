@@ -1,0 +1,109 @@
+"""GPU parity of the decode step's element-wise kernels and of the bf16
+projection epilogue against the fp64 oracle.
+
+Bar: every bf16 output within one bf16 unit in the last place of the fp64
+value (the kernels round an fp32 result once; fp32 error can move that
+rounding by one step), plus, for the projection, the fp32 accumulation
+bound 4 (K/32 + 32) 2^-24 sum_k |x w| of the fp32 kernel."""
+import numpy as np
+import pytest
+import torch
+
+from oracle.decoder import rmsnorm as rmsnorm_ref, silu_mul as silu_mul_ref
+from oracle.linear import bf16_to_f64, linear, linear_abs
+
+pytestmark = pytest.mark.gpu
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+
+
+def bits(t):
+    return t.detach().cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def ulp_bound(ref):
+    """One bf16 step at the magnitude of ref (8 significant bits)."""
+    a = np.abs(ref)
+    e = np.floor(np.log2(np.maximum(a, 2.0 ** -126)))
+    return 2.0 ** (e - 7)
+
+
+def rand_bf16(g, shape, scale=1.0):
+    return (torch.randn(shape, generator=g, device="cuda") * scale).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("m,n,weighted", [(1, 3584, True), (7, 5120, False),
+                                          (64, 18944, True), (3, 8, True)])
+def test_rmsnorm_matches_oracle(m, n, weighted):
+    from paper_2510_12633_amd.api import rmsnorm
+    _need_gpu()
+    g = torch.Generator(device="cuda").manual_seed(m + n)
+    x = rand_bf16(g, (m, n), 3.0)
+    w = rand_bf16(g, (n,)) if weighted else None
+    y = rmsnorm(x, w, eps=1e-6)
+    torch.cuda.synchronize()
+    ref = rmsnorm_ref(bits(x), bits(w) if weighted else None, eps=1e-6)
+    err = np.abs(bf16_to_f64(bits(y)) - ref)
+    print(f"[gpu-step] rmsnorm m={m} n={n}: max err/ulp "
+          f"{(err / ulp_bound(ref)).max():.3f}", flush=True)
+    assert np.all(err <= ulp_bound(ref))
+
+
+@pytest.mark.parametrize("m,inter", [(1, 18944), (16, 27648), (64, 8)])
+def test_silu_mul_matches_oracle(m, inter):
+    from paper_2510_12633_amd.api import silu_mul
+    _need_gpu()
+    g = torch.Generator(device="cuda").manual_seed(m * 7 + inter)
+    gu = rand_bf16(g, (m, 2 * inter), 4.0)
+    y = silu_mul(gu)
+    torch.cuda.synchronize()
+    ref = silu_mul_ref(bits(gu))
+    err = np.abs(bf16_to_f64(bits(y)) - ref)
+    print(f"[gpu-step] silu_mul m={m} I={inter}: max err/ulp "
+          f"{(err / ulp_bound(ref)).max():.3f}", flush=True)
+    assert np.all(err <= ulp_bound(ref) + 2.0 ** -133)
+
+
+@pytest.mark.parametrize("m,n,k,in_place", [(1, 3584, 3584, False),
+                                            (16, 3584, 18944, True),
+                                            (33, 4608, 3584, False),
+                                            (5, 96, 640, True)])
+def test_linear_bf16_with_residual(m, n, k, in_place):
+    from paper_2510_12633_amd.api import SkinnyLinear
+    _need_gpu()
+    g = torch.Generator(device="cuda").manual_seed(m + n + k)
+    x = rand_bf16(g, (m, k))
+    w = rand_bf16(g, (n, k), k ** -0.5)
+    res = rand_bf16(g, (m, n))
+    res_bits = bits(res)
+    lin = SkinnyLinear(w)
+    y = lin.bf16(x, out=res if in_place else None, residual=res)
+    y_plain = lin.bf16(x)
+    torch.cuda.synchronize()
+    xb, wb = bits(x), bits(w)
+    acc = 4 * (k / 32 + 32) * 2.0 ** -24 * linear_abs(xb, wb)
+    for got, r in ((y, bf16_to_f64(res_bits)), (y_plain, 0.0)):
+        ref = linear(xb, wb) + r
+        err = np.abs(bf16_to_f64(bits(got)) - ref)
+        print(f"[gpu-step] linear_bf16 m={m} n={n} k={k}: max err/bound "
+              f"{(err / (acc + ulp_bound(ref))).max():.3f}", flush=True)
+        assert np.all(err <= acc + ulp_bound(ref))
+
+
+def test_decode_step_argument_errors():
+    from paper_2510_12633_amd import _native as N
+    _need_gpu()
+    s = torch.cuda.current_stream().cuda_stream
+    x = torch.zeros((4, 64), dtype=torch.bfloat16, device="cuda")
+    y = torch.empty_like(x)
+    for args in ((x, None, y, 4, 60, 1e-6), (x, None, y, 0, 64, 1e-6),
+                 (x, None, y, 4, 64, -1.0), (x, None, None, 4, 64, 1e-6)):
+        with pytest.raises(N.LaminarError) as e:
+            N.laminar_rmsnorm(*args, s)
+        assert e.value.status == N.LAMINAR_ERR_INVALID_ARG
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_silu_mul(x, y, 4, 12, s)
+    assert e.value.status == N.LAMINAR_ERR_INVALID_ARG
