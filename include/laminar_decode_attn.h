@@ -30,7 +30,8 @@
  *
  * Memory layouts (all row-major, contiguous, element = 2 bytes for bf16 and
  * 1 byte for fp8):
- *   q            [batch, num_q_heads, head_dim]         bf16
+ *   q            [batch, num_q_heads, head_dim]         bf16 (rows
+ *                input_row_stride elements apart when that is set)
  *   k_pages      [num_pages, num_kv_heads, 16*head_dim] bf16 or fp8 e4m3fn
  *   v_pages      [num_pages, num_kv_heads, 16*head_dim] bf16 or fp8 e4m3fn
  *   block_table  [batch, max_blocks_per_seq]            int32
@@ -90,6 +91,12 @@ typedef struct {
                                   per work item (1 .. no split)              */
   int32_t waves_per_item;      /* 0: automatic (4); else 1, 2 or 4 wavefronts
                                   cooperate on one work item                 */
+  int32_t input_row_stride;    /* elements from one trajectory's row of the
+                                  per-token inputs to the next: q for decode
+                                  attention, k_new and v_new for KV append.
+                                  0: contiguous (heads x head_dim); else at
+                                  least that and a multiple of 8, e.g. the
+                                  row of a fused QKV projection's output     */
 } laminar_attn_desc;
 
 typedef struct laminar_plan laminar_plan;   /* opaque, host-owned */
@@ -104,7 +111,8 @@ typedef struct laminar_plan laminar_plan;   /* opaque, host-owned */
  * The plan is reusable by every layer of the step. On success *out owns a
  * new plan (free with laminar_plan_destroy); on error *out is NULL.
  * Errors: INVALID_ARG (NULL pointers, negative or inconsistent sizes, a
- * length needing more than max_blocks_per_seq pages, fp8 without scales),
+ * length needing more than max_blocks_per_seq pages, fp8 without scales,
+ * an input_row_stride below num_q_heads x head_dim or not a multiple of 8),
  * UNSUPPORTED (head_dim not 64/128, group size above 16, page_size != 16).
  */
 laminar_status laminar_plan_create(const laminar_attn_desc* desc,

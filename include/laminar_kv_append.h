@@ -30,10 +30,13 @@
  *
  * Arguments (device pointers unless stated):
  *   desc         host; uses batch, num_kv_heads, head_dim (64 or 128),
- *                page_size (16), num_pages, max_blocks_per_seq, kv_dtype.
- *                Its k_scale / v_scale fields are ignored: the writable
- *                scale arrays are passed below.
- *   k_new, v_new [batch, num_kv_heads, head_dim] bf16, 16-byte aligned.
+ *                page_size (16), num_pages, max_blocks_per_seq, kv_dtype,
+ *                input_row_stride. Its k_scale / v_scale fields are
+ *                ignored: the writable scale arrays are passed below.
+ *   k_new, v_new [batch, num_kv_heads, head_dim] bf16, 16-byte aligned;
+ *                trajectory b's row starts input_row_stride elements after
+ *                trajectory b-1's (0: num_kv_heads x head_dim, contiguous),
+ *                so both may point into a fused QKV projection's output.
  *   block_table  [batch, max_blocks_per_seq] int32.
  *   seq_lens     [batch] int32, lengths after this append.
  *   k_pages, v_pages  the pools, updated in place.
@@ -45,7 +48,8 @@
  * trajectories must be copied before it is written. The append must be
  * ordered before the attention call that reads the token (same stream).
  * Errors: INVALID_ARG (NULL pointers when batch > 0, bad sizes, missing fp8
- * scales, misaligned k_new / v_new), UNSUPPORTED (page_size != 16, head_dim
+ * scales, misaligned k_new / v_new, an input_row_stride below
+ * num_kv_heads x head_dim or not a multiple of 8), UNSUPPORTED (page_size != 16, head_dim
  * not 64 or 128), HIP (launch failure).
  */
 #ifndef LAMINAR_KV_APPEND_H

@@ -41,6 +41,7 @@ class LaminarAttnDesc(ctypes.Structure):
         ("v_scale", c_void_p),
         ("pages_per_item", c_int32),
         ("waves_per_item", c_int32),
+        ("input_row_stride", c_int32),
     ]
 
 

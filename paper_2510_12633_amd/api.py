@@ -43,7 +43,7 @@ class PagedDecodeAttention:
                  v_scale: Optional[torch.Tensor] = None,
                  pages_per_item: int = 0, waves_per_item: int = 0,
                  cus: Optional[int] = None, device="cuda", stream=None,
-                 group_of=None, group_pages=None):
+                 group_of=None, group_pages=None, q_row_stride: int = 0):
         self.desc = N.LaminarAttnDesc(
             batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
             head_dim=head_dim, page_size=16, num_pages=num_pages,
@@ -51,8 +51,10 @@ class PagedDecodeAttention:
             kv_dtype=KV_DTYPES[kv_dtype], softmax_scale=softmax_scale,
             k_scale=None if k_scale is None else k_scale.data_ptr(),
             v_scale=None if v_scale is None else v_scale.data_ptr(),
-            pages_per_item=pages_per_item, waves_per_item=waves_per_item)
+            pages_per_item=pages_per_item, waves_per_item=waves_per_item,
+            input_row_stride=q_row_stride)
         self.device = torch.device(device)
+        self.q_strides = (q_row_stride or num_q_heads * head_dim, head_dim, 1)
         self._scales = (k_scale, v_scale)        # keep alive
         if cus is None:
             cus = num_cus(self.device) if self.device.type == "cuda" else 256
@@ -89,12 +91,19 @@ class PagedDecodeAttention:
                  lse=None, stream=None):
         if out is None or lse is None:
             out, lse = self.outputs()
+        self._check_q(q)
         N.laminar_decode_attn(self.plan, q, k_pages, v_pages, block_table,
                               seq_lens, out, lse, _stream_handle(stream))
         return out, lse
 
+    def _check_q(self, q):
+        if q.shape[0] > 1 and tuple(q.stride()) != self.q_strides:
+            raise ValueError(f"q strides {tuple(q.stride())} differ from the "
+                             f"plan's {self.q_strides}")
+
     def partial(self, q, k_pages, v_pages, block_table, seq_lens, out, lse,
                 stream=None):
+        self._check_q(q)
         N.laminar_decode_attn_partial(self.plan, q, k_pages, v_pages,
                                       block_table, seq_lens, out, lse,
                                       _stream_handle(stream))
@@ -146,11 +155,18 @@ def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages,
     """Append the current token's K/V ([B, Hkv, D] bf16) to the paged pools
     in place (pools [P, Hkv, 16*D]; fp8 scales [P, Hkv] updated too)."""
     b, hkv, d = k_new.shape
+    # rows may be strided (views into a fused QKV output); heads and dims not
+    if (k_new.stride()[1:] != (d, 1) or v_new.stride()[1:] != (d, 1)
+            or k_new.stride(0) != v_new.stride(0)):
+        raise ValueError("k_new and v_new need contiguous [heads, dim] rows "
+                         "and one row stride")
+    row = k_new.stride(0)
     desc = N.LaminarAttnDesc(
         batch=b, num_q_heads=hkv, num_kv_heads=hkv, head_dim=d, page_size=16,
         num_pages=k_pages.shape[0], max_blocks_per_seq=block_table.shape[1],
         kv_dtype=KV_DTYPES[kv_dtype], softmax_scale=1.0, k_scale=None,
-        v_scale=None, pages_per_item=0, waves_per_item=0)
+        v_scale=None, pages_per_item=0, waves_per_item=0,
+        input_row_stride=0 if row == hkv * d else row)
     N.laminar_kv_append(desc, k_new, v_new, block_table, seq_lens, k_pages,
                         v_pages, k_scale, v_scale, _stream_handle(stream))
 

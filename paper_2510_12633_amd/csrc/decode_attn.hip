@@ -55,6 +55,7 @@ constexpr double kLn2d = 0.6931471805599453;
 
 struct DecodeArgs {
   const uint16_t* q;
+  int64_t q_stride;       // elements between trajectories' query rows
   const uint8_t* k_pages;
   const uint8_t* v_pages;
   const float* k_scale;
@@ -231,7 +232,8 @@ __device__ __forceinline__ void load_q(const DecodeArgs& a, int b, int h,
                                        bf16x8 (&qf)[Geo<D, FP8>::KK]) {
   using G = Geo<D, FP8>;
   const u32x4* qp = reinterpret_cast<const u32x4*>(
-      a.q + (size_t(ok ? b : 0) * a.hq + (ok ? h : 0)) * D) + gq * G::KK;
+      a.q + size_t(ok ? b : 0) * a.q_stride + size_t(ok ? h : 0) * D) +
+      gq * G::KK;
 #pragma unroll
   for (int kk = 0; kk < G::KK; ++kk) {
     const u32x4 v = ok ? qp[kk] : u4(0, 0, 0, 0);
@@ -836,6 +838,8 @@ DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
   const laminar_attn_desc& d = p->desc;
   char* ws = static_cast<char*>(p->ws);
   a.q = static_cast<const uint16_t*>(q);
+  a.q_stride = d.input_row_stride ? d.input_row_stride
+                                  : int64_t(d.num_q_heads) * d.head_dim;
   a.k_pages = static_cast<const uint8_t*>(k_pages);
   a.v_pages = static_cast<const uint8_t*>(v_pages);
   a.k_scale = d.k_scale;

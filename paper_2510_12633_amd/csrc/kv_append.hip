@@ -28,6 +28,7 @@ constexpr float kFp8Max = 448.0f;
 struct AppendArgs {
   const uint16_t* k_new;
   const uint16_t* v_new;
+  int64_t row_stride;     // elements between trajectories' rows of k_new/v_new
   const int32_t* block_table;
   const int32_t* seq_lens;
   uint8_t* k_pages;
@@ -100,7 +101,8 @@ __global__ void __launch_bounds__(128) kv_append_kernel(const AppendArgs a) {
   const int kvh = unit - b * a.hkv;
   const bool is_v = (threadIdx.x >> 6) != 0;        // wave-uniform
   const int lane = threadIdx.x & 63;
-  const uint16_t* src = (is_v ? a.v_new : a.k_new) + size_t(unit) * D;
+  const uint16_t* src =
+      (is_v ? a.v_new : a.k_new) + size_t(b) * a.row_stride + size_t(kvh) * D;
   // The new values do not depend on the table: load them first.
   constexpr int PER = D / 64;
   uint32_t xb[PER];
@@ -266,7 +268,14 @@ extern "C" laminar_status laminar_kv_append(
        reinterpret_cast<uintptr_t>(v_pages)) & 15)
     return LAMINAR_ERR_INVALID_ARG;
   if (fp8 && (!k_scale || !v_scale)) return LAMINAR_ERR_INVALID_ARG;
+  if (d->input_row_stride != 0 &&
+      (int64_t(d->input_row_stride) < int64_t(d->num_kv_heads) * d->head_dim ||
+       d->input_row_stride % 8 != 0))
+    return LAMINAR_ERR_INVALID_ARG;
   AppendArgs a;
+  a.row_stride = d->input_row_stride
+                     ? d->input_row_stride
+                     : int64_t(d->num_kv_heads) * d->head_dim;
   a.k_new = static_cast<const uint16_t*>(k_new);
   a.v_new = static_cast<const uint16_t*>(v_new);
   a.block_table = block_table;

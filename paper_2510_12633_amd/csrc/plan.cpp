@@ -31,6 +31,10 @@ laminar_status validate(const laminar_attn_desc* d, const int32_t* lens,
   if (d->num_q_heads % d->num_kv_heads != 0) return LAMINAR_ERR_INVALID_ARG;
   if (!(d->softmax_scale > 0.0f)) return LAMINAR_ERR_INVALID_ARG;
   if (d->pages_per_item < 0) return LAMINAR_ERR_INVALID_ARG;
+  if (d->input_row_stride != 0 &&
+      (int64_t(d->input_row_stride) < int64_t(d->num_q_heads) * d->head_dim ||
+       d->input_row_stride % 8 != 0))
+    return LAMINAR_ERR_INVALID_ARG;
   if (d->waves_per_item != 0 && d->waves_per_item != 1 &&
       d->waves_per_item != 2 && d->waves_per_item != 4)
     return LAMINAR_ERR_INVALID_ARG;

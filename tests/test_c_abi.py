@@ -27,13 +27,13 @@ def declared_functions():
 
 def desc(batch=4, hq=28, hkv=4, d=128, pages=10**6, max_blocks=8192,
          kv=N.LAMINAR_KV_BF16, scale=0.1, ppi=0, waves=0, k_scale=None,
-         v_scale=None, page_size=16):
+         v_scale=None, page_size=16, stride=0):
     return N.LaminarAttnDesc(batch=batch, num_q_heads=hq, num_kv_heads=hkv,
                              head_dim=d, page_size=page_size, num_pages=pages,
                              max_blocks_per_seq=max_blocks, kv_dtype=kv,
                              softmax_scale=scale, k_scale=k_scale,
                              v_scale=v_scale, pages_per_item=ppi,
-                             waves_per_item=waves)
+                             waves_per_item=waves, input_row_stride=stride)
 
 
 def plan_tables(d, lens, cus=256):
@@ -167,6 +167,19 @@ def test_dynamic_tail_is_the_small_end_of_the_list():
         assert N.lib().laminar_plan_num_dynamic_items(p) == 0
     finally:
         N.laminar_plan_destroy(p)
+
+
+def test_plan_input_row_stride_checked():
+    lens = np.array([5, 17, 300, 0], np.int32)
+    for stride, ok in ((0, True), (28 * 128, True), (36 * 128, True),
+                       (28 * 128 - 8, False), (36 * 128 + 4, False)):
+        try:
+            N.laminar_plan_destroy(N.laminar_plan_create(desc(stride=stride),
+                                                         lens, 256))
+            st = N.LAMINAR_OK
+        except N.LaminarError as e:
+            st = e.status
+        assert st == (N.LAMINAR_OK if ok else N.LAMINAR_ERR_INVALID_ARG), stride
 
 
 def test_planner_edge_lengths():
@@ -408,6 +421,8 @@ def test_kv_append_errors_before_any_launch():
     assert call(desc(pages=0)) == INV
     assert call(desc(max_blocks=-1)) == INV
     assert call(desc(kv=7)) == INV
+    assert call(desc(stride=4 * 128 - 8)) == INV          # below Hkv x D
+    assert call(desc(stride=4 * 128 + 4)) == INV          # not 16-byte rows
     assert call(desc(page_size=32)) == UNS
     assert call(desc(d=96)) == UNS
     assert call(desc(), k_new=None) == INV

@@ -224,3 +224,40 @@ def test_append_argument_errors_on_gpu():
     N.laminar_kv_append(d, run.k_new[0], run.v_new[0], bt, lens, run.k_pages,
                         run.v_pages, run.k_scale, run.v_scale, None)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("name,cfg", CASES, ids=[c[0] for c in CASES])
+def test_strided_rows_equal_contiguous(name, cfg):
+    """k_new and v_new read as views into a fused QKV projection's output
+    (rows input_row_stride elements apart) give bit-identical pools and
+    scales to the contiguous call."""
+    from paper_2510_12633_amd.api import kv_append as gpu_kv_append
+    _need_gpu()
+    wl = make_workload(cfg, seed=5, device="cuda")
+    run = make_decode_run(wl, steps=3)
+    c = wl.cfg
+    hq, hkv, d = c.num_q_heads, c.num_kv_heads, c.head_dim
+    bt = torch.as_tensor(run.block_table, device="cuda")
+
+    def state():
+        return [t.clone() if t is not None else None
+                for t in (run.k_pages, run.v_pages, run.k_scale, run.v_scale)]
+
+    plain, strided = state(), state()
+    for step in range(run.steps):
+        lens = torch.as_tensor(run.lens_after(step), device="cuda")
+        b = run.k_new[step].shape[0]
+        qkv = torch.full((b, (hq + 2 * hkv) * d), float("nan"),
+                         dtype=torch.bfloat16, device="cuda")
+        qkv[:, hq * d:(hq + hkv) * d] = run.k_new[step].reshape(b, hkv * d)
+        qkv[:, (hq + hkv) * d:] = run.v_new[step].reshape(b, hkv * d)
+        k_view = qkv[:, hq * d:(hq + hkv) * d].view(b, hkv, d)
+        v_view = qkv[:, (hq + hkv) * d:].view(b, hkv, d)
+        assert k_view.stride(0) == (hq + 2 * hkv) * d
+        gpu_kv_append(run.k_new[step], run.v_new[step], bt, lens, *plain,
+                      kv_dtype=c.kv_dtype)
+        gpu_kv_append(k_view, v_view, bt, lens, *strided, kv_dtype=c.kv_dtype)
+    torch.cuda.synchronize()
+    for got, want, what in zip(strided, plain, ("K", "V", "K scale", "V scale")):
+        if want is not None:
+            assert_same(host(got), host(want), f"{name} strided {what}")

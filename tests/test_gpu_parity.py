@@ -179,6 +179,40 @@ def test_dynamic_tail_repeated_launches_bitwise():
     att.close()
 
 
+@pytest.mark.parametrize("cascade", [False, True])
+def test_strided_q_equals_contiguous(cascade):
+    """q read as a view into a fused QKV projection's output (rows
+    (Hq + 2 Hkv) D elements apart) gives bit-identical out and lse."""
+    from paper_2510_12633_amd.api import PagedDecodeAttention
+    _need_gpu()
+    name, cfg = CASCADE[1] if cascade else CUSTOM[0]
+    wl = make_workload(cfg, seed=11, device="cuda")
+    c = wl.cfg
+    hq, hkv, d = c.num_q_heads, c.num_kv_heads, c.head_dim
+    row = (hq + 2 * hkv) * d
+    qkv = torch.full((wl.batch, row), float("nan"), dtype=torch.bfloat16,
+                     device="cuda")
+    qkv[:, :hq * d] = wl.q.reshape(wl.batch, hq * d)
+    q_view = qkv[:, :hq * d].view(wl.batch, hq, d)
+    bt = torch.as_tensor(wl.block_table, device="cuda")
+    lens = torch.as_tensor(wl.seq_lens, device="cuda")
+    res = []
+    for q, stride in ((wl.q, 0), (q_view, row)):
+        att = PagedDecodeAttention(
+            batch=wl.batch, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+            num_pages=wl.num_pages, max_blocks_per_seq=wl.block_table.shape[1],
+            seq_lens_host=wl.seq_lens, softmax_scale=wl.softmax_scale,
+            q_row_stride=stride,
+            **(dict(zip(("group_of", "group_pages"), prefix_groups(wl)))
+               if cascade else {}))
+        out, lse = att(q, wl.k_pages, wl.v_pages, bt, lens)
+        torch.cuda.synchronize()
+        res.append((out.cpu().numpy(), lse.cpu().numpy()))
+        att.close()
+    assert np.array_equal(res[0][0], res[1][0]), name
+    assert np.array_equal(res[0][1], res[1][1]), name
+
+
 def test_tiny_config_all_outputs():
     _need_gpu()
     wl = make_workload(1, device="cuda")
