@@ -213,6 +213,27 @@ def test_strided_q_equals_contiguous(cascade):
     assert np.array_equal(res[0][1], res[1][1]), name
 
 
+def test_empty_batches():
+    """batch 0 is a no-op; a batch whose trajectories are all empty gives
+    out = 0 and lse = -inf (the merge identity) for every head."""
+    from paper_2510_12633_amd import _native as N
+    from paper_2510_12633_amd.api import PagedDecodeAttention
+    _need_gpu()
+    att = PagedDecodeAttention(
+        batch=0, num_q_heads=8, num_kv_heads=2, head_dim=128, num_pages=1,
+        max_blocks_per_seq=1, seq_lens_host=np.zeros(0, np.int32),
+        softmax_scale=0.1)
+    assert att.num_items == 0
+    N.laminar_decode_attn(att.plan, None, None, None, None, None, None, None,
+                          torch.cuda.current_stream().cuda_stream)
+    att.close()
+    wl = make_workload(custom_config([0, 0, 0], 16, 2, 64), device="cuda")
+    o, l = run_gpu(wl)
+    assert np.array_equal(o, np.zeros_like(o)) and np.isneginf(l).all()
+    o, l = run_gpu(wl, pages_per_item=1, waves_per_item=1)
+    assert np.array_equal(o, np.zeros_like(o)) and np.isneginf(l).all()
+
+
 def test_tiny_config_all_outputs():
     _need_gpu()
     wl = make_workload(1, device="cuda")
