@@ -329,7 +329,7 @@ QWEN7B_PROJECTIONS = {"qkv": (4608, 3584), "o": (3584, 3584),
                       "lm_head": (152064, 3584)}
 
 
-def measure_projections(torch, N, batches=(1, 16, 64), reps=20):
+def measure_projections(torch, N, batches=(1, 16, 64, 128), reps=20):
     """The skinny projection kernel on Qwen2.5-7B's projection shapes (w
     [N, K] bf16, packed once), HIP-event time per call and weight bytes /
     time, next to the library GEMM (torch.matmul) on the same operands.
@@ -392,7 +392,7 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     O and down ones adding the residual stream), its KV append, paged
     attention and SwiGLU; then the LM head) captured in a HIP graph and
     timed at each batch size. Each projection kind runs the faster of this library's
-    skinny kernel (batches up to 64) and the library GEMM, timed first at
+    skinny kernel (batches up to 128) and the library GEMM, timed first at
     that batch; next to the roofline model's step
     time and batch bound. Every replay is checked bit for bit against the
     eager step. Every trajectory holds `context` cached tokens; one KV pool
@@ -449,7 +449,7 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                             dtype=bf)
             times = {}
             for use in (False, True):
-                if use and m > 64:
+                if use and m > 128:
                     continue
                 for p in projs:
                     p.use_skinny = use

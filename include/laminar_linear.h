@@ -27,7 +27,7 @@
  * (same size as w). The 16 rows x 32 k that one matrix-core step consumes
  * are then 1 KB of contiguous bytes, which one wavefront load reads whole.
  *
- * Limits: 1 <= M <= 64, N a multiple of 16, K a multiple of 128 and at most
+ * Limits: 1 <= M <= 128, N a multiple of 16, K a multiple of 128 and at most
  * 2^24; larger batches are compute-bound and belong to a general GEMM.
  * Workspace: laminar_linear_workspace_bytes(M, N, K) bytes of device
  * memory (0 when no K split is used), 256-byte aligned, owned by the

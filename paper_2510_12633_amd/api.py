@@ -185,11 +185,11 @@ def migrate(src_pools, dst_pools, pairs, stream=None):
 
 
 class SkinnyLinear:
-    """y = x w^T for decode batches (M <= 64): w [N, K] bf16 on the device is
+    """y = x w^T for decode batches (M <= 128): w [N, K] bf16 on the device is
     packed once into the kernel's tiled layout (a copy of the same size);
     owns that copy and the K-split workspace for up to max_m rows."""
 
-    def __init__(self, weight, max_m: int = 64, stream=None):
+    def __init__(self, weight, max_m: int = 128, stream=None):
         self.n, self.k = weight.shape
         self.w_packed = torch.empty_like(weight)
         N.laminar_linear_pack(weight, self.w_packed, self.n, self.k,

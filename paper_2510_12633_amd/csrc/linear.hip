@@ -1,4 +1,4 @@
-// Skinny projection product y = x w^T for decode batches (M <= 64) on
+// Skinny projection product y = x w^T for decode batches (M <= 128) on
 // MI355X (gfx950).
 //
 // At decode batch sizes the product streams the whole weight matrix w
@@ -15,8 +15,8 @@
 // the workgroup loads the batch's x [16 MT rows, 128 k] once and stages it
 // in LDS, from where every wavefront reads its B operand; so x is fetched
 // once per four tiles instead of once per tile (at M = 64 it would
-// otherwise be four times the weight traffic). NB steps of loads are in
-// flight. All loads are buffer loads whose range check returns zeros: rows
+// otherwise be four times the weight traffic). Four steps of loads are in
+// flight (two for 65-128 rows, whose x tiles take more registers). All loads are buffer loads whose range check returns zeros: rows
 // of x past M, the steps that pad the last group of NB, and a wavefront
 // past the last tile read zeros without touching memory, so no load is
 // conditional and the compiler keeps exact counts of the loads in flight.
@@ -36,10 +36,11 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kStepK = 128;          // k values per pipeline step
-constexpr int kMaxM = 64;
+constexpr int kMaxM = 128;
 constexpr int kMaxK = 1 << 24;       // keeps every buffer offset in 31 bits
 constexpr int kTargetWaves = 2048;   // 2 per SIMD: ~32 MB of weights in flight
-constexpr int kNB = 4;               // steps in flight
+// steps in flight: 4, or 2 for 128 batch rows (registers)
+template <int MT> constexpr int steps_in_flight() { return MT <= 4 ? 4 : 2; }
 constexpr int kOob = 0x40000000;     // past every buffer: reads as zero
 constexpr int kBufFlags = 0x00020000;
 
@@ -108,6 +109,7 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
   // lane (q, r16) of matrix-core step j holds row r16, k chunk 4 j + q
   const int w_lane = (q * 16 + r16) * 16;
 
+  constexpr int kNB = steps_in_flight<MT>();
   u32x4 wb[kNB][4];
   u32x4 xb[kNB][MT];
   auto load = [&](int s, int i) {
@@ -255,7 +257,9 @@ laminar_status linear_impl(const void* x, const void* w_packed, float* y,
   switch (mt) {
     case 1: hipLaunchKernelGGL(linear_kernel<1>, grid, dim3(256), 0, stream, a); break;
     case 2: hipLaunchKernelGGL(linear_kernel<2>, grid, dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL(linear_kernel<4>, grid, dim3(256), 0, stream, a); break;
+    case 3:
+    case 4: hipLaunchKernelGGL(linear_kernel<4>, grid, dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL(linear_kernel<8>, grid, dim3(256), 0, stream, a); break;
   }
   if (hipGetLastError() != hipSuccess) return LAMINAR_ERR_HIP;
   if (a.splits > 1) {

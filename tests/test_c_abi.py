@@ -440,7 +440,7 @@ def test_linear_errors_before_any_launch():
     assert lib.laminar_linear(None, 16, 16, 1, 16, 128, None, 0, None) == INV
     assert lib.laminar_linear(16, 24, 16, 1, 16, 128, None, 0, None) == INV
     assert lib.laminar_linear(16, 16, 16, 0, 16, 128, None, 0, None) == UNS
-    assert lib.laminar_linear(16, 16, 16, 65, 16, 128, None, 0, None) == UNS
+    assert lib.laminar_linear(16, 16, 16, 129, 16, 128, None, 0, None) == UNS
     assert lib.laminar_linear(16, 16, 16, 1, 24, 128, None, 0, None) == UNS
     assert lib.laminar_linear(16, 16, 16, 1, 16, 100, None, 0, None) == UNS
     assert lib.laminar_linear(16, 16, 16, 1, 16, (1 << 24) + 128, None, 0,
@@ -450,7 +450,7 @@ def test_linear_errors_before_any_launch():
                                    None) == INV
     assert lib.laminar_linear_bf16(16, 16, 16, 24, 1, 16, 128, None, 0,
                                    None) == INV
-    assert lib.laminar_linear_bf16(16, 16, 16, None, 65, 16, 128, None, 0,
+    assert lib.laminar_linear_bf16(16, 16, 16, None, 129, 16, 128, None, 0,
                                    None) == UNS
     # packing: NULL, in place, misaligned, shapes
     assert lib.laminar_linear_pack(None, 16, 16, 128, None) == INV
@@ -575,5 +575,5 @@ def test_linear_kernels_use_no_scratch():
                                       r.stderr)]
     kernels = [(n, sc, o) for n, sc, o in zip(names, scratch, occ)
                if "linear_kernel" in n]
-    assert len(kernels) == 3, kernels      # 16, 32 and 64 batch rows
+    assert len(kernels) == 4, kernels      # 16, 32, 64 and 128 batch rows
     assert all(sc == 0 and o >= 2 for _, sc, o in kernels), kernels

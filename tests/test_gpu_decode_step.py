@@ -70,7 +70,8 @@ def test_silu_mul_matches_oracle(m, inter):
 @pytest.mark.parametrize("m,n,k,in_place", [(1, 3584, 3584, False),
                                             (16, 3584, 18944, True),
                                             (33, 4608, 3584, False),
-                                            (5, 96, 640, True)])
+                                            (5, 96, 640, True),
+                                            (128, 3584, 3584, True)])
 def test_linear_bf16_with_residual(m, n, k, in_place):
     from paper_2510_12633_amd.api import SkinnyLinear
     _need_gpu()

@@ -23,7 +23,8 @@ def bits(t):
 
 SHAPES = [(1, 16, 128), (7, 48, 256), (16, 4608, 3584), (17, 3584, 3584),
           (33, 256, 1024), (64, 3584, 18944), (2, 37888, 3584),
-          (1, 152064, 3584), (48, 96, 640)]
+          (1, 152064, 3584), (48, 96, 640), (65, 4608, 3584),
+          (128, 3584, 18944), (100, 208, 512)]
 
 
 @pytest.mark.parametrize("m,n,k", SHAPES)
@@ -77,7 +78,7 @@ def test_linear_errors():
     y = torch.zeros((4, 32), device="cuda")
     s = torch.cuda.current_stream().cuda_stream
     with pytest.raises(N.LaminarError) as e:
-        N.laminar_linear(x, w, y, 65, 32, 256, None, 0, s)
+        N.laminar_linear(x, w, y, 129, 32, 256, None, 0, s)
     assert e.value.status == N.LAMINAR_ERR_UNSUPPORTED
     with pytest.raises(N.LaminarError) as e:
         N.laminar_linear(x, w, y, 4, 32, 200, None, 0, s)
