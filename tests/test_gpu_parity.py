@@ -213,6 +213,49 @@ def test_strided_q_equals_contiguous(cascade):
     assert np.array_equal(res[0][1], res[1][1]), name
 
 
+def test_distinct_plans_on_two_streams():
+    """Two plans with their own workspaces, bound and run on two streams at
+    once (the staging ring of the uploads is shared), give the same bits as
+    running them one after the other."""
+    from paper_2510_12633_amd.api import PagedDecodeAttention
+    _need_gpu()
+    wls = [make_workload(CUSTOM[0][1], seed=21, device="cuda"),
+           make_workload(CUSTOM[1][1], seed=22, device="cuda")]
+
+    def make(wl, stream):
+        c = wl.cfg
+        return PagedDecodeAttention(
+            batch=wl.batch, num_q_heads=c.num_q_heads,
+            num_kv_heads=c.num_kv_heads, head_dim=c.head_dim,
+            num_pages=wl.num_pages, max_blocks_per_seq=wl.block_table.shape[1],
+            seq_lens_host=wl.seq_lens, softmax_scale=wl.softmax_scale,
+            kv_dtype=c.kv_dtype, k_scale=wl.k_scale, v_scale=wl.v_scale,
+            pages_per_item=2, stream=stream)
+
+    def run(wl, att, stream):
+        bt = torch.as_tensor(wl.block_table, device="cuda")
+        lens = torch.as_tensor(wl.seq_lens, device="cuda")
+        return att(wl.q, wl.k_pages, wl.v_pages, bt, lens, stream=stream)
+
+    seq = []
+    for wl in wls:
+        att = make(wl, None)
+        o, l = run(wl, att, None)
+        torch.cuda.synchronize()
+        seq.append((o.cpu().numpy(), l.cpu().numpy()))
+        att.close()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for rep in range(3):
+        atts = [make(wl, s) for wl, s in zip(wls, streams)]
+        outs = [run(wl, att, s) for wl, att, s in zip(wls, atts, streams)]
+        torch.cuda.synchronize()
+        for (o, l), (so, sl) in zip(outs, seq):
+            assert np.array_equal(o.cpu().numpy(), so)
+            assert np.array_equal(l.cpu().numpy(), sl)
+        for att in atts:
+            att.close()
+
+
 def test_empty_batches():
     """batch 0 is a no-op; a batch whose trajectories are all empty gives
     out = 0 and lse = -inf (the merge identity) for every head."""
