@@ -491,6 +491,30 @@ def test_planner_under_address_and_ub_sanitizers(tmp_path):
     assert "plan_check OK" in r.stdout
 
 
+def test_repack_host_code_under_address_and_ub_sanitizers(tmp_path):
+    """Algorithm 1, the page assignment of a migration and the roofline
+    bound over random and edge-case inputs, built with g++ under ASan and
+    UBSan; every returned index and count is checked."""
+    gxx = shutil.which("g++")
+    if not gxx:
+        pytest.skip("g++ not available")
+    exe = tmp_path / "repack_check"
+    src = os.path.join(ROOT, "tests", "repack_check.cpp")
+    repack = os.path.join(ROOT, "paper_2510_12633_amd", "csrc", "repack.cpp")
+    cmd = [gxx, "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=all", "-I", os.path.join(ROOT, "include"),
+           src, repack, "-o", str(exe)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    env = dict(os.environ,
+               ASAN_OPTIONS="detect_leaks=1:verify_asan_link_order=0",
+               UBSAN_OPTIONS="print_stacktrace=1")
+    r = subprocess.run([str(exe)], capture_output=True, text=True, env=env,
+                       timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "repack_check OK" in r.stdout
+
+
 def test_attention_kernels_do_not_spill_in_the_page_loop():
     """The page-pair double buffer fills most of the register file. A spill
     inside the page loop costs ~15% of bandwidth, so no attention kernel
