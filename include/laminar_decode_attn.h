@@ -155,9 +155,10 @@ size_t laminar_plan_workspace_bytes(const laminar_plan* plan);
  * on `stream`. The lists are first copied into a pinned, device-mapped host
  * staging slot of the library (one small ring per device, allocated on first
  * use and kept until the process exits) and a small kernel on `stream`
- * copies them into the workspace, so the upload neither waits for earlier
- * work on the stream nor crosses to a DMA engine, and the plan may be
- * destroyed as soon as this call returns.
+ * copies them into the workspace, so the upload does not cross to a DMA
+ * engine and the plan may be destroyed as soon as this call returns. The
+ * ring has eight slots: the call waits only when the upload eight binds ago
+ * has not run yet.
  * Lists larger than one staging slot (1 MiB, about 65k work items) are
  * copied directly and the call waits for `stream` to finish the copy.
  * The workspace must stay allocated, and must not be used by anything else,

@@ -920,8 +920,9 @@ bool inputs_ok(const laminar_plan* p, const void* q, const void* k_pages,
 // pinned, device-mapped host slots, and a small kernel on the caller's
 // stream copies them into the workspace. Compared with a DMA copy this keeps
 // the upload on the same hardware queue as the attention kernels (no
-// cross-engine hand-offs around it), never blocks the host on earlier work,
-// and lets the caller free the plan as soon as bind returns. One ring per
+// cross-engine hand-offs around it), blocks the host only when the oldest of
+// eight uploads has not yet run (the host is then eight steps ahead), and
+// lets the caller free the plan as soon as bind returns. One ring per
 // device, created on first use and kept for the life of the process; a slot
 // is reused only after the event recorded behind its last upload completed.
 // Copies n16 16-byte words from device-mapped pinned host memory.
