@@ -15,7 +15,8 @@
  * x [M, K] bf16 (one row per trajectory), w [N, K] bf16 (one row per output
  * feature: the usual layout of a linear layer's weight), y [M, N] fp32,
  * all row-major and contiguous. Products of bf16 values are exact and are
- * accumulated in fp32 on the matrix cores; with several K splits the
+ * accumulated in fp32 on the matrix cores; with several K splits (over
+ * workgroups, or over the four wavefronts of one workgroup for M <= 4) the
  * partial sums are added in a fixed order, so results are deterministic.
  *
  * Packed weights. laminar_linear reads w in a packed layout made once per
@@ -53,7 +54,9 @@ extern "C" {
 laminar_status laminar_linear_pack(const void* w, void* w_packed, int32_t n,
                                    int32_t k, hipStream_t stream);
 
-/* Number of K splits the call will use (1: none). 0 outside the limits. */
+/* Number of K ranges the call spreads over workgroups (1: none, also when
+ * K is split only among the wavefronts of each workgroup, which needs no
+ * workspace). 0 outside the limits. */
 int32_t laminar_linear_splits(int32_t m, int32_t n, int32_t k);
 
 /* Device workspace bytes for the K splits (0 when there are none). */

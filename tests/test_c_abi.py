@@ -467,6 +467,12 @@ def test_linear_errors_before_any_launch():
                               None) == INV
     assert N.laminar_linear_splits(1, 152064, 3584) == 1
     assert N.laminar_linear_workspace_bytes(1, 152064, 3584) == 0
+    # up to 4 rows and 160 steps of K the split stays inside a workgroup
+    for m, n, k in ((1, 3584, 3584), (4, 3584, 18944), (3, 48, 640)):
+        assert N.laminar_linear_splits(m, n, k) == 1
+        assert N.laminar_linear_workspace_bytes(m, n, k) == 0
+    assert N.laminar_linear_splits(5, 3584, 3584) > 1
+    assert N.laminar_linear_splits(1, 5120, 27648) > 1     # 216 steps
     assert N.laminar_linear_splits(0, 16, 128) == 0
 
 
@@ -598,6 +604,7 @@ def test_linear_kernels_use_no_scratch():
     occ = [int(x) for x in re.findall(r"Occupancy \[waves/SIMD\]: (\d+)",
                                       r.stderr)]
     kernels = [(n, sc, o) for n, sc, o in zip(names, scratch, occ)
-               if "linear_kernel" in n]
-    assert len(kernels) == 4, kernels      # 16, 32, 64 and 128 batch rows
+               if "linear_kernel" in n or "linear_wave_split" in n]
+    # 16, 32, 64 and 128 batch rows, and the split over wavefronts
+    assert len(kernels) == 5, kernels
     assert all(sc == 0 and o >= 2 for _, sc, o in kernels), kernels

@@ -24,7 +24,11 @@ def bits(t):
 SHAPES = [(1, 16, 128), (7, 48, 256), (16, 4608, 3584), (17, 3584, 3584),
           (33, 256, 1024), (64, 3584, 18944), (2, 37888, 3584),
           (1, 152064, 3584), (48, 96, 640), (65, 4608, 3584),
-          (128, 3584, 18944), (100, 208, 512)]
+          (128, 3584, 18944), (100, 208, 512),
+          # K split over the wavefronts of a workgroup (M <= 4): ragged
+          # step counts per wavefront, 7B and 32B shapes
+          (4, 48, 640), (1, 3584, 3584), (3, 3584, 18944), (2, 7168, 5120),
+          (4, 5120, 20480)]
 
 
 @pytest.mark.parametrize("m,n,k", SHAPES)
