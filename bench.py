@@ -451,28 +451,34 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     def choose(m):
         """Per projection kind, the faster of the skinny kernel and the
         library GEMM at this batch, timed over every layer's weights in turn
-        (as in a step, so the 256 MB Infinity Cache does not hold them)."""
+        (as in a step, so the 256 MB Infinity Cache does not hold them);
+        the best of three alternating passes each, so that one slow pass
+        (a first call that tunes, a clock change) cannot decide."""
         picks = {}
         for i, kind in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
             projs = ([lm_head] * 4 if kind == "lm_head" else
                      [layer[i] for layer in layers])
             x = torch.randn((m, projs[0].k), generator=gen, device="cuda",
                             dtype=bf)
-            times = {}
-            for use in (False, True):
-                if use and m > 128:
-                    continue
+            uses = (False, True) if m <= 128 else (False,)
+            for use in uses:
                 for p in projs:
                     p.use_skinny = use
                 projs[0](x)
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record()
-                for p in projs:
-                    p(x)
-                e1.record()
-                torch.cuda.synchronize()
-                times[use] = e0.elapsed_time(e1)
+            torch.cuda.synchronize()
+            times = {use: float("inf") for use in uses}
+            for _ in range(3):
+                for use in uses:
+                    for p in projs:
+                        p.use_skinny = use
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    for p in projs:
+                        p(x)
+                    e1.record()
+                    torch.cuda.synchronize()
+                    times[use] = min(times[use], e0.elapsed_time(e1))
             best = min(times, key=times.get)
             for p in projs:
                 p.use_skinny = best
