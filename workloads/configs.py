@@ -127,18 +127,20 @@ CONFIGS = (
 # trajectories and lengths, the kv-heads split across GPUs with their query
 # heads. Attention needs no exchange between the shares, so one GPU's call
 # is exactly this.
+_FULL = {c.name: c for c in CONFIGS}
+
 TP_SHARES = (
     WorkloadConfig(
         name="32b_fp8_tp4", index=6, batch=128, num_q_heads=10,
         num_kv_heads=2, head_dim=128, kv_dtype="fp8_e4m3fn",
-        lengths=CONFIGS[3].lengths, seed_of=4,
+        lengths=_FULL["32b_fp8"].lengths, seed_of=_FULL["32b_fp8"].index,
         description="32b_fp8 on one GPU of four: 10q/2kv heads, the same "
                     "trajectory lengths"),
     WorkloadConfig(
         name="agentic_mix_tp8", index=7, batch=512, num_q_heads=8,
         num_kv_heads=1, head_dim=128, kv_dtype="bf16",
-        lengths=CONFIGS[4].lengths, prefix_group=8, prefix_tokens=1024,
-        seed_of=5,
+        lengths=_FULL["agentic_mix"].lengths, prefix_group=8, prefix_tokens=1024,
+        seed_of=_FULL["agentic_mix"].index,
         description="agentic_mix on one GPU of eight: 8q/1kv heads, the "
                     "same trajectory lengths and shared prefixes"),
 )
