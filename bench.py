@@ -424,7 +424,10 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
 
     class Proj:
         """One projection's weight in two layouts: packed by this library's
-        skinny kernel, and [K, N] for the library GEMM (x @ w)."""
+        skinny kernel, and [K, N] for the library GEMM (x @ w). `mode` says
+        which runs: "library", "skinny" (after a separate cast or SwiGLU
+        launch when the input needs one) or "fused" (the skinny kernel
+        makes its operand from the fp32 or gate-and-up input on load)."""
 
         def __init__(self, k, n):
             nk = (torch.randn((n, k), generator=gen, device="cuda",
@@ -433,12 +436,20 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             self.kn = nk.t().contiguous()
             self.skinny = SkinnyLinear(nk)
             del nk
-            self.use_skinny = False
+            self.mode = "library"
 
-        def __call__(self, x, residual=None):
+        def __call__(self, x, residual=None, swiglu=False):
             """bf16(x w^T), plus residual when given (in place into it on
-            the skinny path)."""
-            if self.use_skinny:
+            the skinny path). fp32 x is rounded to bf16 and, with swiglu, x
+            [M, 2K] is SwiGLU's gate and up."""
+            if self.mode == "fused":
+                return self.skinny.bf16(x, out=residual, residual=residual,
+                                        swiglu=swiglu)
+            if swiglu:
+                x = silu_mul(x)
+            elif x.dtype != bf:
+                x = x.to(bf)
+            if self.mode == "skinny":
                 return self.skinny.bf16(x, out=residual, residual=residual)
             if residual is None:
                 return x @ self.kn
@@ -449,40 +460,49 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     lm_head = Proj(h, vocab)
 
     def choose(m):
-        """Per projection kind, the faster of the skinny kernel and the
-        library GEMM at this batch, timed over every layer's weights in turn
-        (as in a step, so the 256 MB Infinity Cache does not hold them);
-        the best of three alternating passes each, so that one slow pass
-        (a first call that tunes, a clock change) cannot decide."""
+        """Per projection kind, the fastest way to run it at this batch:
+        the library GEMM, the skinny kernel, and for O and down also the
+        skinny kernel with its input made on load. Each is timed over every
+        layer's weights in turn (as in a step, so the 256 MB Infinity Cache
+        does not hold them), the best of three alternating passes, so that
+        one slow pass (a first call that tunes, a clock change) cannot
+        decide."""
         picks = {}
         for i, kind in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
             projs = ([lm_head] * 4 if kind == "lm_head" else
                      [layer[i] for layer in layers])
-            x = torch.randn((m, projs[0].k), generator=gen, device="cuda",
-                            dtype=bf)
-            uses = (False, True) if m <= 128 else (False,)
-            for use in uses:
+            # the operand as the step hands it over: the attention's fp32
+            # output to O, gate and up to down
+            kw = {"swiglu": kind == "down"}
+            x = torch.randn((m, projs[0].k * (2 if kind == "down" else 1)),
+                            generator=gen, device="cuda",
+                            dtype=torch.float32 if kind == "o" else bf)
+            modes = ["library"]
+            if m <= 128:
+                modes += ["skinny"] + (["fused"] if kind in ("o", "down") else [])
+            for mode in modes:
                 for p in projs:
-                    p.use_skinny = use
-                projs[0](x)
+                    p.mode = mode
+                projs[0](x, **kw)
             torch.cuda.synchronize()
-            times = {use: float("inf") for use in uses}
+            times = {mode: float("inf") for mode in modes}
             for _ in range(3):
-                for use in uses:
+                for mode in modes:
                     for p in projs:
-                        p.use_skinny = use
+                        p.mode = mode
                     e0 = torch.cuda.Event(enable_timing=True)
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record()
                     for p in projs:
-                        p(x)
+                        p(x, **kw)
                     e1.record()
                     torch.cuda.synchronize()
-                    times[use] = min(times[use], e0.elapsed_time(e1))
+                    times[mode] = min(times[mode], e0.elapsed_time(e1))
             best = min(times, key=times.get)
             for p in projs:
-                p.use_skinny = best
-            picks[kind] = "laminar_linear" if best else "library_gemm"
+                p.mode = best
+            picks[kind] = {"library": "library_gemm", "skinny": "laminar_linear",
+                           "fused": "laminar_linear_fused_input"}[best]
         return picks
 
     stream = torch.cuda.current_stream()
@@ -521,9 +541,9 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                     v_new = qkv[:, (hq + hkv) * d:].view(m, hkv, d)
                     kv_append(k_new, v_new, table, lens, kp, vp, stream=cur)
                     att(q, kp, vp, table, lens, out, lse, stream=cur)
-                    x = wo(out.view(m, hq * d).to(bf), residual=x)
+                    x = wo(out.view(m, hq * d), residual=x)
                     gu = wgu(rmsnorm(x, stream=cur))
-                    x = wd(silu_mul(gu, stream=cur), residual=x)
+                    x = wd(gu, residual=x, swiglu=True)
                 return lm_head(rmsnorm(x, stream=cur))
 
             # The step is ~400 launches: capture it in a HIP graph so the

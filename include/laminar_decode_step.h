@@ -18,7 +18,8 @@
  *                      silu(g) = g / (1 + exp(-g)),  i < I
  *
  * All arithmetic in fp32 from bf16 inputs, one rounding to bf16 (nearest
- * even) at the end. Layouts row-major and contiguous: x, y [M, N] bf16,
+ * even) at the end; exp(-g) and the division of silu use the hardware
+ * exponential and reciprocal (a few fp32 ulp before that rounding). Layouts row-major and contiguous: x, y [M, N] bf16,
  * weight [N] bf16 (NULL for all ones), gu [M, 2I] bf16 (gate then up), y
  * [M, I] bf16. Pointers 16-byte aligned; N and I multiples of 8. y may not
  * overlap the inputs. Errors: INVALID_ARG (NULL, misaligned, M < 1, N or I

@@ -29,10 +29,13 @@
  * are then 1 KB of contiguous bytes, which one wavefront load reads whole.
  *
  * Limits: 1 <= M <= 128, N a multiple of 16, K a multiple of 128 and at most
- * 2^24; larger batches are compute-bound and belong to a general GEMM.
+ * 2^24, and x padded to 16, 32, 64 or 128 rows at most 1 GiB (the kernels'
+ * buffer offsets are 32-bit); larger batches are compute-bound and belong
+ * to a general GEMM.
  * Workspace: laminar_linear_workspace_bytes(M, N, K) bytes of device
- * memory (0 when no K split is used), 256-byte aligned, owned by the
- * caller; calls that share a workspace must be ordered on one stream.
+ * memory (0 when K is not split over workgroups), 256-byte aligned, owned
+ * by the caller; calls that share a workspace must be ordered on one
+ * stream.
  * Pointers: x, w, w_packed and y 16-byte aligned; the caller owns every
  * buffer.
  * Errors: INVALID_ARG (NULL pointers, misalignment, w_packed equal to w, a
@@ -55,11 +58,12 @@ laminar_status laminar_linear_pack(const void* w, void* w_packed, int32_t n,
                                    int32_t k, hipStream_t stream);
 
 /* Number of K ranges the call spreads over workgroups (1: none, also when
- * K is split only among the wavefronts of each workgroup, which needs no
- * workspace). 0 outside the limits. */
+ * K is split only among the wavefronts of each workgroup). The same for
+ * every kind of x. 0 outside the limits. */
 int32_t laminar_linear_splits(int32_t m, int32_t n, int32_t k);
 
-/* Device workspace bytes for the K splits (0 when there are none). */
+/* Device workspace bytes for the K splits over workgroups (0 when there
+ * are none). */
 size_t laminar_linear_workspace_bytes(int32_t m, int32_t n, int32_t k);
 
 /* y = x w^T with w given in the packed layout. */
@@ -78,6 +82,31 @@ laminar_status laminar_linear_bf16(const void* x, const void* w_packed,
                                    void* y, const void* residual, int32_t m,
                                    int32_t n, int32_t k, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream);
+
+/* What the x argument of laminar_linear_bf16_ex holds. */
+typedef enum {
+  LAMINAR_X_BF16 = 0,      /* x [M, K] bf16, as in laminar_linear_bf16 */
+  LAMINAR_X_F32 = 1,       /* x [M, K] fp32; each value is rounded to bf16
+                              (nearest even) before the product, as a cast
+                              of x to bf16 would */
+  LAMINAR_X_SILU_MUL = 2   /* x [M, 2K] bf16, gate then up: the product's
+                              operand is bf16(silu(gate) * up), exactly what
+                              laminar_silu_mul writes */
+} laminar_linear_x;
+
+/* laminar_linear_bf16 with the operand made from x on load (x_kind, one of
+ * laminar_linear_x). A decode step uses it to read the fp32 attention
+ * output directly in the O projection and the gate+up output directly in
+ * the down projection, without the separate cast and SwiGLU launches; the
+ * results equal those of the separate launches bit for bit. x is 16-byte
+ * aligned. Errors as laminar_linear_bf16, plus INVALID_ARG for an unknown
+ * x_kind. */
+laminar_status laminar_linear_bf16_ex(const void* x, int32_t x_kind,
+                                      const void* w_packed, void* y,
+                                      const void* residual, int32_t m,
+                                      int32_t n, int32_t k, void* workspace,
+                                      size_t workspace_bytes,
+                                      hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -25,6 +25,10 @@ LAMINAR_ERR_HIP = 4
 LAMINAR_KV_BF16 = 0
 LAMINAR_KV_FP8_E4M3FN = 1
 
+LAMINAR_X_BF16 = 0
+LAMINAR_X_F32 = 1
+LAMINAR_X_SILU_MUL = 2
+
 
 class LaminarAttnDesc(ctypes.Structure):
     _fields_ = [
@@ -121,6 +125,10 @@ _SIGNATURES = {
     "laminar_linear_bf16": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p,
                                       c_int32, c_int32, c_int32, c_void_p,
                                       c_size_t, c_void_p]),
+    "laminar_linear_bf16_ex": (c_int32, [c_void_p, c_int32, c_void_p,
+                                         c_void_p, c_void_p, c_int32, c_int32,
+                                         c_int32, c_void_p, c_size_t,
+                                         c_void_p]),
     "laminar_rmsnorm": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32,
                                   c_int32, ctypes.c_float, c_void_p]),
     "laminar_silu_mul": (c_int32, [c_void_p, c_void_p, c_int32, c_int32,
@@ -391,6 +399,16 @@ def laminar_linear_bf16(x, w_packed, y, residual, m: int, n: int, k: int,
                                      _ptr(residual), int(m), int(n), int(k),
                                      _ptr(workspace), int(workspace_bytes),
                                      _ptr(stream)), "laminar_linear_bf16")
+
+
+def laminar_linear_bf16_ex(x, x_kind: int, w_packed, y, residual, m: int,
+                           n: int, k: int, workspace, workspace_bytes: int,
+                           stream):
+    _check(lib().laminar_linear_bf16_ex(_ptr(x), int(x_kind), _ptr(w_packed),
+                                        _ptr(y), _ptr(residual), int(m),
+                                        int(n), int(k), _ptr(workspace),
+                                        int(workspace_bytes), _ptr(stream)),
+           "laminar_linear_bf16_ex")
 
 
 def laminar_rmsnorm(x, weight, y, m: int, n: int, eps: float, stream):

@@ -207,14 +207,27 @@ class SkinnyLinear:
                          self.ws_bytes, _stream_handle(stream))
         return out
 
-    def bf16(self, x, out=None, residual=None, stream=None):
-        """bf16(x w^T + residual) [M, N]; out may be the residual itself."""
+    def bf16(self, x, out=None, residual=None, swiglu=False, stream=None):
+        """bf16(x w^T + residual) [M, N]; out may be the residual itself.
+        fp32 x [M, K] is rounded to bf16 on load; with swiglu, x [M, 2K]
+        bf16 holds gate then up and the operand is silu(gate) * up. Both
+        equal the separate cast or laminar_silu_mul followed by this call,
+        bit for bit, in one launch."""
         m = x.shape[0]
+        if swiglu:
+            kind = N.LAMINAR_X_SILU_MUL
+            want = (torch.bfloat16, 2 * self.k)
+        elif x.dtype == torch.float32:
+            kind, want = N.LAMINAR_X_F32, (torch.float32, self.k)
+        else:
+            kind, want = N.LAMINAR_X_BF16, (torch.bfloat16, self.k)
+        if (x.dtype, x.shape[1]) != want or not x.is_contiguous():
+            raise ValueError(f"x must be contiguous {want[0]} [M, {want[1]}]")
         if out is None:
             out = torch.empty((m, self.n), dtype=torch.bfloat16, device=x.device)
-        N.laminar_linear_bf16(x, self.w_packed, out, residual, m, self.n,
-                              self.k, self.ws, self.ws_bytes,
-                              _stream_handle(stream))
+        N.laminar_linear_bf16_ex(x, kind, self.w_packed, out, residual, m,
+                                 self.n, self.k, self.ws, self.ws_bytes,
+                                 _stream_handle(stream))
         return out
 
 

@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdint>
 
+#include "activation.h"
 #include "laminar_decode_step.h"
 
 namespace {
@@ -56,13 +57,7 @@ silu_mul_kernel(const bf16x8* __restrict__ gu, bf16x8* __restrict__ y,
   const size_t m = t / chunks, c = t - m * chunks;
   const bf16x8 g = gu[m * 2 * chunks + c];
   const bf16x8 u = gu[m * 2 * chunks + chunks + c];
-  bf16x8 o;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float gf = float(g[e]);
-    o[e] = (__bf16)(gf / (1.0f + expf(-gf)) * float(u[e]));
-  }
-  y[t] = o;
+  y[t] = laminar::silu_mul8(g, u);
 }
 
 bool misaligned16(const void* p) {

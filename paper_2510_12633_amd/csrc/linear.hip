@@ -32,6 +32,7 @@
 
 #include <cstdint>
 
+#include "activation.h"
 #include "laminar_linear.h"
 
 namespace {
@@ -50,15 +51,20 @@ constexpr int kMaxK = 1 << 24;       // keeps every buffer offset in 31 bits
 // the long-K shapes.
 constexpr int kMaxGroups = 512;
 // the split inside one workgroup: at most 4 rows and 160 steps of K
-constexpr int kWaveSplitMaxM = 4;
+constexpr int kWaveSplitMaxM = 4;      // rows of the x layout in its LDS
 constexpr int kWaveSplitMaxSteps = 160;
 // steps in flight: 4, or 2 for 128 batch rows (registers)
 template <int MT> constexpr int steps_in_flight() { return MT <= 4 ? 4 : 2; }
 constexpr int kOob = 0x40000000;     // past every buffer: reads as zero
 constexpr int kBufFlags = 0x00020000;
 
+// What x holds: the bf16 operand itself, fp32 values rounded to bf16 on
+// load, or a SwiGLU's gate and up halves combined on load.
+constexpr int kXBf16 = 0, kXF32 = 1, kXSiluMul = 2;
+
 struct LinearArgs {
-  const uint16_t* x;     // [M, K]
+  const void* x;         // [M, x_ld] of the kind the kernel is built for
+  int32_t x_ld;          // elements per row of x: K, or 2 K for gate and up
   const uint16_t* w;     // packed [N/16][K/8][16][8]
   float* y;              // [M, N] fp32 output, or NULL when yb is set
   uint16_t* yb;          // [M, N] bf16 output (rounded to nearest even)
@@ -95,7 +101,43 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int MT>
+// One 16-byte chunk of the bf16 operand (8 consecutive k of one row) as
+// loaded: one load for bf16 x, two for fp32 x (32 bytes) or for gate and up.
+template <int XK> struct XRaw { u32x4 v[XK == kXBf16 ? 1 : 2]; };
+
+template <int XK> constexpr int kXBytes = XK == kXF32 ? 4 : 2;
+
+// Loads the chunk at element e = row * x_ld + k of x (k a multiple of 8);
+// an offset at or past kOob reads zeros.
+template <int XK>
+__device__ __forceinline__ void load_x(XRaw<XK>& c, __amdgpu_buffer_rsrc_t xr,
+                                       int byte_off, int k_bytes) {
+  c.v[0] = __builtin_bit_cast(
+      u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, byte_off, 0, 0));
+  if constexpr (XK == kXF32)
+    c.v[1] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, byte_off + 16, 0, 0));
+  if constexpr (XK == kXSiluMul)     // up is K elements after gate
+    c.v[1] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, byte_off + k_bytes, 0, 0));
+}
+
+// The bf16 operand of a loaded chunk (zeros stay zeros in every kind).
+template <int XK>
+__device__ __forceinline__ u32x4 x_operand(const XRaw<XK>& c) {
+  if constexpr (XK == kXF32)
+    return __builtin_bit_cast(
+        u32x4, laminar::round8(__builtin_bit_cast(f32x4, c.v[0]),
+                               __builtin_bit_cast(f32x4, c.v[1])));
+  else if constexpr (XK == kXSiluMul)
+    return __builtin_bit_cast(
+        u32x4, laminar::silu_mul8(__builtin_bit_cast(bf16x8, c.v[0]),
+                                  __builtin_bit_cast(bf16x8, c.v[1])));
+  else
+    return c.v[0];
+}
+
+template <int MT, int XK>
 __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
   // x of one step, double-buffered: chunk (t, k/8 = c, row r) at
   // t * 256 + c * 16 + r, so the 64 lanes of a wavefront read 1 KB of
@@ -117,14 +159,15 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.w) + size_t(has_tile ? tile : 0) * 16 * a.k, 0,
       has_tile ? a.k * 32 : 0, kBufFlags);
+  constexpr int xe = kXBytes<XK>;
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(a.x), 0, a.m * a.k * 2, kBufFlags);
+      const_cast<void*>(a.x), 0, a.m * a.x_ld * xe, kBufFlags);
   // lane (q, r16) of matrix-core step j holds row r16, k chunk 4 j + q
   const int w_lane = (q * 16 + r16) * 16;
 
   constexpr int kNB = steps_in_flight<MT>();
   u32x4 wb[kNB][4];
-  u32x4 xb[kNB][MT];
+  XRaw<XK> xb[kNB][MT];
   auto load = [&](int s, int i) {
     const bool in = s < s1;
     const int kb = s * kStepK;
@@ -136,9 +179,9 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
                                                        /*nt*/ 2));
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-      const int xo = in ? ((16 * t + x_row) * a.k + kb + 8 * x_chunk) * 2 : kOob;
-      xb[i][t] = __builtin_bit_cast(
-          u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xo, 0, 0));
+      const int xo =
+          in ? ((16 * t + x_row) * a.x_ld + kb + 8 * x_chunk) * xe : kOob;
+      load_x<XK>(xb[i][t], xr, xo, a.k * 2);
     }
   };
 
@@ -155,7 +198,7 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
       const int s = st + i;
       u32x4* buf = xs[s & 1];
 #pragma unroll
-      for (int t = 0; t < MT; ++t) buf[t * 256 + tid] = xb[i][t];
+      for (int t = 0; t < MT; ++t) buf[t * 256 + tid] = x_operand<XK>(xb[i][t]);
       // The buffer written here was last read two steps ago, before every
       // wavefront passed the previous step's barrier.
       lds_barrier();
@@ -187,12 +230,18 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
 }
 
 // One 16-row tile per workgroup, K split over its four wavefronts: wave w
-// takes steps w, w + 4, w + 8, ... and loads its own x (at most four rows,
-// so a few hundred bytes per step, served by L2). The four sums are added
-// in LDS in wavefront order, so the result does not depend on timing.
+// takes steps w, w + 4, w + 8, ... The sums of the four are added in LDS in
+// wavefront order, so the result does not depend on timing. x has at most
+// four rows here: per step a wavefront loads those rows' 128 k with one
+// 16-byte chunk per lane (two for fp32 or gate and up), makes the bf16
+// operand, and passes it through its own 1 KB of LDS into the matrix-core
+// layout (rows 4-15 are zeros). So the raw x in flight takes 4-8 registers
+// per step instead of the 16-32 of loading the operand layout directly.
+template <int XK>
 __global__ void __launch_bounds__(256) linear_wave_split_kernel(const LinearArgs a) {
   constexpr int kNB = 4;
   __shared__ f32x4 part[3][64];
+  __shared__ u32x4 xw[4][64];          // per wavefront: x [4 rows][128 k]
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int tile = blockIdx.x;
@@ -201,39 +250,45 @@ __global__ void __launch_bounds__(256) linear_wave_split_kernel(const LinearArgs
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.w) + size_t(tile) * 16 * a.k, 0, a.k * 32,
       kBufFlags);
+  constexpr int xe = kXBytes<XK>;
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(a.x), 0, a.m * a.k * 2, kBufFlags);
+      const_cast<void*>(a.x), 0, a.m * a.x_ld * xe, kBufFlags);
   const int w_lane = (q * 16 + r16) * 16;
+  // this lane loads x row lane / 16, k chunk lane % 16 of each step, which
+  // is chunk (lane / 16) * 16 + lane % 16 = lane of the wavefront's LDS
+  const int x_lane = ((lane >> 4) * a.x_ld + 8 * (lane & 15)) * xe;
   u32x4 wb[kNB][4];
-  u32x4 xb[kNB][4];
-  // lane (q, r16) of matrix-core step j holds w row r16 and x row r16, k
-  // chunk 4 j + q; rows of x past M read as zeros
+  XRaw<XK> xb[kNB];
   auto load = [&](int s, int i) {
     const bool in = s < steps;
     const int kb = s * kStepK;
     const int wo = in ? kb * 32 + w_lane : kOob;
-    const int xo = in ? (r16 * a.k + kb + 8 * q) * 2 : kOob;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       wb[i][j] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(wr, wo + 1024 * j, 0,
                                                        /*nt*/ 2));
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      xb[i][j] = __builtin_bit_cast(
-          u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xo + 64 * j, 0, 0));
+    load_x<XK>(xb[i], xr, in ? kb * xe + x_lane : kOob, a.k * 2);
   };
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  u32x4* xs = xw[wave];
 #pragma unroll
   for (int i = 0; i < kNB; ++i) load(wave + 4 * i, i);
   for (int st = wave; st < steps; st += 4 * kNB) {
 #pragma unroll
     for (int i = 0; i < kNB; ++i) {
+      // LDS accesses of one wavefront complete in order: the reads below
+      // see this write, and the next step's write follows these reads
+      xs[lane] = x_operand<XK>(xb[i]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 4; ++j) {
+        // lane (q, r16) of matrix-core step j: x row r16, k chunk 4 j + q
+        const u32x4 xv = xs[(r16 & 3) * 16 + 4 * j + q];
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             __builtin_bit_cast(bf16x8, wb[i][j]),
-            __builtin_bit_cast(bf16x8, xb[i][j]), acc, 0, 0, 0);
+            __builtin_bit_cast(bf16x8, r16 < 4 ? xv : u32x4{0, 0, 0, 0}), acc,
+            0, 0, 0);
+      }
       load(st + 4 * i + 4 * kNB, i);
     }
   }
@@ -280,13 +335,20 @@ bool shape_ok(int32_t m, int32_t n, int32_t k) {
   return m >= 1 && m <= kMaxM && shape_ok(n, k);
 }
 
+// Batch tiles of 16 rows the kernel is instantiated for: 1, 2, 4 or 8.
+int launch_tiles(int32_t m) {
+  const int mt = (m + 15) / 16;
+  return mt <= 2 ? mt : (mt <= 4 ? 4 : 8);
+}
+
 struct SplitPlan {
   int32_t splits;      // K ranges over workgroups (1: none)
   int32_t per;         // steps per range
   bool wave_split;     // K split over the four wavefronts of a workgroup
 };
 
-SplitPlan split_plan(int32_t m, int32_t n, int32_t k) {
+// The K split over workgroups alone (what the workspace is sized for).
+SplitPlan group_split_plan(int32_t n, int32_t k) {
   const int32_t tiles = n / 16, steps = k / kStepK;
   int32_t want = kMaxGroups / ((tiles + 3) / 4);
   if (want < 1) want = 1;
@@ -294,7 +356,18 @@ SplitPlan split_plan(int32_t m, int32_t n, int32_t k) {
   SplitPlan p;
   p.per = (steps + want - 1) / want;
   p.splits = (steps + p.per - 1) / p.per;
-  p.wave_split = p.splits > 1 && m <= kWaveSplitMaxM && steps <= kWaveSplitMaxSteps;
+  p.wave_split = false;
+  return p;
+}
+
+// The plan does not depend on what x holds, so the fused kinds of x sum in
+// the same order as a bf16 x. A split over workgroups leaves at most 1024
+// tiles, all resident with four workgroups per CU.
+SplitPlan split_plan(int32_t m, int32_t n, int32_t k) {
+  SplitPlan p = group_split_plan(n, k);
+  const int32_t steps = k / kStepK;
+  p.wave_split = p.splits > 1 && m <= kWaveSplitMaxM &&
+                 steps <= kWaveSplitMaxSteps;
   if (p.wave_split) {
     p.splits = 1;
     p.per = steps;
@@ -310,17 +383,49 @@ bool misaligned16(const void* p) {
 
 namespace {
 
-laminar_status linear_impl(const void* x, const void* w_packed, float* y,
-                           void* yb, const void* res, int32_t m, int32_t n,
-                           int32_t k, void* workspace, size_t workspace_bytes,
-                           hipStream_t stream) {
+template <int XK>
+hipError_t launch(const LinearArgs& a, const SplitPlan& plan, int m,
+                  hipStream_t stream) {
+  if (plan.wave_split) {
+    hipLaunchKernelGGL((linear_wave_split_kernel<XK>), dim3(a.n_tiles),
+                       dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
+  const dim3 grid((a.n_tiles + 3) / 4, a.splits);
+  switch (launch_tiles(m)) {
+    case 1: hipLaunchKernelGGL((linear_kernel<1, XK>), grid, dim3(256), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((linear_kernel<2, XK>), grid, dim3(256), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL((linear_kernel<4, XK>), grid, dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL((linear_kernel<8, XK>), grid, dim3(256), 0, stream, a); break;
+  }
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && a.splits > 1) {
+    const size_t total = size_t(m) * a.n / 4;
+    hipLaunchKernelGGL(linear_reduce, dim3(unsigned((total + 255) / 256)),
+                       dim3(256), 0, stream, a);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
+                           float* y, void* yb, const void* res, int32_t m,
+                           int32_t n, int32_t k, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
   if (!x || !w_packed || (!y && !yb)) return LAMINAR_ERR_INVALID_ARG;
+  if (x_kind != kXBf16 && x_kind != kXF32 && x_kind != kXSiluMul)
+    return LAMINAR_ERR_INVALID_ARG;
   if (misaligned16(x) || misaligned16(w_packed) || misaligned16(y) ||
       misaligned16(yb) || misaligned16(res))
     return LAMINAR_ERR_INVALID_ARG;
   if (!shape_ok(m, n, k)) return LAMINAR_ERR_UNSUPPORTED;
+  // byte offsets into x, padding rows included, stay below 2^31
+  const size_t row_bytes = size_t(k) * (x_kind == kXBf16 ? 2 : 4);
+  if (size_t(16) * launch_tiles(m) * row_bytes > size_t(kOob))
+    return LAMINAR_ERR_UNSUPPORTED;
   LinearArgs a;
-  a.x = static_cast<const uint16_t*>(x);
+  a.x = x;
+  a.x_ld = x_kind == kXSiluMul ? 2 * k : k;
   a.w = static_cast<const uint16_t*>(w_packed);
   a.y = y;
   a.yb = static_cast<uint16_t*>(yb);
@@ -340,28 +445,14 @@ laminar_status linear_impl(const void* x, const void* w_packed, float* y,
       return LAMINAR_ERR_INVALID_ARG;
     a.part = static_cast<float*>(workspace);
   }
-  if (plan.wave_split) {
-    hipLaunchKernelGGL(linear_wave_split_kernel, dim3(a.n_tiles), dim3(256), 0,
-                       stream, a);
-    return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
-  }
-  const dim3 grid((a.n_tiles + 3) / 4, a.splits);
-  const int mt = (m + 15) / 16;
-  switch (mt) {
-    case 1: hipLaunchKernelGGL(linear_kernel<1>, grid, dim3(256), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL(linear_kernel<2>, grid, dim3(256), 0, stream, a); break;
-    case 3:
-    case 4: hipLaunchKernelGGL(linear_kernel<4>, grid, dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL(linear_kernel<8>, grid, dim3(256), 0, stream, a); break;
-  }
-  if (hipGetLastError() != hipSuccess) return LAMINAR_ERR_HIP;
-  if (a.splits > 1) {
-    const size_t total = size_t(m) * n / 4;
-    hipLaunchKernelGGL(linear_reduce, dim3(unsigned((total + 255) / 256)),
-                       dim3(256), 0, stream, a);
-    if (hipGetLastError() != hipSuccess) return LAMINAR_ERR_HIP;
-  }
-  return LAMINAR_OK;
+  hipError_t e;
+  if (x_kind == kXF32)
+    e = launch<kXF32>(a, plan, m, stream);
+  else if (x_kind == kXSiluMul)
+    e = launch<kXSiluMul>(a, plan, m, stream);
+  else
+    e = launch<kXBf16>(a, plan, m, stream);
+  return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
 }
 
 }  // namespace
@@ -394,8 +485,8 @@ laminar_status laminar_linear(const void* x, const void* w_packed, float* y,
                               int32_t m, int32_t n, int32_t k, void* workspace,
                               size_t workspace_bytes, hipStream_t stream) {
   if (!y) return LAMINAR_ERR_INVALID_ARG;
-  return linear_impl(x, w_packed, y, nullptr, nullptr, m, n, k, workspace,
-                     workspace_bytes, stream);
+  return linear_impl(x, kXBf16, w_packed, y, nullptr, nullptr, m, n, k,
+                     workspace, workspace_bytes, stream);
 }
 
 laminar_status laminar_linear_bf16(const void* x, const void* w_packed,
@@ -403,8 +494,19 @@ laminar_status laminar_linear_bf16(const void* x, const void* w_packed,
                                    int32_t n, int32_t k, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream) {
   if (!y) return LAMINAR_ERR_INVALID_ARG;
-  return linear_impl(x, w_packed, nullptr, y, residual, m, n, k, workspace,
-                     workspace_bytes, stream);
+  return linear_impl(x, kXBf16, w_packed, nullptr, y, residual, m, n, k,
+                     workspace, workspace_bytes, stream);
+}
+
+laminar_status laminar_linear_bf16_ex(const void* x, int32_t x_kind,
+                                      const void* w_packed, void* y,
+                                      const void* residual, int32_t m,
+                                      int32_t n, int32_t k, void* workspace,
+                                      size_t workspace_bytes,
+                                      hipStream_t stream) {
+  if (!y) return LAMINAR_ERR_INVALID_ARG;
+  return linear_impl(x, x_kind, w_packed, nullptr, y, residual, m, n, k,
+                     workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

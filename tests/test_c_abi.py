@@ -452,6 +452,19 @@ def test_linear_errors_before_any_launch():
                                    None) == INV
     assert lib.laminar_linear_bf16(16, 16, 16, None, 129, 16, 128, None, 0,
                                    None) == UNS
+    # fused x kinds: unknown kind, misaligned x, x offsets past 31 bits
+    ex = lib.laminar_linear_bf16_ex
+    assert ex(16, 3, 16, 16, None, 1, 16, 128, None, 0, None) == INV
+    assert ex(16, -1, 16, 16, None, 1, 16, 128, None, 0, None) == INV
+    assert ex(24, N.LAMINAR_X_F32, 16, 16, None, 1, 16, 128, None, 0, None) == INV
+    assert ex(16, N.LAMINAR_X_SILU_MUL, 16, None, None, 1, 16, 128, None, 0,
+              None) == INV
+    assert ex(16, N.LAMINAR_X_F32, 16, 16, None, 128, 16, 1 << 22, None, 0,
+              None) == UNS                      # 128 rows x 16 MiB of fp32
+    assert ex(16, N.LAMINAR_X_SILU_MUL, 16, 16, None, 65, 16, 1 << 22, None,
+              0, None) == UNS                   # 128 padded rows x 16 MiB of gate+up
+    assert lib.laminar_linear(16, 16, 16, 128, 16, 1 << 23, None, 0,
+                              None) == UNS      # 128 rows x 16 MiB of bf16
     # packing: NULL, in place, misaligned, shapes
     assert lib.laminar_linear_pack(None, 16, 16, 128, None) == INV
     assert lib.laminar_linear_pack(16, 16, 16, 128, None) == INV
@@ -605,6 +618,15 @@ def test_linear_kernels_use_no_scratch():
                                       r.stderr)]
     kernels = [(n, sc, o) for n, sc, o in zip(names, scratch, occ)
                if "linear_kernel" in n or "linear_wave_split" in n]
-    # 16, 32, 64 and 128 batch rows, and the split over wavefronts
-    assert len(kernels) == 5, kernels
-    assert all(sc == 0 and o >= 2 for _, sc, o in kernels), kernels
+    # 16, 32, 64 and 128 batch rows and the split over wavefronts, for each
+    # of the three kinds of x
+    assert len(kernels) == 15, kernels
+    assert all(sc == 0 for _, sc, o in kernels), kernels
+    # two wavefronts per SIMD for the workgroup split (the 128-row kernel on
+    # gate and up excepted); the split over wavefronts, which runs up to
+    # 1024 tiles in one grid, keeps them all resident with four per SIMD
+    for n, _, o in kernels:
+        if "wave_split" in n:
+            assert o >= 4, (n, o)
+        elif "ILi8ELi2E" not in n:
+            assert o >= 2, (n, o)

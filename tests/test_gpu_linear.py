@@ -98,3 +98,42 @@ def test_linear_errors():
                      torch.empty(max(need, 1), dtype=torch.uint8, device="cuda"),
                      need, s)
     torch.cuda.synchronize()
+
+
+FUSED_SHAPES = [(1, 3584, 3584), (4, 3584, 3584), (3, 5120, 5120),
+                (2, 3584, 18944), (4, 48, 640), (5, 4608, 3584),
+                (17, 256, 1024), (64, 3584, 18944), (128, 208, 512)]
+
+
+@pytest.mark.parametrize("m,n,k", FUSED_SHAPES)
+def test_fused_inputs_equal_the_separate_launches(m, n, k):
+    """fp32 x rounded on load equals a cast then the bf16-x call, and gate
+    and up combined on load equal laminar_silu_mul then the call, bit for
+    bit, with and without the residual (in place). The shapes cover the
+    split over wavefronts (M <= 4 and at most 256 or 512 tiles), the split
+    over workgroups and no split."""
+    from paper_2510_12633_amd.api import SkinnyLinear, silu_mul
+    _need_gpu()
+    print(f"[gpu-linear-fused] m={m} n={n} k={k}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(7 * m + n + k)
+    w = (torch.randn((n, k), generator=g, device="cuda") / k ** 0.5).to(torch.bfloat16)
+    lin = SkinnyLinear(w)
+    x32 = torch.randn((m, k), generator=g, device="cuda") * 3
+    gu = (torch.randn((m, 2 * k), generator=g, device="cuda") * 4).to(torch.bfloat16)
+    res = torch.randn((m, n), generator=g, device="cuda").to(torch.bfloat16)
+    for fused, separate in ((lambda **kw: lin.bf16(x32, **kw),
+                             lambda **kw: lin.bf16(x32.to(torch.bfloat16), **kw)),
+                            (lambda **kw: lin.bf16(gu, swiglu=True, **kw),
+                             lambda **kw: lin.bf16(silu_mul(gu), **kw))):
+        a, b = fused(), separate()
+        ra, rb = res.clone(), res.clone()
+        fused(out=ra, residual=ra)
+        separate(out=rb, residual=rb)
+        torch.cuda.synchronize()
+        assert torch.equal(bits_t(a), bits_t(b))
+        assert torch.equal(bits_t(ra), bits_t(rb))
+        assert torch.isfinite(a.float()).all()
+
+
+def bits_t(t):
+    return t.view(torch.int16)
