@@ -438,15 +438,18 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             del nk
             self.mode = "library"
 
-        def __call__(self, x, residual=None, swiglu=False):
+        def __call__(self, x, residual=None, swiglu=False, norm=None):
             """bf16(x w^T), plus residual when given (in place into it on
-            the skinny path). fp32 x is rounded to bf16 and, with swiglu, x
-            [M, 2K] is SwiGLU's gate and up."""
+            the skinny path). fp32 x is rounded to bf16; with swiglu, x
+            [M, 2K] is SwiGLU's gate and up; with norm (a [K] weight), the
+            operand is the RMS norm of x."""
             if self.mode == "fused":
                 return self.skinny.bf16(x, out=residual, residual=residual,
-                                        swiglu=swiglu)
+                                        swiglu=swiglu, norm_weight=norm)
             if swiglu:
                 x = silu_mul(x)
+            elif norm is not None:
+                x = rmsnorm(x, norm)
             elif x.dtype != bf:
                 x = x.to(bf)
             if self.mode == "skinny":
@@ -458,6 +461,10 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     layers = [(Proj(h, (hq + 2 * hkv) * d), Proj(hq * d, h),
                Proj(h, 2 * inter), Proj(inter, h)) for _ in range(L)]
     lm_head = Proj(h, vocab)
+    # RMS norm weights: before attention and before the MLP of each layer,
+    # and the final one
+    norms = (1 + 0.1 * torch.randn((2 * L + 1, h), generator=gen,
+                                   device="cuda")).to(bf)
 
     def choose(m):
         """Per projection kind, the fastest way to run it at this batch:
@@ -471,15 +478,19 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
         for i, kind in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
             projs = ([lm_head] * 4 if kind == "lm_head" else
                      [layer[i] for layer in layers])
-            # the operand as the step hands it over: the attention's fp32
-            # output to O, gate and up to down
-            kw = {"swiglu": kind == "down"}
+            # the operand as the step hands it over: the residual stream
+            # and a norm weight to QKV, gate+up and the LM head, the
+            # attention's fp32 output to O, gate and up to down
+            normed = kind in ("qkv", "gate_up", "lm_head")
+            kw = {"swiglu": kind == "down", "norm": norms[0] if normed else None}
             x = torch.randn((m, projs[0].k * (2 if kind == "down" else 1)),
                             generator=gen, device="cuda",
                             dtype=torch.float32 if kind == "o" else bf)
             modes = ["library"]
             if m <= 128:
-                modes += ["skinny"] + (["fused"] if kind in ("o", "down") else [])
+                modes.append("skinny")
+            if m <= (4 if normed else 128):
+                modes.append("fused")
             for mode in modes:
                 for p in projs:
                     p.mode = mode
@@ -533,8 +544,8 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                 cur = torch.cuda.current_stream()
                 x = x0.clone()                    # the residual stream
 
-                for wqkv, wo, wgu, wd in layers:
-                    qkv = wqkv(rmsnorm(x, stream=cur))
+                for li, (wqkv, wo, wgu, wd) in enumerate(layers):
+                    qkv = wqkv(x, norm=norms[2 * li])
                     # q, k and v are read in place from the fused output
                     q = qkv[:, :hq * d].view(m, hq, d)
                     k_new = qkv[:, hq * d:(hq + hkv) * d].view(m, hkv, d)
@@ -542,9 +553,9 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                     kv_append(k_new, v_new, table, lens, kp, vp, stream=cur)
                     att(q, kp, vp, table, lens, out, lse, stream=cur)
                     x = wo(out.view(m, hq * d), residual=x)
-                    gu = wgu(rmsnorm(x, stream=cur))
+                    gu = wgu(x, norm=norms[2 * li + 1])
                     x = wd(gu, residual=x, swiglu=True)
-                return lm_head(rmsnorm(x, stream=cur))
+                return lm_head(x, norm=norms[2 * L])
 
             # The step is ~400 launches: capture it in a HIP graph so the
             # curve shows the GPU's time, not the host's launch rate.

@@ -100,13 +100,32 @@ typedef enum {
  * the down projection, without the separate cast and SwiGLU launches; the
  * results equal those of the separate launches bit for bit. x is 16-byte
  * aligned. Errors as laminar_linear_bf16, plus INVALID_ARG for an unknown
- * x_kind. */
+ * x_kind (the RMS-norm input has its own call below). */
 laminar_status laminar_linear_bf16_ex(const void* x, int32_t x_kind,
                                       const void* w_packed, void* y,
                                       const void* residual, int32_t m,
                                       int32_t n, int32_t k, void* workspace,
                                       size_t workspace_bytes,
                                       hipStream_t stream);
+
+/* laminar_linear_bf16 on RMS-normalised rows, the norm done on load:
+ * the operand is bf16((x[m, k] r_m) norm_weight[k]) with
+ * r_m = 1 / sqrt(mean_k x[m, k]^2 + eps), the pre-norm of a decoder layer
+ * in front of its QKV and gate+up projections. Every workgroup finds the
+ * r_m it needs with the summation order of laminar_rmsnorm, so the result
+ * equals laminar_rmsnorm followed by laminar_linear_bf16 bit for bit, in
+ * one launch. x [M, K] bf16 and norm_weight [K] bf16, 16-byte aligned.
+ * Errors: INVALID_ARG (as laminar_linear_bf16, and a NULL or misaligned
+ * norm_weight, eps negative or not finite), UNSUPPORTED (also M > 4: the
+ * norm of larger batches is one laminar_rmsnorm launch). */
+laminar_status laminar_linear_bf16_rmsnorm(const void* x,
+                                           const void* norm_weight, float eps,
+                                           const void* w_packed, void* y,
+                                           const void* residual, int32_t m,
+                                           int32_t n, int32_t k,
+                                           void* workspace,
+                                           size_t workspace_bytes,
+                                           hipStream_t stream);
 
 #ifdef __cplusplus
 }

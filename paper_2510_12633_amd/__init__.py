@@ -26,7 +26,8 @@ from ._native import (LaminarModelShape, LaminarRolloutState,
                       laminar_repack_plan, laminar_roofline_batch_bound,
                       laminar_roofline_step_seconds)
 from ._native import (laminar_linear, laminar_linear_bf16,
-                      laminar_linear_bf16_ex, laminar_linear_pack,
+                      laminar_linear_bf16_ex, laminar_linear_bf16_rmsnorm,
+                      laminar_linear_pack,
                       laminar_linear_splits, laminar_linear_workspace_bytes)
 from .api import (PagedDecodeAttention, SkinnyLinear, kv_append, migrate,
                   rmsnorm, silu_mul)

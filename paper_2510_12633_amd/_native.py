@@ -129,6 +129,11 @@ _SIGNATURES = {
                                          c_void_p, c_void_p, c_int32, c_int32,
                                          c_int32, c_void_p, c_size_t,
                                          c_void_p]),
+    "laminar_linear_bf16_rmsnorm": (c_int32, [c_void_p, c_void_p,
+                                              ctypes.c_float, c_void_p,
+                                              c_void_p, c_void_p, c_int32,
+                                              c_int32, c_int32, c_void_p,
+                                              c_size_t, c_void_p]),
     "laminar_rmsnorm": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32,
                                   c_int32, ctypes.c_float, c_void_p]),
     "laminar_silu_mul": (c_int32, [c_void_p, c_void_p, c_int32, c_int32,
@@ -409,6 +414,15 @@ def laminar_linear_bf16_ex(x, x_kind: int, w_packed, y, residual, m: int,
                                         int(n), int(k), _ptr(workspace),
                                         int(workspace_bytes), _ptr(stream)),
            "laminar_linear_bf16_ex")
+
+
+def laminar_linear_bf16_rmsnorm(x, norm_weight, eps: float, w_packed, y,
+                                residual, m: int, n: int, k: int, workspace,
+                                workspace_bytes: int, stream):
+    _check(lib().laminar_linear_bf16_rmsnorm(
+        _ptr(x), _ptr(norm_weight), float(eps), _ptr(w_packed), _ptr(y),
+        _ptr(residual), int(m), int(n), int(k), _ptr(workspace),
+        int(workspace_bytes), _ptr(stream)), "laminar_linear_bf16_rmsnorm")
 
 
 def laminar_rmsnorm(x, weight, y, m: int, n: int, eps: float, stream):

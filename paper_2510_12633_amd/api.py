@@ -207,13 +207,27 @@ class SkinnyLinear:
                          self.ws_bytes, _stream_handle(stream))
         return out
 
-    def bf16(self, x, out=None, residual=None, swiglu=False, stream=None):
+    def bf16(self, x, out=None, residual=None, swiglu=False, norm_weight=None,
+             eps: float = 1e-6, stream=None):
         """bf16(x w^T + residual) [M, N]; out may be the residual itself.
         fp32 x [M, K] is rounded to bf16 on load; with swiglu, x [M, 2K]
-        bf16 holds gate then up and the operand is silu(gate) * up. Both
-        equal the separate cast or laminar_silu_mul followed by this call,
-        bit for bit, in one launch."""
+        bf16 holds gate then up and the operand is silu(gate) * up; with
+        norm_weight [K] bf16 (at most 4 rows), the operand is
+        rmsnorm(x, norm_weight, eps). Each equals the separate cast,
+        laminar_silu_mul or laminar_rmsnorm followed by this call, bit for
+        bit, in one launch."""
         m = x.shape[0]
+        if norm_weight is not None:
+            if x.dtype != torch.bfloat16 or x.shape[1] != self.k or swiglu:
+                raise ValueError(f"x must be bf16 [M, {self.k}] for the norm")
+            if out is None:
+                out = torch.empty((m, self.n), dtype=torch.bfloat16,
+                                  device=x.device)
+            N.laminar_linear_bf16_rmsnorm(x, norm_weight, eps, self.w_packed,
+                                          out, residual, m, self.n, self.k,
+                                          self.ws, self.ws_bytes,
+                                          _stream_handle(stream))
+            return out
         if swiglu:
             kind = N.LAMINAR_X_SILU_MUL
             want = (torch.bfloat16, 2 * self.k)

@@ -43,6 +43,44 @@ __device__ __forceinline__ bf16x8_t round8(f32x4_t lo, f32x4_t hi) {
   return o;
 }
 
+// RMS norm pieces, shared by laminar_rmsnorm and the projection's fused
+// norm so that both sum in the same order and round identically.
+//
+// Sum of squares of one 16-byte chunk added to a running fma chain.
+__device__ __forceinline__ float sumsq8(bf16x8_t v, float ss) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ss = fmaf(float(v[e]), float(v[e]), ss);
+  return ss;
+}
+
+// Butterfly sum over a 64-lane wavefront: every lane ends with the same
+// value (each stage adds the same two operands on both lanes).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// 1 / sqrt(mean of squares + eps) from the sums of four 64-thread groups.
+__device__ __forceinline__ float rms_inverse(float p0, float p1, float p2,
+                                             float p3, float inv_n,
+                                             float eps) {
+  const float total = (p0 + p1) + (p2 + p3);
+  return 1.0f / sqrtf(total * inv_n + eps);
+}
+
+// Eight normalised outputs: (x r) w, rounded once to bf16.
+__device__ __forceinline__ bf16x8_t rms_scale8(bf16x8_t x, bf16x8_t w,
+                                               float r) {
+  bf16x8_t o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float s = float(x[e]) * r;
+    o[e] = (__bf16)(s * float(w[e]));
+  }
+  return o;
+}
+
 }  // namespace laminar
 
 #endif  // LAMINAR_ACTIVATION_H

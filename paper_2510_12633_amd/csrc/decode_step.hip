@@ -15,8 +15,11 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-// One workgroup per row: sum of squares over 16-byte chunks, a workgroup
-// reduction, then a second pass (served by L2) that scales and rounds.
+// One workgroup per row: thread t sums the squares of chunks t, t + 256,
+// ... in one fma chain, each wavefront adds its 64 chains by a butterfly,
+// and the four wavefront sums are added as (w0 + w1) + (w2 + w3); then a
+// second pass (served by L2) scales and rounds. The projection kernel's
+// fused norm follows the same order.
 __global__ void __launch_bounds__(256)
 rmsnorm_kernel(const bf16x8* __restrict__ x, const bf16x8* __restrict__ w,
                bf16x8* __restrict__ y, int chunks, float inv_n, float eps) {
@@ -24,26 +27,22 @@ rmsnorm_kernel(const bf16x8* __restrict__ x, const bf16x8* __restrict__ w,
   const bf16x8* xr = x + size_t(blockIdx.x) * chunks;
   bf16x8* yr = y + size_t(blockIdx.x) * chunks;
   float ss = 0.f;
-  for (int c = threadIdx.x; c < chunks; c += 256) {
-    const bf16x8 v = xr[c];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) ss = fmaf(float(v[e]), float(v[e]), ss);
-  }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+  for (int c = threadIdx.x; c < chunks; c += 256) ss = laminar::sumsq8(xr[c], ss);
+  ss = laminar::wave_sum(ss);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const float total = (part[0] + part[1]) + (part[2] + part[3]);
-  const float r = 1.0f / sqrtf(total * inv_n + eps);
+  const float r =
+      laminar::rms_inverse(part[0], part[1], part[2], part[3], inv_n, eps);
   for (int c = threadIdx.x; c < chunks; c += 256) {
     const bf16x8 v = xr[c];
-    bf16x8 o;
+    if (w) {
+      yr[c] = laminar::rms_scale8(v, w[c], r);
+    } else {
+      bf16x8 o;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float s = float(v[e]) * r;
-      o[e] = (__bf16)(w ? s * float(w[c][e]) : s);
+      for (int e = 0; e < 8; ++e) o[e] = (__bf16)(float(v[e]) * r);
+      yr[c] = o;
     }
-    yr[c] = o;
   }
 }
 

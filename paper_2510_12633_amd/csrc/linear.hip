@@ -30,6 +30,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdint>
 
 #include "activation.h"
@@ -59,12 +60,16 @@ constexpr int kOob = 0x40000000;     // past every buffer: reads as zero
 constexpr int kBufFlags = 0x00020000;
 
 // What x holds: the bf16 operand itself, fp32 values rounded to bf16 on
-// load, or a SwiGLU's gate and up halves combined on load.
-constexpr int kXBf16 = 0, kXF32 = 1, kXSiluMul = 2;
+// load, a SwiGLU's gate and up halves combined on load, or the input of an
+// RMS norm (scaled by the row's 1 / rms and the norm weight on load).
+constexpr int kXBf16 = 0, kXF32 = 1, kXSiluMul = 2, kXRmsNorm = 3;
+constexpr int kNormMaxM = 4;        // rows of the fused norm: one per wavefront
 
 struct LinearArgs {
   const void* x;         // [M, x_ld] of the kind the kernel is built for
   int32_t x_ld;          // elements per row of x: K, or 2 K for gate and up
+  const uint16_t* norm_w;  // [K] bf16 weight of the fused RMS norm
+  float norm_inv_k, norm_eps;
   const uint16_t* w;     // packed [N/16][K/8][16][8]
   float* y;              // [M, N] fp32 output, or NULL when yb is set
   uint16_t* yb;          // [M, N] bf16 output (rounded to nearest even)
@@ -102,29 +107,51 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // One 16-byte chunk of the bf16 operand (8 consecutive k of one row) as
-// loaded: one load for bf16 x, two for fp32 x (32 bytes) or for gate and up.
+// loaded: one load for bf16 x, two for fp32 x (32 bytes), for gate and up,
+// or for x and the norm weight.
 template <int XK> struct XRaw { u32x4 v[XK == kXBf16 ? 1 : 2]; };
 
 template <int XK> constexpr int kXBytes = XK == kXF32 ? 4 : 2;
 
-// Loads the chunk at element e = row * x_ld + k of x (k a multiple of 8);
-// an offset at or past kOob reads zeros.
-template <int XK>
-__device__ __forceinline__ void load_x(XRaw<XK>& c, __amdgpu_buffer_rsrc_t xr,
-                                       int byte_off, int k_bytes) {
-  c.v[0] = __builtin_bit_cast(
-      u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, byte_off, 0, 0));
-  if constexpr (XK == kXF32)
-    c.v[1] = __builtin_bit_cast(
-        u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, byte_off + 16, 0, 0));
-  if constexpr (XK == kXSiluMul)     // up is K elements after gate
-    c.v[1] = __builtin_bit_cast(
-        u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, byte_off + k_bytes, 0, 0));
+// Where x chunks come from: x itself, and the norm weight for kXRmsNorm.
+struct XSource {
+  __amdgpu_buffer_rsrc_t x, norm_w;
+  int k_bytes;                  // gate to up, in bytes
+};
+
+XSource __device__ __forceinline__ x_source(const LinearArgs& a, int xe) {
+  XSource src;
+  src.x = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.x), 0,
+                                            a.m * a.x_ld * xe, kBufFlags);
+  src.norm_w = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.norm_w), 0, a.norm_w ? a.k * 2 : 0, kBufFlags);
+  src.k_bytes = a.k * 2;
+  return src;
 }
 
-// The bf16 operand of a loaded chunk (zeros stay zeros in every kind).
+// Loads the chunk at byte offset byte_off of x whose k is at byte offset
+// k_off of a [K] bf16 row; offsets at or past kOob read zeros.
 template <int XK>
-__device__ __forceinline__ u32x4 x_operand(const XRaw<XK>& c) {
+__device__ __forceinline__ void load_x(XRaw<XK>& c, const XSource& src,
+                                       int byte_off, int k_off) {
+  c.v[0] = __builtin_bit_cast(
+      u32x4, __builtin_amdgcn_raw_buffer_load_b128(src.x, byte_off, 0, 0));
+  if constexpr (XK == kXF32)
+    c.v[1] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(src.x, byte_off + 16, 0, 0));
+  if constexpr (XK == kXSiluMul)     // up is K elements after gate
+    c.v[1] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(src.x, byte_off + src.k_bytes,
+                                                     0, 0));
+  if constexpr (XK == kXRmsNorm)
+    c.v[1] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(src.norm_w, k_off, 0, 0));
+}
+
+// The bf16 operand of a loaded chunk (zeros stay zeros in every kind; r is
+// the row's 1 / rms for kXRmsNorm, 0 for rows past M).
+template <int XK>
+__device__ __forceinline__ u32x4 x_operand(const XRaw<XK>& c, float r) {
   if constexpr (XK == kXF32)
     return __builtin_bit_cast(
         u32x4, laminar::round8(__builtin_bit_cast(f32x4, c.v[0]),
@@ -133,8 +160,42 @@ __device__ __forceinline__ u32x4 x_operand(const XRaw<XK>& c) {
     return __builtin_bit_cast(
         u32x4, laminar::silu_mul8(__builtin_bit_cast(bf16x8, c.v[0]),
                                   __builtin_bit_cast(bf16x8, c.v[1])));
+  else if constexpr (XK == kXRmsNorm)
+    return __builtin_bit_cast(
+        u32x4, laminar::rms_scale8(__builtin_bit_cast(bf16x8, c.v[0]),
+                                   __builtin_bit_cast(bf16x8, c.v[1]), r));
   else
     return c.v[0];
+}
+
+// 1 / rms of x row `row` (bf16, K per row), summed in laminar_rmsnorm's
+// order: that kernel's thread t sums chunks t, t + 256, ... in one fma
+// chain; here lane l of one wavefront keeps the chains of threads l,
+// l + 64, l + 128 and l + 192, and each is added up by the same butterfly.
+// 0 for rows past M.
+__device__ __forceinline__ float row_rms_inverse(const LinearArgs& a,
+                                                 __amdgpu_buffer_rsrc_t xr,
+                                                 int row, int lane) {
+  const int chunks = a.k >> 3;
+  float p[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < chunks; c0 += 256) {
+    u32x4 v[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int c = c0 + 64 * b + lane;      // thread 64 b + lane
+      v[b] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     xr, c < chunks ? (row * a.k + 8 * c) * 2 : kOob, 0, 0));
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      p[b] = laminar::sumsq8(__builtin_bit_cast(bf16x8, v[b]), p[b]);
+  }
+#pragma unroll
+  for (int w = 0; w < 4; ++w) p[w] = laminar::wave_sum(p[w]);
+  const float r =
+      laminar::rms_inverse(p[0], p[1], p[2], p[3], a.norm_inv_k, a.norm_eps);
+  return row < a.m ? r : 0.f;
 }
 
 template <int MT, int XK>
@@ -160,8 +221,7 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
       const_cast<uint16_t*>(a.w) + size_t(has_tile ? tile : 0) * 16 * a.k, 0,
       has_tile ? a.k * 32 : 0, kBufFlags);
   constexpr int xe = kXBytes<XK>;
-  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<void*>(a.x), 0, a.m * a.x_ld * xe, kBufFlags);
+  const XSource xsrc = x_source(a, xe);
   // lane (q, r16) of matrix-core step j holds row r16, k chunk 4 j + q
   const int w_lane = (q * 16 + r16) * 16;
 
@@ -181,7 +241,7 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
     for (int t = 0; t < MT; ++t) {
       const int xo =
           in ? ((16 * t + x_row) * a.x_ld + kb + 8 * x_chunk) * xe : kOob;
-      load_x<XK>(xb[i][t], xr, xo, a.k * 2);
+      load_x<XK>(xb[i][t], xsrc, xo, in ? (kb + 8 * x_chunk) * 2 : kOob);
     }
   };
 
@@ -190,6 +250,17 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
   for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < kNB; ++i) load(s0 + i, i);
+  // the fused norm (one tile of at most 4 rows): wavefront w finds row w's
+  // 1 / rms while the first weights are on their way
+  float r_row = 0.f;
+  if constexpr (XK == kXRmsNorm) {
+    static_assert(MT == 1, "the fused norm covers one 16-row tile");
+    __shared__ float rr[kNormMaxM];
+    const float r = row_rms_inverse(a, xsrc.x, wave, lane);
+    if (lane == 0) rr[wave] = r;
+    lds_barrier();
+    r_row = x_row < kNormMaxM ? rr[x_row & 3] : 0.f;
+  }
   // Steps past s1 (the last group padded to kNB steps) load zeros and add
   // nothing, so every step runs the same code.
   for (int st = s0; st < s1; st += kNB) {
@@ -198,7 +269,7 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
       const int s = st + i;
       u32x4* buf = xs[s & 1];
 #pragma unroll
-      for (int t = 0; t < MT; ++t) buf[t * 256 + tid] = x_operand<XK>(xb[i][t]);
+      for (int t = 0; t < MT; ++t) buf[t * 256 + tid] = x_operand<XK>(xb[i][t], r_row);
       // The buffer written here was last read two steps ago, before every
       // wavefront passed the previous step's barrier.
       lds_barrier();
@@ -251,8 +322,7 @@ __global__ void __launch_bounds__(256) linear_wave_split_kernel(const LinearArgs
       const_cast<uint16_t*>(a.w) + size_t(tile) * 16 * a.k, 0, a.k * 32,
       kBufFlags);
   constexpr int xe = kXBytes<XK>;
-  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<void*>(a.x), 0, a.m * a.x_ld * xe, kBufFlags);
+  const XSource xsrc = x_source(a, xe);
   const int w_lane = (q * 16 + r16) * 16;
   // this lane loads x row lane / 16, k chunk lane % 16 of each step, which
   // is chunk (lane / 16) * 16 + lane % 16 = lane of the wavefront's LDS
@@ -268,18 +338,29 @@ __global__ void __launch_bounds__(256) linear_wave_split_kernel(const LinearArgs
       wb[i][j] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(wr, wo + 1024 * j, 0,
                                                        /*nt*/ 2));
-    load_x<XK>(xb[i], xr, in ? kb * xe + x_lane : kOob, a.k * 2);
+    load_x<XK>(xb[i], xsrc, in ? kb * xe + x_lane : kOob,
+               in ? (kb + 8 * (lane & 15)) * 2 : kOob);
   };
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   u32x4* xs = xw[wave];
 #pragma unroll
   for (int i = 0; i < kNB; ++i) load(wave + 4 * i, i);
+  // the fused norm: wavefront w finds row w's 1 / rms while the first
+  // weights are on their way; this lane's x row is lane / 16
+  float r_row = 0.f;
+  if constexpr (XK == kXRmsNorm) {
+    __shared__ float rr[kNormMaxM];
+    const float r = row_rms_inverse(a, xsrc.x, wave, lane);
+    if (lane == 0) rr[wave] = r;
+    lds_barrier();
+    r_row = rr[lane >> 4];
+  }
   for (int st = wave; st < steps; st += 4 * kNB) {
 #pragma unroll
     for (int i = 0; i < kNB; ++i) {
       // LDS accesses of one wavefront complete in order: the reads below
       // see this write, and the next step's write follows these reads
-      xs[lane] = x_operand<XK>(xb[i]);
+      xs[lane] = x_operand<XK>(xb[i], r_row);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         // lane (q, r16) of matrix-core step j: x row r16, k chunk 4 j + q
@@ -392,11 +473,15 @@ hipError_t launch(const LinearArgs& a, const SplitPlan& plan, int m,
     return hipGetLastError();
   }
   const dim3 grid((a.n_tiles + 3) / 4, a.splits);
-  switch (launch_tiles(m)) {
-    case 1: hipLaunchKernelGGL((linear_kernel<1, XK>), grid, dim3(256), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((linear_kernel<2, XK>), grid, dim3(256), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL((linear_kernel<4, XK>), grid, dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL((linear_kernel<8, XK>), grid, dim3(256), 0, stream, a); break;
+  if constexpr (XK == kXRmsNorm) {      // at most 4 rows: one tile
+    hipLaunchKernelGGL((linear_kernel<1, XK>), grid, dim3(256), 0, stream, a);
+  } else {
+    switch (launch_tiles(m)) {
+      case 1: hipLaunchKernelGGL((linear_kernel<1, XK>), grid, dim3(256), 0, stream, a); break;
+      case 2: hipLaunchKernelGGL((linear_kernel<2, XK>), grid, dim3(256), 0, stream, a); break;
+      case 4: hipLaunchKernelGGL((linear_kernel<4, XK>), grid, dim3(256), 0, stream, a); break;
+      default: hipLaunchKernelGGL((linear_kernel<8, XK>), grid, dim3(256), 0, stream, a); break;
+    }
   }
   hipError_t e = hipGetLastError();
   if (e == hipSuccess && a.splits > 1) {
@@ -411,14 +496,20 @@ hipError_t launch(const LinearArgs& a, const SplitPlan& plan, int m,
 laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
                            float* y, void* yb, const void* res, int32_t m,
                            int32_t n, int32_t k, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream) {
+                           size_t workspace_bytes, hipStream_t stream,
+                           const void* norm_w = nullptr, float eps = 0.f) {
   if (!x || !w_packed || (!y && !yb)) return LAMINAR_ERR_INVALID_ARG;
-  if (x_kind != kXBf16 && x_kind != kXF32 && x_kind != kXSiluMul)
+  if (x_kind != kXBf16 && x_kind != kXF32 && x_kind != kXSiluMul &&
+      x_kind != kXRmsNorm)
     return LAMINAR_ERR_INVALID_ARG;
   if (misaligned16(x) || misaligned16(w_packed) || misaligned16(y) ||
-      misaligned16(yb) || misaligned16(res))
+      misaligned16(yb) || misaligned16(res) || misaligned16(norm_w))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (x_kind == kXRmsNorm &&
+      (!norm_w || !(eps >= 0.f) || !std::isfinite(eps)))
     return LAMINAR_ERR_INVALID_ARG;
   if (!shape_ok(m, n, k)) return LAMINAR_ERR_UNSUPPORTED;
+  if (x_kind == kXRmsNorm && m > kNormMaxM) return LAMINAR_ERR_UNSUPPORTED;
   // byte offsets into x, padding rows included, stay below 2^31
   const size_t row_bytes = size_t(k) * (x_kind == kXBf16 ? 2 : 4);
   if (size_t(16) * launch_tiles(m) * row_bytes > size_t(kOob))
@@ -426,6 +517,9 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
   LinearArgs a;
   a.x = x;
   a.x_ld = x_kind == kXSiluMul ? 2 * k : k;
+  a.norm_w = static_cast<const uint16_t*>(norm_w);
+  a.norm_inv_k = 1.0f / float(k);
+  a.norm_eps = eps;
   a.w = static_cast<const uint16_t*>(w_packed);
   a.y = y;
   a.yb = static_cast<uint16_t*>(yb);
@@ -450,6 +544,8 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
     e = launch<kXF32>(a, plan, m, stream);
   else if (x_kind == kXSiluMul)
     e = launch<kXSiluMul>(a, plan, m, stream);
+  else if (x_kind == kXRmsNorm)
+    e = launch<kXRmsNorm>(a, plan, m, stream);
   else
     e = launch<kXBf16>(a, plan, m, stream);
   return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
@@ -498,13 +594,26 @@ laminar_status laminar_linear_bf16(const void* x, const void* w_packed,
                      workspace, workspace_bytes, stream);
 }
 
+laminar_status laminar_linear_bf16_rmsnorm(const void* x,
+                                           const void* norm_weight, float eps,
+                                           const void* w_packed, void* y,
+                                           const void* residual, int32_t m,
+                                           int32_t n, int32_t k,
+                                           void* workspace,
+                                           size_t workspace_bytes,
+                                           hipStream_t stream) {
+  if (!y) return LAMINAR_ERR_INVALID_ARG;
+  return linear_impl(x, kXRmsNorm, w_packed, nullptr, y, residual, m, n, k,
+                     workspace, workspace_bytes, stream, norm_weight, eps);
+}
+
 laminar_status laminar_linear_bf16_ex(const void* x, int32_t x_kind,
                                       const void* w_packed, void* y,
                                       const void* residual, int32_t m,
                                       int32_t n, int32_t k, void* workspace,
                                       size_t workspace_bytes,
                                       hipStream_t stream) {
-  if (!y) return LAMINAR_ERR_INVALID_ARG;
+  if (!y || x_kind == kXRmsNorm) return LAMINAR_ERR_INVALID_ARG;
   return linear_impl(x, x_kind, w_packed, nullptr, y, residual, m, n, k,
                      workspace, workspace_bytes, stream);
 }

@@ -465,6 +465,17 @@ def test_linear_errors_before_any_launch():
               0, None) == UNS                   # 128 padded rows x 16 MiB of gate+up
     assert lib.laminar_linear(16, 16, 16, 128, 16, 1 << 23, None, 0,
                               None) == UNS      # 128 rows x 16 MiB of bf16
+    assert ex(16, 3, 16, 16, None, 1, 16, 128, None, 0, None) == INV
+    # the fused norm: weight, eps, at most 4 rows
+    f = ctypes.c_float
+    nm = lib.laminar_linear_bf16_rmsnorm
+    assert nm(16, None, f(1e-6), 16, 16, None, 1, 16, 128, None, 0, None) == INV
+    assert nm(16, 24, f(1e-6), 16, 16, None, 1, 16, 128, None, 0, None) == INV
+    assert nm(16, 16, f(-1.0), 16, 16, None, 1, 16, 128, None, 0, None) == INV
+    assert nm(16, 16, f(float("inf")), 16, 16, None, 1, 16, 128, None, 0,
+              None) == INV
+    assert nm(16, 16, f(1e-6), 16, None, None, 1, 16, 128, None, 0, None) == INV
+    assert nm(16, 16, f(1e-6), 16, 16, None, 5, 16, 128, None, 0, None) == UNS
     # packing: NULL, in place, misaligned, shapes
     assert lib.laminar_linear_pack(None, 16, 16, 128, None) == INV
     assert lib.laminar_linear_pack(16, 16, 16, 128, None) == INV
@@ -618,15 +629,18 @@ def test_linear_kernels_use_no_scratch():
                                       r.stderr)]
     kernels = [(n, sc, o) for n, sc, o in zip(names, scratch, occ)
                if "linear_kernel" in n or "linear_wave_split" in n]
-    # 16, 32, 64 and 128 batch rows and the split over wavefronts, for each
-    # of the three kinds of x
-    assert len(kernels) == 15, kernels
+    # 16, 32, 64 and 128 batch rows and the split over wavefronts for bf16,
+    # fp32 and gate-and-up x; one tile and the split over wavefronts for the
+    # fused norm
+    assert len(kernels) == 17, kernels
     assert all(sc == 0 for _, sc, o in kernels), kernels
     # two wavefronts per SIMD for the workgroup split (the 128-row kernel on
     # gate and up excepted); the split over wavefronts, which runs up to
     # 1024 tiles in one grid, keeps them all resident with four per SIMD
+    # (three with the fused norm's prologue, which only delays a second
+    # round of workgroups past 768 tiles)
     for n, _, o in kernels:
         if "wave_split" in n:
-            assert o >= 4, (n, o)
+            assert o >= (3 if "ILi3E" in n else 4), (n, o)
         elif "ILi8ELi2E" not in n:
             assert o >= 2, (n, o)

@@ -137,3 +137,35 @@ def test_fused_inputs_equal_the_separate_launches(m, n, k):
 
 def bits_t(t):
     return t.view(torch.int16)
+
+
+NORM_SHAPES = [(1, 4608, 3584), (4, 37888, 3584), (3, 48, 640),
+               (2, 7168, 5120), (4, 256, 1024), (2, 3584, 20608)]
+
+
+@pytest.mark.parametrize("m,n,k", NORM_SHAPES)
+def test_fused_norm_equals_rmsnorm_then_linear(m, n, k):
+    """The RMS norm done on load equals laminar_rmsnorm followed by the
+    bf16 call bit for bit (same summation order, same roundings), with and
+    without the residual. Shapes: split over wavefronts (K of 640 to 5120
+    chunks, one to three passes of the row sum), no split (gate+up) and a
+    split over workgroups (161 steps of K)."""
+    from paper_2510_12633_amd.api import SkinnyLinear, rmsnorm
+    _need_gpu()
+    print(f"[gpu-linear-norm] m={m} n={n} k={k}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(11 * m + n + k)
+    w = (torch.randn((n, k), generator=g, device="cuda") / k ** 0.5).to(torch.bfloat16)
+    lin = SkinnyLinear(w)
+    x = (torch.randn((m, k), generator=g, device="cuda") * 5).to(torch.bfloat16)
+    nw = (1 + 0.2 * torch.randn((k,), generator=g, device="cuda")).to(torch.bfloat16)
+    res = torch.randn((m, n), generator=g, device="cuda").to(torch.bfloat16)
+    for eps in (1e-6, 0.0):
+        a = lin.bf16(x, norm_weight=nw, eps=eps)
+        b = lin.bf16(rmsnorm(x, nw, eps=eps))
+        ra, rb = res.clone(), res.clone()
+        lin.bf16(x, out=ra, residual=ra, norm_weight=nw, eps=eps)
+        lin.bf16(rmsnorm(x, nw, eps=eps), out=rb, residual=rb)
+        torch.cuda.synchronize()
+        assert torch.equal(bits_t(a), bits_t(b))
+        assert torch.equal(bits_t(ra), bits_t(rb))
+        assert torch.isfinite(a.float()).all()
