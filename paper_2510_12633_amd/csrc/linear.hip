@@ -16,10 +16,11 @@
 // in LDS, from where every wavefront reads its B operand; so x is fetched
 // once per four tiles instead of once per tile (at M = 64 it would
 // otherwise be four times the weight traffic). Four steps of loads are in
-// flight (two for 65-128 rows, whose x tiles take more registers). All loads are buffer loads whose range check returns zeros: rows
-// of x past M, the steps that pad the last group of NB, and a wavefront
-// past the last tile read zeros without touching memory, so no load is
-// conditional and the compiler keeps exact counts of the loads in flight.
+// flight (two for 65-128 rows, whose x tiles take more registers). All
+// loads are buffer loads whose range check returns zeros: rows of x past
+// M, the steps that pad the last group of NB, and a wavefront past the
+// last tile read zeros without touching memory, so no load is conditional
+// and the compiler keeps exact counts of the loads in flight.
 // When N alone gives too few wavefronts to keep HBM busy, K is split and a
 // second kernel adds the partial sums in a fixed order. For one to four
 // rows and K up to 160 steps, the split stays inside a workgroup instead:
@@ -27,6 +28,13 @@
 // sums are added in LDS. That saves the second launch and the partial sums:
 // 1-4 us of the 13-31 us that the QKV, O and down projections of 7B-32B
 // models take at one row.
+//
+// x can also be what the decode step has at hand rather than the operand
+// itself: the fp32 attention output, SwiGLU's gate and up, or the residual
+// stream with an RMS norm in front (at most 4 rows). The staging makes the
+// bf16 operand from it with the arithmetic of the separate kernel it
+// replaces, and the K split does not depend on it, so the results are
+// those of the separate launches bit for bit.
 
 #include <hip/hip_runtime.h>
 
@@ -44,7 +52,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kStepK = 128;          // k values per pipeline step
 constexpr int kMaxM = 128;
-constexpr int kMaxK = 1 << 24;       // keeps every buffer offset in 31 bits
+constexpr int kMaxK = 1 << 24;       // keeps weight offsets in 31 bits
 // K is split into as many ranges as keep the grid within two workgroups
 // per compute unit (512 on the 256 CUs). Measured over the projections of
 // 7B-32B models at 1-128 rows, a grid past that loses 5-15% (a third
