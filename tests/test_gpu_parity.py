@@ -458,3 +458,26 @@ def test_full_size_config_sampled(idx, cascade):
           f"sampled {seqs}", seqs=seqs)
     del wl
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name,cfg", [
+    ("g7_d128_bf16", custom_config([1, 17, 300, 5000, 40000], 28, 4, 128)),
+    ("g5_d128_fp8", custom_config([2, 33, 999, 7000], 40, 8, 128,
+                                  kv_dtype="fp8_e4m3fn")),
+    ("g16_d64_bf16", custom_config([5, 64, 2500], 32, 2, 64)),
+], ids=lambda v: v if isinstance(v, str) else "")
+def test_extreme_score_ranges(name, cfg):
+    """Scores far outside exp's fp32 range (q scaled by 100: |s| up to a
+    few hundred, a sharply peaked softmax) and all-zero scores (q = 0: the
+    softmax is uniform, out is the mean of V and lse = ln n exactly)."""
+    _need_gpu()
+    wl = make_workload(cfg, seed=23, device="cuda")
+    q0 = wl.q.clone()
+    for factor in (100.0, 0.0):
+        wl.q.copy_((q0.float() * factor).to(wl.q.dtype))
+        ref = decode_attention_from_host(host_arrays(wl), workers=8)
+        out, lse = run_gpu(wl)
+        check((out, lse), ref, f"{name} q x {factor:g}")
+        if factor == 0.0:
+            n = np.repeat(wl.seq_lens.astype(np.float64), cfg.num_q_heads)
+            assert np.allclose(lse.reshape(-1), np.log(n), atol=1e-4, rtol=0)
