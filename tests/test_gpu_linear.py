@@ -140,7 +140,8 @@ def bits_t(t):
 
 
 NORM_SHAPES = [(1, 4608, 3584), (4, 37888, 3584), (3, 48, 640),
-               (2, 7168, 5120), (4, 256, 1024), (2, 3584, 20608)]
+               (2, 7168, 5120), (4, 256, 1024), (2, 3584, 20608),
+               (3, 208, 20608)]
 
 
 @pytest.mark.parametrize("m,n,k", NORM_SHAPES)
@@ -148,8 +149,9 @@ def test_fused_norm_equals_rmsnorm_then_linear(m, n, k):
     """The RMS norm done on load equals laminar_rmsnorm followed by the
     bf16 call bit for bit (same summation order, same roundings), with and
     without the residual. Shapes: split over wavefronts (K of 640 to 5120
-    chunks, one to three passes of the row sum), no split (gate+up) and a
-    split over workgroups (161 steps of K)."""
+    chunks, one to three passes of the row sum), no split (gate+up), a
+    split over workgroups (161 steps of K), and one whose last workgroup
+    has wavefronts past the last tile (13 tiles)."""
     from paper_2510_12633_amd.api import SkinnyLinear, rmsnorm
     _need_gpu()
     print(f"[gpu-linear-norm] m={m} n={n} k={k}", flush=True)
