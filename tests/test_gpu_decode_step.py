@@ -108,3 +108,75 @@ def test_decode_step_argument_errors():
     with pytest.raises(N.LaminarError) as e:
         N.laminar_silu_mul(x, y, 4, 12, s)
     assert e.value.status == N.LAMINAR_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("m", [1, 3, 4])
+def test_fused_decode_step_equals_unfused(m):
+    """A two-layer decoder step (RMS norm, QKV, KV append, paged attention,
+    O with the residual, norm, gate+up, SwiGLU, down with the residual, LM
+    head) run once with every norm, cast and SwiGLU as its own launch and
+    once with all of them made on load in the projections: logits, the
+    residual stream and the KV pages agree bit for bit."""
+    from paper_2510_12633_amd.api import (PagedDecodeAttention, SkinnyLinear,
+                                          kv_append, rmsnorm, silu_mul)
+    _need_gpu()
+    print(f"[gpu-decode-step] fused vs unfused m={m}", flush=True)
+    L, h, hq, hkv, d, inter, vocab = 2, 512, 8, 2, 64, 1024, 2048
+    g = torch.Generator(device="cuda").manual_seed(41 + m)
+    bf = torch.bfloat16
+
+    def lin(k, n):
+        return SkinnyLinear(rand_bf16(g, (n, k), k ** -0.5))
+
+    layers = [(lin(h, (hq + 2 * hkv) * d), lin(hq * d, h), lin(h, 2 * inter),
+               lin(inter, h)) for _ in range(L)]
+    head = lin(h, vocab)
+    norms = (1 + 0.1 * torch.randn((2 * L + 1, h), generator=g,
+                                   device="cuda")).to(bf)
+    ctx = 40
+    pages = -(-(ctx + 1) // 16)
+    kp0 = rand_bf16(g, (m * pages, hkv, 16 * d))
+    vp0 = rand_bf16(g, (m * pages, hkv, 16 * d))
+    table = torch.arange(m * pages, dtype=torch.int32, device="cuda").view(m, pages)
+    lens_host = np.full(m, ctx + 1, np.int32)
+    lens = torch.as_tensor(lens_host, device="cuda")
+    att = PagedDecodeAttention(
+        batch=m, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+        num_pages=m * pages, max_blocks_per_seq=pages, seq_lens_host=lens_host,
+        softmax_scale=d ** -0.5, q_row_stride=(hq + 2 * hkv) * d)
+    out, lse = att.outputs()
+    x0 = rand_bf16(g, (m, h))
+
+    def step(fused):
+        kp, vp = kp0.clone(), vp0.clone()
+        x = x0.clone()
+        for li, (wqkv, wo, wgu, wd) in enumerate(layers):
+            if fused:
+                qkv = wqkv.bf16(x, norm_weight=norms[2 * li])
+            else:
+                qkv = wqkv.bf16(rmsnorm(x, norms[2 * li]))
+            q = qkv[:, :hq * d].view(m, hq, d)
+            k_new = qkv[:, hq * d:(hq + hkv) * d].view(m, hkv, d)
+            v_new = qkv[:, (hq + hkv) * d:].view(m, hkv, d)
+            kv_append(k_new, v_new, table, lens, kp, vp)
+            att(q, kp, vp, table, lens, out, lse)
+            a = out.view(m, hq * d)
+            wo.bf16(a if fused else a.to(bf), out=x, residual=x)
+            if fused:
+                gu = wgu.bf16(x, norm_weight=norms[2 * li + 1])
+                wd.bf16(gu, out=x, residual=x, swiglu=True)
+            else:
+                gu = wgu.bf16(rmsnorm(x, norms[2 * li + 1]))
+                wd.bf16(silu_mul(gu), out=x, residual=x)
+        if fused:
+            logits = head.bf16(x, norm_weight=norms[2 * L])
+        else:
+            logits = head.bf16(rmsnorm(x, norms[2 * L]))
+        torch.cuda.synchronize()
+        return logits, x, kp, vp
+
+    a, b = step(False), step(True)
+    for ta, tb in zip(a, b):
+        assert torch.equal(ta.view(torch.int16), tb.view(torch.int16))
+    assert torch.isfinite(a[0].float()).all()
+    att.close()
