@@ -634,13 +634,14 @@ def test_linear_kernels_use_no_scratch():
     # fused norm
     assert len(kernels) == 17, kernels
     assert all(sc == 0 for _, sc, o in kernels), kernels
-    # two wavefronts per SIMD for the workgroup split (the 128-row kernel on
-    # gate and up excepted); the split over wavefronts, which runs up to
-    # 1024 tiles in one grid, keeps them all resident with four per SIMD
-    # (three with the fused norm's prologue, which only delays a second
-    # round of workgroups past 768 tiles)
+    # two wavefronts per SIMD for the workgroup split up to 64 rows (the
+    # 128-row kernels hold two tiles' accumulators for 128 rows and run one
+    # per SIMD, which measured faster than one tile at two); the split over
+    # wavefronts, which runs up to 1024 tiles in one grid, keeps them all
+    # resident with four per SIMD (three with the fused norm's prologue,
+    # which only delays a second round of workgroups past 768 tiles)
     for n, _, o in kernels:
         if "wave_split" in n:
             assert o >= (3 if "ILi3E" in n else 4), (n, o)
-        elif "ILi8ELi2E" not in n:
+        elif "linear_kernelILi8E" not in n:
             assert o >= 2, (n, o)
