@@ -528,8 +528,12 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             kp = torch.randn((m * pages, hkv, 16 * d), generator=gen,
                              device="cuda", dtype=bf)
             vp = torch.randn_like(kp)
-            table = torch.arange(m * pages, dtype=torch.int32,
-                                 device="cuda").view(m, pages)
+            # pages as a paged allocator hands them out once it has seen
+            # some churn: a random permutation of the pool (with each
+            # trajectory's pages contiguous, every workgroup walks the pool
+            # at the same stride and attention ran ~20% slower)
+            table = torch.randperm(m * pages, generator=gen, device="cuda"
+                                   ).to(torch.int32).view(m, pages)
             lens_host = np.full(m, n_tok, np.int32)
             lens = torch.as_tensor(lens_host, device="cuda")
             att = PagedDecodeAttention(
