@@ -489,7 +489,7 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             modes = ["library"]
             if m <= 128:
                 modes.append("skinny")
-            if m <= (4 if normed else 128):
+            if m <= (8 if normed else 128):
                 modes.append("fused")
             for mode in modes:
                 for p in projs:

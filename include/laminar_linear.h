@@ -116,7 +116,7 @@ laminar_status laminar_linear_bf16_ex(const void* x, int32_t x_kind,
  * equals laminar_rmsnorm followed by laminar_linear_bf16 bit for bit, in
  * one launch. x [M, K] bf16 and norm_weight [K] bf16, 16-byte aligned.
  * Errors: INVALID_ARG (as laminar_linear_bf16, and a NULL or misaligned
- * norm_weight, eps negative or not finite), UNSUPPORTED (also M > 4: the
+ * norm_weight, eps negative or not finite), UNSUPPORTED (also M > 8: the
  * norm of larger batches is one laminar_rmsnorm launch). */
 laminar_status laminar_linear_bf16_rmsnorm(const void* x,
                                            const void* norm_weight, float eps,

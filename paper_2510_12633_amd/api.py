@@ -212,7 +212,7 @@ class SkinnyLinear:
         """bf16(x w^T + residual) [M, N]; out may be the residual itself.
         fp32 x [M, K] is rounded to bf16 on load; with swiglu, x [M, 2K]
         bf16 holds gate then up and the operand is silu(gate) * up; with
-        norm_weight [K] bf16 (at most 4 rows), the operand is
+        norm_weight [K] bf16 (at most 8 rows), the operand is
         rmsnorm(x, norm_weight, eps). Each equals the separate cast,
         laminar_silu_mul or laminar_rmsnorm followed by this call, bit for
         bit, in one launch."""

@@ -31,7 +31,7 @@
 //
 // x can also be what the decode step has at hand rather than the operand
 // itself: the fp32 attention output, SwiGLU's gate and up, or the residual
-// stream with an RMS norm in front (at most 4 rows). The staging makes the
+// stream with an RMS norm in front (at most 8 rows). The staging makes the
 // bf16 operand from it with the arithmetic of the separate kernel it
 // replaces, and the K split does not depend on it, so the results are
 // those of the separate launches bit for bit.
@@ -76,7 +76,8 @@ constexpr int kBufFlags = 0x00020000;
 // load, a SwiGLU's gate and up halves combined on load, or the input of an
 // RMS norm (scaled by the row's 1 / rms and the norm weight on load).
 constexpr int kXBf16 = 0, kXF32 = 1, kXSiluMul = 2, kXRmsNorm = 3;
-constexpr int kNormMaxM = 4;        // rows of the fused norm: one per wavefront
+// rows of the fused norm: one or two per wavefront of the workgroup
+constexpr int kNormMaxM = 8;
 
 struct LinearArgs {
   const void* x;         // [M, x_ld] of the kind the kernel is built for
@@ -273,16 +274,20 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
     for (int t = 0; t < MT; ++t) acc[tt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < kNB; ++i) load(s0 + i, i);
-  // the fused norm (one tile of at most 4 rows): wavefront w finds row w's
-  // 1 / rms while the first weights are on their way
+  // the fused norm (one tile of at most 8 rows): wavefront w finds the
+  // 1 / rms of rows w and w + 4 while the first weights are on their way
   float r_row = 0.f;
   if constexpr (XK == kXRmsNorm) {
     static_assert(MT == 1, "the fused norm covers one 16-row tile");
     __shared__ float rr[kNormMaxM];
-    const float r = row_rms_inverse(a, xsrc.x, wave, lane);
-    if (lane == 0) rr[wave] = r;
+    const float r0 = row_rms_inverse(a, xsrc.x, wave, lane);
+    const float r1 = a.m > 4 ? row_rms_inverse(a, xsrc.x, wave + 4, lane) : 0.f;
+    if (lane == 0) {
+      rr[wave] = r0;
+      rr[wave + 4] = r1;
+    }
     lds_barrier();
-    r_row = x_row < kNormMaxM ? rr[x_row & 3] : 0.f;
+    r_row = x_row < kNormMaxM ? rr[x_row & 7] : 0.f;
   }
   // Steps past s1 (the last group padded to kNB steps) load zeros and add
   // nothing, so every step runs the same code.
@@ -377,8 +382,8 @@ __global__ void __launch_bounds__(256) linear_wave_split_kernel(const LinearArgs
   u32x4* xs = xw[wave];
 #pragma unroll
   for (int i = 0; i < kNB; ++i) load(wave + 4 * i, i);
-  // the fused norm: wavefront w finds row w's 1 / rms while the first
-  // weights are on their way; this lane's x row is lane / 16
+  // the fused norm (at most 4 rows here): wavefront w finds row w's 1 / rms
+  // while the first weights are on their way; this lane's x row is lane / 16
   float r_row = 0.f;
   if constexpr (XK == kXRmsNorm) {
     __shared__ float rr[kNormMaxM];
@@ -507,7 +512,7 @@ hipError_t launch(const LinearArgs& a, const SplitPlan& plan, int m,
   // four wavefronts of tiles_per_wave tiles per workgroup
   const dim3 grid1((a.n_tiles + 3) / 4, a.splits);
   const dim3 grid2((a.n_tiles + 7) / 8, a.splits);
-  if constexpr (XK == kXRmsNorm) {      // at most 4 rows: one tile
+  if constexpr (XK == kXRmsNorm) {      // at most 8 rows: one tile
     hipLaunchKernelGGL((linear_kernel<1, XK>), grid1, dim3(256), 0, stream, a);
   } else {
     switch (launch_tiles(m)) {

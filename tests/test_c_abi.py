@@ -475,7 +475,7 @@ def test_linear_errors_before_any_launch():
     assert nm(16, 16, f(float("inf")), 16, 16, None, 1, 16, 128, None, 0,
               None) == INV
     assert nm(16, 16, f(1e-6), 16, None, None, 1, 16, 128, None, 0, None) == INV
-    assert nm(16, 16, f(1e-6), 16, 16, None, 5, 16, 128, None, 0, None) == UNS
+    assert nm(16, 16, f(1e-6), 16, 16, None, 9, 16, 128, None, 0, None) == UNS
     # packing: NULL, in place, misaligned, shapes
     assert lib.laminar_linear_pack(None, 16, 16, 128, None) == INV
     assert lib.laminar_linear_pack(16, 16, 16, 128, None) == INV

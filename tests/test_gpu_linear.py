@@ -141,7 +141,8 @@ def bits_t(t):
 
 NORM_SHAPES = [(1, 4608, 3584), (4, 37888, 3584), (3, 48, 640),
                (2, 7168, 5120), (4, 256, 1024), (2, 3584, 20608),
-               (3, 208, 20608)]
+               (3, 208, 20608), (5, 4608, 3584), (8, 37888, 3584),
+               (7, 208, 5120)]
 
 
 @pytest.mark.parametrize("m,n,k", NORM_SHAPES)
@@ -150,8 +151,9 @@ def test_fused_norm_equals_rmsnorm_then_linear(m, n, k):
     bf16 call bit for bit (same summation order, same roundings), with and
     without the residual. Shapes: split over wavefronts (K of 640 to 5120
     chunks, one to three passes of the row sum), no split (gate+up), a
-    split over workgroups (161 steps of K), and one whose last workgroup
-    has wavefronts past the last tile (13 tiles)."""
+    split over workgroups (161 steps of K), one whose last workgroup has
+    wavefronts past the last tile (13 tiles), and 5-8 rows (two rows per
+    wavefront)."""
     from paper_2510_12633_amd.api import SkinnyLinear, rmsnorm
     _need_gpu()
     print(f"[gpu-linear-norm] m={m} n={n} k={k}", flush=True)
