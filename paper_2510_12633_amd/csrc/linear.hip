@@ -53,15 +53,17 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kStepK = 128;          // k values per pipeline step
 constexpr int kMaxM = 128;
 constexpr int kMaxK = 1 << 24;       // keeps weight offsets in 31 bits
-// K is split into as many ranges as keep the grid within two workgroups
-// per compute unit (512 on the 256 CUs). Measured over the projections of
-// 7B-32B models at 1-128 rows, a grid past that loses 5-15% (a third
-// workgroup on some CUs finishes last) and a coarser split up to 15% on
-// the long-K shapes.
-constexpr int kMaxGroups = 512;
-// the split inside one workgroup: at most 4 rows and 160 steps of K
+// K is split into as many ranges as keep the grid within one workgroup per
+// compute unit (256). Measured over the QKV, O and down projections of
+// 7B-32B models at 1-128 rows, that beat two per CU by 3-13% at 5-32 rows
+// and by up to 30% from 64 rows on (where the partial sums cost as much
+// HBM traffic as the weights), and a third per CU lost 5-15% more.
+constexpr int kMaxGroups = 256;
+// the split inside one workgroup: at most 4 rows, 160 steps of K and 1024
+// tiles (all workgroups resident at four per CU)
 constexpr int kWaveSplitMaxM = 4;      // rows of the x layout in its LDS
 constexpr int kWaveSplitMaxSteps = 160;
+constexpr int kWaveSplitMaxTiles = 1024;
 // Tiles per wavefront: from 33 rows on, each wavefront takes two tiles, so
 // one staged x step feeds twice the weights (at M = 64 and 128 the QKV, O,
 // down and LM-head products ran 10-17% faster than with one tile; gate+up
@@ -465,10 +467,12 @@ struct SplitPlan {
   bool wave_split;     // K split over the four wavefronts of a workgroup
 };
 
-// The K split over workgroups alone (what the workspace is sized for).
-SplitPlan group_split_plan(int32_t n, int32_t k) {
+// The K split over workgroups alone (what the workspace is sized for); a
+// workgroup covers 4 tiles, or 8 from 33 rows on.
+SplitPlan group_split_plan(int32_t m, int32_t n, int32_t k) {
   const int32_t tiles = n / 16, steps = k / kStepK;
-  int32_t want = kMaxGroups / ((tiles + 3) / 4);
+  const int32_t per_group = launch_tiles(m) >= 4 ? 8 : 4;
+  int32_t want = kMaxGroups / ((tiles + per_group - 1) / per_group);
   if (want < 1) want = 1;
   if (want > steps) want = steps;
   SplitPlan p;
@@ -482,10 +486,10 @@ SplitPlan group_split_plan(int32_t n, int32_t k) {
 // the same order as a bf16 x. A split over workgroups leaves at most 1024
 // tiles, all resident with four workgroups per CU.
 SplitPlan split_plan(int32_t m, int32_t n, int32_t k) {
-  SplitPlan p = group_split_plan(n, k);
+  SplitPlan p = group_split_plan(m, n, k);
   const int32_t steps = k / kStepK;
-  p.wave_split = p.splits > 1 && m <= kWaveSplitMaxM &&
-                 steps <= kWaveSplitMaxSteps;
+  p.wave_split = m <= kWaveSplitMaxM && steps >= 2 &&
+                 steps <= kWaveSplitMaxSteps && n / 16 <= kWaveSplitMaxTiles;
   if (p.wave_split) {
     p.splits = 1;
     p.per = steps;
