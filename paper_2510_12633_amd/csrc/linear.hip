@@ -10,13 +10,14 @@
 // wavefront reads exactly that.
 //
 // A workgroup is four wavefronts on four consecutive tiles (64 output
-// features) over one range of K. Per pipeline step of 128 k, each wavefront
-// loads its tile's 4 KB of weights (non-temporal: they are read once) and
+// features; eight tiles, two per wavefront, from 33 rows on) over one range
+// of K. Per pipeline step of 128 k, each wavefront loads its tiles' 4 KB
+// each of weights (non-temporal: they are read once) and
 // the workgroup loads the batch's x [16 MT rows, 128 k] once and stages it
 // in LDS, from where every wavefront reads its B operand; so x is fetched
 // once per four tiles instead of once per tile (at M = 64 it would
 // otherwise be four times the weight traffic). Four steps of loads are in
-// flight (two for 65-128 rows, whose x tiles take more registers). All
+// flight (two from 33 rows on, whose tiles take more registers). All
 // loads are buffer loads whose range check returns zeros: rows of x past
 // M, the steps that pad the last group of NB, and a wavefront past the
 // last tile read zeros without touching memory, so no load is conditional
@@ -56,7 +57,7 @@ constexpr int kMaxK = 1 << 24;       // keeps weight offsets in 31 bits
 // K is split into as many ranges as keep the grid within one workgroup per
 // compute unit (256). Measured over the QKV, O and down projections of
 // 7B-32B models at 1-128 rows, that beat two per CU by 3-13% at 5-32 rows
-// and by up to 30% from 64 rows on (where the partial sums cost as much
+// and by up to 25% from 64 rows on (where the partial sums cost as much
 // HBM traffic as the weights), and a third per CU lost 5-15% more.
 constexpr int kMaxGroups = 256;
 // the split inside one workgroup: at most 4 rows, 160 steps of K and 1024
