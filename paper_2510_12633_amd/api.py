@@ -218,8 +218,14 @@ class SkinnyLinear:
         bit, in one launch."""
         m = x.shape[0]
         if norm_weight is not None:
-            if x.dtype != torch.bfloat16 or x.shape[1] != self.k or swiglu:
-                raise ValueError(f"x must be bf16 [M, {self.k}] for the norm")
+            if (x.dtype != torch.bfloat16 or x.shape[1] != self.k or swiglu
+                    or not x.is_contiguous()):
+                raise ValueError(f"x must be contiguous bf16 [M, {self.k}] "
+                                 "for the norm")
+            if (norm_weight.dtype != torch.bfloat16
+                    or tuple(norm_weight.shape) != (self.k,)
+                    or not norm_weight.is_contiguous()):
+                raise ValueError(f"norm_weight must be contiguous bf16 [{self.k}]")
             if out is None:
                 out = torch.empty((m, self.n), dtype=torch.bfloat16,
                                   device=x.device)
