@@ -4,7 +4,7 @@
  * and the gated (SwiGLU) activation of each layer.
  *
  * What it computes. The decode-latency curve (the paper's §2.4) and the
- * roofline batch bound B of Algorithm 1 (§6.2) are about whole decode
+ * roofline batch bound B of Algorithm 1 (§5.2) are about whole decode
  * steps of the rollout models (Qwen2.5, §8 "Models"), whose layers put
  * these two operations around the projections of laminar_linear.h and the
  * attention of laminar_decode_attn.h. They move a few kilobytes per token

@@ -8,7 +8,7 @@
  * rows, so they are bound by HBM bandwidth and set the latency floor that
  * makes a small decode batch cost about as much as a larger one (the
  * paper's §2.4) and that the roofline batch bound B of Algorithm 1 refers
- * to (§6.2):
+ * to (§5.2):
  *
  *     y[m, n] = sum_k x[m, k] * w[n, k]      m < M, n < N, k < K
  *

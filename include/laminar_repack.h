@@ -4,7 +4,7 @@
  * moves the released rollouts' trajectories into their destinations.
  *
  * What it computes. Long-tail generation leaves many rollouts running a
- * few long trajectories each. Repacking (the paper's §6.2) picks rollouts
+ * few long trajectories each. Repacking (the paper's §5.2) picks rollouts
  * whose KV usage is falling (below the limit and below the previous check)
  * and that run fewer trajectories than the roofline batch bound, visits
  * them from the least used up, and moves each into the candidate that can
@@ -39,7 +39,7 @@ typedef struct {
 } laminar_rollout_state;
 
 /*
- * Consolidation plan (Algorithm 1, §6.2). Writes the (source, destination)
+ * Consolidation plan (Algorithm 1, §5.2). Writes the (source, destination)
  * rollout indices of every planned move, in decision order, to src_out /
  * dst_out (host, capacity >= num_rollouts) and their number to *num_pairs.
  * O(candidates^2) time, host only.
@@ -100,7 +100,7 @@ typedef struct {
 } laminar_model_shape;
 
 /*
- * Roofline batch bound B of Algorithm 1 (§6.2): the smallest decode batch
+ * Roofline batch bound B of Algorithm 1 (§5.2): the smallest decode batch
  * at which one step's projections (per layer QKV, O, gate+up and down, and
  * the LM head; a [M, K] x [K, N] product does 2 M N K flops and moves
  * weight_bytes N K + act_bytes M (K + N) bytes) are compute-bound at peak

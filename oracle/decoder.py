@@ -5,7 +5,7 @@ CPU-baseline leg may import or call this module. The GPU library never does,
 and this module imports nothing from the GPU path.
 
 What it computes. The decode-latency curve (§2.4) and the roofline batch
-bound B of Algorithm 1 (§6.2) concern whole decode steps of the paper's
+bound B of Algorithm 1 (§5.2) concern whole decode steps of the paper's
 rollout models (Qwen2.5, §8 "Models"). Besides the projections and the
 attention, each layer of those models runs an RMS pre-norm before its
 attention and its MLP, and a gated (SwiGLU) activation inside the MLP. The

@@ -7,7 +7,7 @@ and this module imports nothing from the GPU path.
 What it computes. Every decode step runs each layer's projections (QKV, O,
 gate and up, down) and the LM head over the batch's current tokens; they
 set the step's latency floor that the roofline batch bound B refers to
-(§6.2) and the flat part of the latency-versus-batch figure (§2.4). The
+(§5.2) and the flat part of the latency-versus-batch figure (§2.4). The
 operation is the plain product
 
     y[m, n] = sum_k x[m, k] * w[n, k]

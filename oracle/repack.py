@@ -5,7 +5,7 @@ TEST INFRASTRUCTURE. Only the tests, the package smoke check and the bench's
 CPU-baseline leg may import or call this module. The GPU library never does,
 and this module imports nothing from the GPU path.
 
-Consolidation (Algorithm 1, §6.2 "Repacking algorithm"). Each rollout
+Consolidation (Algorithm 1, §5.2 "Repacking algorithm"). Each rollout
 replica r reports its KV-cache usage r.used, its usage at the previous check
 r.prev and its running trajectory count r.reqs. With the usage limit c_max
 and the roofline batch bound b_max:

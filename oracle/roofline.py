@@ -7,7 +7,7 @@ and this module imports nothing from the GPU path.
 What it computes. Repacking bounds a destination's decode batch by B, the
 largest batch decoded at nearly the latency of a small one: under the
 roofline model it is where decoding turns from memory-bound to
-compute-bound (§6.2, where B enters Algorithm 1; §2.4 and its
+compute-bound (§5.2, where B enters Algorithm 1; §2.4 and its
 latency-versus-batch figure show the flat, memory-bound part). One decode
 step of a dense decoder (L layers, hidden size h, Hq query and Hkv KV heads
 of size D, gated MLP of width I, vocabulary V; weights of wb bytes,

@@ -2,7 +2,7 @@
 // page assignment of a migration, and the roofline batch bound B that the
 // plan takes as input. Pure host C++: no HIP call.
 //
-// The plan follows the paper's Algorithm 1 (§6.2): candidates are the
+// The plan follows the paper's Algorithm 1 (§5.2): candidates are the
 // rollouts whose KV usage is falling and below the limit and that run fewer
 // trajectories than the roofline batch bound; they are visited from the
 // least used up, and each that has neither been emptied nor received

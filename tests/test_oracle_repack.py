@@ -117,3 +117,60 @@ def test_migration_preserves_attention():
     a2["block_table"] = np.where(bt >= 0, dst[np.maximum(bt, 0)], -1).astype(np.int32)
     out1, lse1 = decode_attention_from_host(a2)
     assert np.array_equal(out0, out1) and np.array_equal(lse0, lse1)
+
+
+def _literal_algorithm1(used, prev, reqs, c_max, b_max):
+    """Algorithm 1 of §5.2 taken word for word: a visited candidate is
+    skipped only when it was emptied; CanFit counts the destination's own
+    usage, what is planned into it and the source's own usage."""
+    s_list = sorted(candidates(used, prev, reqs, c_max, b_max),
+                    key=lambda r: used[r])
+    plan, emptied = [], set()
+    for s in s_list:
+        if s in emptied:
+            continue
+        into = lambda d: [x for x, dd in plan if dd == d]
+        fits = [d for d in s_list if d != s and d not in emptied
+                and used[d] + sum(used[x] for x in into(d)) + used[s] <= c_max
+                and reqs[d] + sum(reqs[x] for x in into(d)) + reqs[s] <= b_max]
+        if not fits:
+            continue
+        best = max(used[d] + sum(used[x] for x in into(d)) for d in fits)
+        plan.append((s, next(d for d in fits
+                             if used[d] + sum(used[x] for x in into(d)) == best)))
+        emptied.add(s)
+    return plan
+
+
+def _final_loads(plan, used, reqs):
+    """Usage and trajectory count of every rollout once the plan has run:
+    a moved rollout takes everything it holds, including what was planned
+    into it, to its destination."""
+    dest = dict(plan)
+
+    def home(r):
+        while r in dest:
+            r = dest[r]
+        return r
+    c = [0] * len(used)
+    n = [0] * len(used)
+    for r in range(len(used)):
+        c[home(r)] += used[r]
+        n[home(r)] += reqs[r]
+    return c, n
+
+
+def test_literal_loop_breaks_the_limit_on_the_worked_example():
+    """Why the oracle keeps a destination in place: on the worked example
+    the literal loop also moves rollout 1, which already received 0 and 2,
+    into rollout 5, and rollout 5 then ends above C_max (105 > 100 pages)
+    and above B (22 > 16 trajectories). The oracle's plan stays within
+    both bounds."""
+    used, prev, reqs, c_max, b_max, want = load_example()
+    literal = _literal_algorithm1(used, prev, reqs, c_max, b_max)
+    assert literal == want + [(1, 5)]
+    c, n = _final_loads(literal, used, reqs)
+    assert c[5] == 105 > c_max and n[5] == 22 > b_max
+    c, n = _final_loads(want, used, reqs)
+    for _, d in want:
+        assert c[d] <= c_max and n[d] <= b_max
