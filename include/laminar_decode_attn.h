@@ -111,7 +111,8 @@ typedef struct laminar_plan laminar_plan;   /* opaque, host-owned */
  * The plan is reusable by every layer of the step. On success *out owns a
  * new plan (free with laminar_plan_destroy); on error *out is NULL.
  * Errors: INVALID_ARG (NULL pointers, negative or inconsistent sizes, a
- * length needing more than max_blocks_per_seq pages, fp8 without scales,
+ * length needing more than max_blocks_per_seq pages, fp8 without scales
+ * or with scale pointers that are not 4-byte aligned,
  * an input_row_stride below num_q_heads x head_dim or not a multiple of 8),
  * UNSUPPORTED (head_dim not 64/128, group size above 16, page_size != 16).
  */
@@ -178,8 +179,10 @@ laminar_status laminar_plan_bind_workspace(laminar_plan* plan, void* workspace,
  * entries outside [0, num_pages) contribute nothing. Calls with one plan
  * share its workspace (partial results and the counter that hands out the
  * dynamic tail items) and must therefore be ordered on one stream.
- * Errors: INVALID_ARG (NULL plan or pointer), WORKSPACE (no workspace
- * bound), HIP.
+ * Errors, checked in this order before any launch: INVALID_ARG (NULL
+ * plan; with batch > 0, a NULL pointer, or q, k_pages, v_pages or out not
+ * 16-byte aligned, or block_table, seq_lens or lse not 4-byte aligned),
+ * WORKSPACE (no workspace bound), HIP.
  */
 laminar_status laminar_decode_attn(const laminar_plan* plan, const void* q,
                                    const void* k_pages, const void* v_pages,
@@ -203,7 +206,9 @@ laminar_status laminar_decode_attn_partial(const laminar_plan* plan,
 /*
  * The second half: merge the partial (out, lse) of each split trajectory into
  * out and lse. Must follow laminar_decode_attn_partial with the same plan on
- * the same stream. Errors: INVALID_ARG, WORKSPACE, HIP.
+ * the same stream. Errors: INVALID_ARG (NULL plan; with batch > 0, out
+ * NULL or not 16-byte aligned, lse NULL or not 4-byte aligned), WORKSPACE,
+ * HIP.
  */
 laminar_status laminar_decode_attn_merge(const laminar_plan* plan, float* out,
                                          float* lse, hipStream_t stream);

@@ -909,11 +909,24 @@ laminar_status run_merge(const laminar_plan* p, const DecodeArgs& a,
   return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
 }
 
+bool aligned(const void* ptr, uintptr_t bytes) {
+  return ptr && (reinterpret_cast<uintptr_t>(ptr) & (bytes - 1)) == 0;
+}
+
+// Pointers of a call: present, and aligned as the kernels access them (q
+// rows, K/V tiles and out rows move in 16-byte vectors; the block table,
+// lengths and lse in 4-byte words).
 bool inputs_ok(const laminar_plan* p, const void* q, const void* k_pages,
                const void* v_pages, const int32_t* block_table,
                const int32_t* seq_lens, const float* out, const float* lse) {
   if (p->desc.batch == 0) return true;
-  return q && k_pages && v_pages && block_table && seq_lens && out && lse;
+  return aligned(q, 16) && aligned(k_pages, 16) && aligned(v_pages, 16) &&
+         aligned(block_table, 4) && aligned(seq_lens, 4) &&
+         aligned(out, 16) && aligned(lse, 4);
+}
+
+bool outputs_ok(const laminar_plan* p, const float* out, const float* lse) {
+  return p->desc.batch == 0 || (aligned(out, 16) && aligned(lse, 4));
 }
 
 // Pinned staging for plan uploads. The tables are copied into one of a few
@@ -1025,10 +1038,11 @@ laminar_status laminar_decode_attn_partial(const laminar_plan* plan,
                                            const int32_t* block_table,
                                            const int32_t* seq_lens, float* out,
                                            float* lse, hipStream_t stream) {
-  laminar_status st = check_bound(plan);
-  if (st != LAMINAR_OK) return st;
+  if (!plan) return LAMINAR_ERR_INVALID_ARG;
   if (!inputs_ok(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse))
     return LAMINAR_ERR_INVALID_ARG;
+  laminar_status st = check_bound(plan);
+  if (st != LAMINAR_OK) return st;
   const DecodeArgs a = make_args(plan, q, k_pages, v_pages, block_table,
                                  seq_lens, out, lse);
   return run_partial(plan, a, stream);
@@ -1036,9 +1050,10 @@ laminar_status laminar_decode_attn_partial(const laminar_plan* plan,
 
 laminar_status laminar_decode_attn_merge(const laminar_plan* plan, float* out,
                                          float* lse, hipStream_t stream) {
+  if (!plan) return LAMINAR_ERR_INVALID_ARG;
+  if (!outputs_ok(plan, out, lse)) return LAMINAR_ERR_INVALID_ARG;
   laminar_status st = check_bound(plan);
   if (st != LAMINAR_OK) return st;
-  if (plan->desc.batch > 0 && (!out || !lse)) return LAMINAR_ERR_INVALID_ARG;
   const DecodeArgs a = make_args(plan, nullptr, nullptr, nullptr, nullptr,
                                  nullptr, out, lse);
   return run_merge(plan, a, stream);
@@ -1049,10 +1064,11 @@ laminar_status laminar_decode_attn(const laminar_plan* plan, const void* q,
                                    const int32_t* block_table,
                                    const int32_t* seq_lens, float* out,
                                    float* lse, hipStream_t stream) {
-  laminar_status st = check_bound(plan);
-  if (st != LAMINAR_OK) return st;
+  if (!plan) return LAMINAR_ERR_INVALID_ARG;
   if (!inputs_ok(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse))
     return LAMINAR_ERR_INVALID_ARG;
+  laminar_status st = check_bound(plan);
+  if (st != LAMINAR_OK) return st;
   const DecodeArgs a = make_args(plan, q, k_pages, v_pages, block_table,
                                  seq_lens, out, lse);
   st = run_partial(plan, a, stream);

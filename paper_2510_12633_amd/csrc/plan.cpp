@@ -40,7 +40,10 @@ laminar_status validate(const laminar_attn_desc* d, const int32_t* lens,
     return LAMINAR_ERR_INVALID_ARG;
   if (d->kv_dtype != LAMINAR_KV_BF16 && d->kv_dtype != LAMINAR_KV_FP8_E4M3FN)
     return LAMINAR_ERR_INVALID_ARG;
-  if (d->kv_dtype == LAMINAR_KV_FP8_E4M3FN && (!d->k_scale || !d->v_scale))
+  if (d->kv_dtype == LAMINAR_KV_FP8_E4M3FN &&
+      (!d->k_scale || !d->v_scale ||
+       (reinterpret_cast<uintptr_t>(d->k_scale) & 3) != 0 ||
+       (reinterpret_cast<uintptr_t>(d->v_scale) & 3) != 0))
     return LAMINAR_ERR_INVALID_ARG;
   if (d->page_size != 16) return LAMINAR_ERR_UNSUPPORTED;
   if (d->head_dim != 64 && d->head_dim != 128) return LAMINAR_ERR_UNSUPPORTED;

@@ -645,3 +645,38 @@ def test_linear_kernels_use_no_scratch():
             assert o >= (3 if "ILi3E" in n else 4), (n, o)
         elif "linear_kernelILi8E" not in n:
             assert o >= 2, (n, o)
+
+
+def test_attention_pointer_alignment_checked_before_any_launch():
+    """q, k_pages, v_pages and out are read or written in 16-byte vectors,
+    block_table, seq_lens and lse in 4-byte words: a pointer off that
+    alignment (a sliced tensor) is refused before the workspace is even
+    looked at, so an unbound plan still reports INVALID_ARG for it."""
+    lib = N.lib()
+    p = N.laminar_plan_create(desc(batch=2), np.array([40, 9], np.int32), 256)
+    try:
+        good = [4096] * 7           # q, k, v, table, lens, out, lse
+        for fn in (lib.laminar_decode_attn, lib.laminar_decode_attn_partial):
+            assert fn(p, *good, None) == N.LAMINAR_ERR_WORKSPACE
+            for i, need in enumerate((16, 16, 16, 4, 4, 16, 4)):
+                for off in {need // 2, 2} - {0}:
+                    if off % need == 0:
+                        continue
+                    bad = list(good)
+                    bad[i] += off
+                    assert fn(p, *bad, None) == N.LAMINAR_ERR_INVALID_ARG, (i, off)
+                bad = list(good)
+                bad[i] = None
+                assert fn(p, *bad, None) == N.LAMINAR_ERR_INVALID_ARG, i
+        merge = lib.laminar_decode_attn_merge
+        assert merge(p, 4096, 4096, None) == N.LAMINAR_ERR_WORKSPACE
+        assert merge(p, 4096 + 8, 4096, None) == N.LAMINAR_ERR_INVALID_ARG
+        assert merge(p, 4096, 4096 + 2, None) == N.LAMINAR_ERR_INVALID_ARG
+        assert merge(p, None, 4096, None) == N.LAMINAR_ERR_INVALID_ARG
+    finally:
+        N.laminar_plan_destroy(p)
+    # fp8 scales are read as 4-byte words
+    with pytest.raises(N.LaminarError) as e:
+        N.laminar_plan_create(desc(kv=N.LAMINAR_KV_FP8_E4M3FN, k_scale=4098,
+                                   v_scale=4096), np.array([40, 9, 1, 1], np.int32), 256)
+    assert e.value.status == N.LAMINAR_ERR_INVALID_ARG
