@@ -72,6 +72,10 @@ def parse_args(argv=None):
                    help="skip the repack planner and page-migration timing")
     p.add_argument("--fixed-plan", action="store_true",
                    help="plan once outside the timed loop (kernel-only steps)")
+    p.add_argument("--no-per-config", action="store_true",
+                   help="measure the named workload only, not every one")
+    p.add_argument("--no-parity", action="store_true",
+                   help="skip the oracle check of every trajectory")
     return p.parse_args(argv)
 
 
@@ -186,34 +190,48 @@ def cpu_baseline(wl, budget_s: float):
 
 
 def calibrate(torch, N, nbytes=4 << 30, iters=10):
-    """Achievable HBM read and copy bandwidth (GB/s) on this device."""
+    """Achievable HBM bandwidth (GB/s) on this device: a sequential read, a
+    copy (bytes read + written), and gathers of random 4 KiB tiles (the
+    size of one bf16 (page, kv-head) KV tile at head_dim 128) and of random
+    64-byte tiles through an index list, each tile of the buffer once in a
+    random order (tile bytes only; the index list adds 4 bytes per tile)."""
     buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     buf.fill_(1)
     sink = torch.empty(N.laminar_hbm_read_sink_floats(), dtype=torch.float32,
                        device="cuda")
     s = torch.cuda.current_stream()
     h = s.cuda_stream
-    for _ in range(2):
-        N.laminar_hbm_read(buf, nbytes, sink, h)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(s)
-    for _ in range(iters):
-        N.laminar_hbm_read(buf, nbytes, sink, h)
-    e1.record(s)
-    torch.cuda.synchronize()
-    read = nbytes * iters / (e0.elapsed_time(e1) / 1e3) / 1e9
+
+    def timed(fn, moved):
+        for _ in range(2):
+            fn()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(iters):
+            fn()
+        e1.record(s)
+        torch.cuda.synchronize()
+        return moved * iters / (e0.elapsed_time(e1) / 1e3) / 1e9
+
+    res = {"read": timed(lambda: N.laminar_hbm_read(buf, nbytes, sink, h),
+                         nbytes)}
     half = nbytes // 2
     dst, src = buf[:half], buf[half:]
-    N.laminar_hbm_copy(dst, src, half, h)
-    e0.record(s)
-    for _ in range(iters):
-        N.laminar_hbm_copy(dst, src, half, h)
-    e1.record(s)
-    torch.cuda.synchronize()
-    copy = 2 * half * iters / (e0.elapsed_time(e1) / 1e3) / 1e9
+    res["copy"] = timed(lambda: N.laminar_hbm_copy(dst, src, half, h), 2 * half)
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    for tile, span in ((4096, nbytes), (64, 1 << 30)):
+        n = span // tile
+        idx = torch.randperm(n, generator=gen, device="cuda").to(torch.int32)
+        gsink = torch.empty(N.laminar_hbm_gather_sink_words(n, tile),
+                            dtype=torch.int32, device="cuda")
+        key = "gather_4KiB" if tile == 4096 else "gather_64B"
+        res[key] = timed(lambda: N.laminar_hbm_gather(buf, nbytes, tile, idx,
+                                                      n, gsink, h), span)
+        del idx, gsink
     del buf
     torch.cuda.empty_cache()
-    return read, copy
+    return res
 
 
 def measure_append(torch, wl, steps=24):
@@ -613,29 +631,57 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             "peak_bw": peak_bw, "curves": curves}
 
 
-def main(argv=None):
-    args = parse_args(argv)
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not "
-              "supported (the decode-attention path needs no collectives and "
-              "shards by trajectory or kv-head with no exchange).",
-              file=sys.stderr)
-        sys.exit(2)
+ALL_WORKLOADS = ("tiny", "7b_pre_repack", "post_repack", "32b_fp8",
+                 "agentic_mix", "32b_fp8_tp4", "agentic_mix_tp8")
 
+
+def host_workers() -> int:
+    return max(1, len(os.sched_getaffinity(0)))
+
+
+def oracle_parity(wl, out, lse):
+    """Every trajectory and head of the GPU's out and lse against the fp64
+    oracle on the host; returns the errors and the oracle's wall time."""
     import numpy as np
-    import torch
+    from threadpoolctl import threadpool_limits
 
-    from paper_2510_12633_amd import _native as N
+    from oracle import decode_attention_from_host
+    from workloads import host_arrays
+
+    o = out.cpu().numpy()
+    l = lse.cpu().numpy()
+    arrays = host_arrays(wl)
+    cores = host_workers()
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        ro, rl = decode_attention_from_host(arrays, workers=cores)
+        dt = time.perf_counter() - t0
+    del arrays
+    fin = np.isfinite(rl)
+    ok_shape = (np.isfinite(o).all() and np.isfinite(l[fin]).all()
+                and np.array_equal(np.isneginf(l), np.isneginf(rl)))
+    return {"max_abs_err_out": float(np.abs(o - ro).max()) if o.size else 0.0,
+            "max_abs_err_lse": float(np.abs(l[fin] - rl[fin]).max())
+            if fin.any() else 0.0,
+            "all_rows_written_and_finite": bool(ok_shape),
+            "trajectories_checked": int(wl.batch),
+            "oracle_s": round(dt, 3), "oracle_threads": cores}
+
+
+def measure(torch, N, name, steps, warm, args, seed=None):
+    """One workload: `steps` timed whole steps (host plan, table upload,
+    partial kernel, merge) after `warm` untimed ones, the two kernels timed
+    with HIP events on the launch stream; then the same with one plan
+    reused (one layer's call of a decode step whose plan all layers share);
+    then one more whole step into NaN-filled outputs, checked against the
+    oracle over every trajectory. Returns (entry, extras)."""
+    import numpy as np
+
     from paper_2510_12633_amd.api import KV_DTYPES, num_cus
-    from workloads import get_config, make_workload
+    from workloads import get_config, make_workload, prefix_groups
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    N.lib()      # fail loudly if the HIP library is not built
-
-    cfg = get_config(args.workload)
-    wl = make_workload(cfg, seed=args.seed, device="cuda")
+    cfg = get_config(name)
+    wl = make_workload(cfg, seed=seed, device="cuda")
     dev_lens = torch.as_tensor(wl.seq_lens, device="cuda")
     bt = torch.as_tensor(wl.block_table, device="cuda")
     cus = num_cus()
@@ -660,8 +706,6 @@ def main(argv=None):
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
-    # Workspace sized for this batch's plan; reused every step.
-    from workloads import prefix_groups
     group_of, group_pages = prefix_groups(wl)
     use_cascade = group_of is not None and args.cascade != "off"
 
@@ -680,15 +724,14 @@ def main(argv=None):
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
     N.laminar_plan_bind_workspace(plan0, ws, ws_bytes, sh)
 
-    steps, warm = args.steps, args.warmup
     ev = [(torch.cuda.Event(enable_timing=True),
            torch.cuda.Event(enable_timing=True),
            torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     plan_ns, bind_ns = [], []
     live = [plan0]
 
-    def one_step(i, events=None):
-        if args.fixed_plan:
+    def one_step(i, events=None, fixed=False):
+        if fixed:
             plan = plan0
         else:
             t0 = time.perf_counter_ns()
@@ -709,60 +752,147 @@ def main(argv=None):
         if events:
             events[2].record(stream)
 
-    for i in range(warm):
-        one_step(i)
-    torch.cuda.synchronize()
-    # plans are destroyed only after the stream has passed their uploads
-    for p in live[1:]:
-        N.laminar_plan_destroy(p)
-    live[1:] = []
-    plan_ns.clear()
-    bind_ns.clear()
+    def release():
+        # plans are destroyed only after the stream has passed their uploads
+        torch.cuda.synchronize()
+        for p in live[1:]:
+            N.laminar_plan_destroy(p)
+        live[1:] = []
 
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t_start.record(stream)
-    for i in range(steps):
-        one_step(warm + i, ev[i])
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    for p in live[1:]:
-        N.laminar_plan_destroy(p)
-    live[1:] = []
+    def timed_loop(fixed):
+        for i in range(warm):
+            one_step(i, fixed=fixed)
+        release()
+        plan_ns.clear()
+        bind_ns.clear()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        t_start.record(stream)
+        for i in range(steps):
+            one_step(warm + i, ev[i], fixed=fixed)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        ms_step = t_start.elapsed_time(t_end) / steps
+        k1 = [a.elapsed_time(b) for a, b, _ in ev]
+        k2 = [b.elapsed_time(c) for _, b, c in ev]
+        return ms_step, k1, k2, wall
 
-    ms_total = t_start.elapsed_time(t_end)
-    ms_step = ms_total / steps
-    k1 = [a.elapsed_time(b) for a, b, _ in ev]
-    k2 = [b.elapsed_time(c) for _, b, c in ev]
+    if args.fixed_plan:
+        ms_step, k1, k2, wall = timed_loop(True)
+        ms_layer = ms_step
+    else:
+        ms_step, k1, k2, wall = timed_loop(False)
+        plan_host = list(plan_ns)
+        bind_host = list(bind_ns)
+        release()
+        ms_layer = timed_loop(True)[0]
+        plan_ns[:], bind_ns[:] = plan_host, bind_host
+    release()
+
     k1_ms = sum(k1) / len(k1)
     k2_ms = sum(k2) / len(k2)
     step_s = ms_step / 1e3
-
-    value = kv_bytes / step_s / 1e12
     achieved = alg_bytes / (k1_ms / 1e3) / 1e9
     traffic, traffic_src = read_traffic(cfg.name)
+
+    # one more whole step into NaN-filled outputs, against the oracle
+    out.fill_(float("nan"))
+    lse.fill_(float("nan"))
+    one_step(0)
+    release()
+    parity = None if args.no_parity else oracle_parity(wl, out, lse)
+
+    entry = {
+        "workload": cfg.name,
+        "batch": wl.batch,
+        "heads_q_kv": [cfg.num_q_heads, cfg.num_kv_heads],
+        "kv_dtype": cfg.kv_dtype,
+        "context_tokens": int(wl.seq_lens.sum()),
+        "kv_bytes": kv_bytes,
+        "algorithmic_bytes": alg_bytes,
+        "decode_items_us": round(k1_ms * 1e3, 2),
+        "decode_merge_us": round(k2_ms * 1e3, 2),
+        "step_ms": round(ms_step, 5),
+        "layer_call_ms": round(ms_layer, 5),
+        "kv_TBps_step": round(kv_bytes / step_s / 1e12, 4),
+        "frac_hbm_peak_step": round(kv_bytes / step_s / 1e9 / HBM_PEAK_GBPS, 4),
+        "frac_hbm_peak_layer_call": round(kv_bytes / (ms_layer / 1e3) / 1e9
+                                          / HBM_PEAK_GBPS, 4),
+        "frac_hbm_peak_kernel": round(achieved / HBM_PEAK_GBPS, 4),
+        "tokens_per_s": round(wl.batch / step_s, 1),
+        "traffic_over_algorithmic": (round(traffic / alg_bytes, 4)
+                                     if traffic else None),
+        "work_items": n_items,
+        "cascade_prefix": use_cascade,
+    }
+    if parity:
+        entry.update(parity)
+    extras = {
+        "wl": wl, "cfg": cfg, "ms_step": ms_step, "k1": k1, "k2": k2,
+        "k1_ms": k1_ms, "k2_ms": k2_ms, "wall": wall, "achieved": achieved,
+        "traffic": traffic, "traffic_src": traffic_src, "plan_ns": plan_ns,
+        "bind_ns": bind_ns, "ppi": ppi, "waves": waves, "n_items": n_items,
+        "n_merges": n_merges, "use_cascade": use_cascade, "rot": rot,
+        "parity": parity, "ms_layer": ms_layer,
+    }
+    N.laminar_plan_destroy(plan0)
+    del ws, out, lse
+    return entry, extras
+
+
+def main(argv=None):
+    args = parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not "
+              "supported (the decode-attention path needs no collectives and "
+              "shards by trajectory or kv-head with no exchange).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2510_12633_amd import _native as N
+    from workloads import get_config
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    N.lib()      # fail loudly if the HIP library is not built
+
+    cfg = get_config(args.workload)
+    print(f"[bench] {cfg.name}: {args.steps} steps after {args.warmup}",
+          file=sys.stderr, flush=True)
+    entry, x = measure(torch, N, cfg.name, args.steps, args.warmup, args,
+                       seed=args.seed)
+    wl = x["wl"]
+    k1, k2 = x["k1"], x["k2"]
+    ms_step = x["ms_step"]
+    step_s = ms_step / 1e3
+    kv_bytes = wl.kv_bytes_unique()
+    alg_bytes = wl.algorithmic_bytes()
+    value = kv_bytes / step_s / 1e12
     roofline = {
         "bound": "hbm",
         "kernel": PARTIAL_KERNEL,
-        "achieved": round(achieved, 1),
+        "achieved": round(x["achieved"], 1),
         "peak": HBM_PEAK_GBPS,
         "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBPS, 4),
-        "traffic": traffic,
+        "frac": round(x["achieved"] / HBM_PEAK_GBPS, 4),
+        "traffic": x["traffic"],
         "algorithmic_bytes_per_launch": alg_bytes,
-        "avg_launch_ms": round(k1_ms, 5),
+        "avg_launch_ms": round(x["k1_ms"], 5),
     }
-
+    plan_ns, bind_ns = x["plan_ns"], x["bind_ns"]
     result = {
         "metric": METRIC,
         "value": round(value, 4),
         "unit": "TB/s",
         "n_gpus": 1,
-        "steps": steps,
-        "warmup": warm,
+        "steps": args.steps,
+        "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
         "higher_is_better": True,
         "scaling": "weak",
@@ -778,45 +908,76 @@ def main(argv=None):
             "kv_dtype": cfg.kv_dtype,
             "context_tokens": int(wl.seq_lens.sum()),
             "seed": wl.seed,
-            "pages_per_item": ppi,
-            "waves_per_item": waves,
-            "work_items": n_items,
-            "merged_units": n_merges,
+            "pages_per_item": x["ppi"],
+            "waves_per_item": x["waves"],
+            "work_items": x["n_items"],
+            "merged_units": x["n_merges"],
             "plan_every_step": not args.fixed_plan,
-            "cascade_prefix": use_cascade,
-            "kv_pool_copies_rotated": rot.n if rot else 1,
+            "cascade_prefix": x["use_cascade"],
+            "kv_pool_copies_rotated": x["rot"].n if x["rot"] else 1,
         },
         "frac_hbm_peak": round(value * 1e3 / HBM_PEAK_GBPS, 4),
         "tokens_per_s": round(wl.batch / step_s, 1),
         "context_tokens_per_s": round(float(wl.seq_lens.sum()) / step_s, 1),
         "kv_bytes": kv_bytes,
         "algorithmic_bytes": alg_bytes,
-        "kernel_ms": {"decode_items": round(k1_ms, 5),
-                      "decode_merge": round(k2_ms, 5)},
+        "kernel_ms": {"decode_items": round(x["k1_ms"], 5),
+                      "decode_merge": round(x["k2_ms"], 5)},
         "kernel_ms_median": {"decode_items": round(sorted(k1)[len(k1) // 2], 5),
                              "decode_merge": round(sorted(k2)[len(k2) // 2], 5)},
+        # one layer's call with the step's plan already uploaded (every
+        # layer of a decode step shares one plan)
+        "layer_call_ms": round(x["ms_layer"], 5),
         "plan_host_ms": round(sum(plan_ns) / max(len(plan_ns), 1) / 1e6, 5)
         if plan_ns else None,
         # bind: tables into a pinned staging slot and the upload launch; it
         # waits when the host is eight steps ahead of the GPU
         "bind_host_ms": round(sum(bind_ns) / max(len(bind_ns), 1) / 1e6, 5)
         if bind_ns else None,
-        "wall_s_timed": round(wall, 4),
+        "wall_s_timed": round(x["wall"], 4),
         "roofline": roofline,
     }
-    if traffic_src == "stale":
+    if x["parity"]:
+        result["max_abs_err_out"] = x["parity"]["max_abs_err_out"]
+        result["max_abs_err_lse"] = x["parity"]["max_abs_err_lse"]
+        result["parity"] = x["parity"]
+    if x["traffic_src"] == "stale":
         result["roofline"]["traffic_note"] = "counters predate the current kernel"
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget_s)
+    del x, wl
+    torch.cuda.empty_cache()
     if not args.no_calibrate:
-        rd, cp = calibrate(torch, N)
-        result["hbm_calibration_GBps"] = {"read": round(rd, 1),
-                                          "copy": round(cp, 1)}
-        result["frac_of_calibrated_read"] = round(value * 1e3 / rd, 4)
-    if not args.no_append:
-        app = measure_append(torch, wl)
-        if app is not None:
-            result["kv_append"] = app
-    if not args.no_repack:
-        result["repack"] = measure_repack(torch, N, wl)
+        cal = calibrate(torch, N)
+        result["hbm_calibration_GBps"] = {k: round(v, 1) for k, v in cal.items()}
+        result["frac_of_calibrated_read"] = round(value * 1e3 / cal["read"], 4)
+        result["frac_of_calibrated_gather"] = round(
+            roofline["achieved"] / cal["gather_4KiB"], 4)
+    if not args.no_per_config:
+        rows = []
+        for name in ALL_WORKLOADS:
+            if name == cfg.name:
+                rows.append(entry)
+                continue
+            print(f"[bench] per-config {name}", file=sys.stderr, flush=True)
+            e, xx = measure(torch, N, name, args.steps, args.warmup, args)
+            del xx
+            torch.cuda.empty_cache()
+            rows.append(e)
+        result["per_config"] = rows
+    else:
+        result["per_config"] = [entry]
+    if not (args.no_append and args.no_repack):
+        from workloads import make_workload
+        wl = make_workload(cfg, seed=args.seed, device="cuda")
+        if not args.no_append:
+            app = measure_append(torch, wl)
+            if app is not None:
+                result["kv_append"] = app
+        if not args.no_repack:
+            result["repack"] = measure_repack(torch, N, wl)
+        del wl
+        torch.cuda.empty_cache()
     if not args.no_projections:
         result["projections"] = measure_projections(torch, N)
     if args.latency_curve:
@@ -826,9 +987,6 @@ def main(argv=None):
         if args.curve_contexts:
             kw["contexts"] = tuple(int(x) for x in args.curve_contexts.split(","))
         result["latency_curve"] = latency_curve(torch, N, **kw)
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget_s)
-    N.laminar_plan_destroy(plan0)
     print(json.dumps(result), flush=True)
 
 

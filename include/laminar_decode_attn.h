@@ -257,6 +257,23 @@ const char* laminar_status_string(laminar_status status);
  * Errors: INVALID_ARG, HIP.
  */
 int32_t laminar_hbm_read_sink_floats(void);
+/*
+ * laminar_hbm_gather reads n_idx tiles of tile_bytes (a power of two, at
+ * least 16) from src, tile t of the list being bytes
+ * [idx[t] * tile_bytes, (idx[t] + 1) * tile_bytes) of the src_bytes-long
+ * buffer (indices outside it are clamped to its last tile), the way the
+ * attention kernel gathers 4 KiB KV tiles through a block table. src is
+ * 16-byte aligned; idx (int32, n_idx entries) and sink are device memory.
+ * sink receives laminar_hbm_gather_sink_words(n_idx, tile_bytes) uint32
+ * partial sums, one per workgroup; their sum mod 2^32 is the sum of every
+ * 32-bit word read, a checksum the caller can recompute. n_idx == 0 does
+ * nothing. Errors: INVALID_ARG, HIP.
+ */
+int32_t laminar_hbm_gather_sink_words(int64_t n_idx, size_t tile_bytes);
+laminar_status laminar_hbm_gather(const void* src, size_t src_bytes,
+                                  size_t tile_bytes, const int32_t* idx,
+                                  int64_t n_idx, uint32_t* sink,
+                                  hipStream_t stream);
 laminar_status laminar_hbm_read(const void* src, size_t bytes, float* sink,
                                 hipStream_t stream);
 laminar_status laminar_hbm_copy(void* dst, const void* src, size_t bytes,

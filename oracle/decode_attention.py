@@ -149,9 +149,20 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, *,
         for b in range(b_count):
             one(b)
     else:
-        with ThreadPoolExecutor(max_workers=workers) as ex:
+        # one BLAS thread per worker: a full BLAS pool in every worker
+        # oversubscribes the host and runs ~40x slower
+        with _blas_threads(1), ThreadPoolExecutor(max_workers=workers) as ex:
             list(ex.map(one, range(b_count)))
     return out, lse
+
+
+def _blas_threads(n: int):
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:          # no control over BLAS threads: run as is
+        from contextlib import nullcontext
+        return nullcontext()
+    return threadpool_limits(n)
 
 
 def decode_attention_from_host(arrays: dict, workers: int = 1):

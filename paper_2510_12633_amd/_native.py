@@ -103,6 +103,9 @@ _SIGNATURES = {
     "laminar_hbm_read_sink_floats": (c_int32, []),
     "laminar_hbm_read": (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p]),
     "laminar_hbm_copy": (c_int32, [c_void_p, c_void_p, c_size_t, c_void_p]),
+    "laminar_hbm_gather_sink_words": (c_int32, [ctypes.c_int64, c_size_t]),
+    "laminar_hbm_gather": (c_int32, [c_void_p, c_size_t, c_size_t, c_void_p,
+                                     ctypes.c_int64, c_void_p, c_void_p]),
     "laminar_kv_append": (c_int32, [POINTER(LaminarAttnDesc)] + [c_void_p] * 8
                           + [c_void_p]),
     "laminar_repack_plan": (c_int32, [POINTER(LaminarRolloutState), c_int32,
@@ -447,3 +450,14 @@ def laminar_hbm_read(src, nbytes: int, sink, stream):
 def laminar_hbm_copy(dst, src, nbytes: int, stream):
     _check(lib().laminar_hbm_copy(_ptr(dst), _ptr(src), int(nbytes),
                                   _ptr(stream)), "laminar_hbm_copy")
+
+
+def laminar_hbm_gather_sink_words(n_idx: int, tile_bytes: int) -> int:
+    return int(lib().laminar_hbm_gather_sink_words(int(n_idx), int(tile_bytes)))
+
+
+def laminar_hbm_gather(src, src_bytes: int, tile_bytes: int, idx, n_idx: int,
+                       sink, stream):
+    _check(lib().laminar_hbm_gather(_ptr(src), int(src_bytes), int(tile_bytes),
+                                    _ptr(idx), int(n_idx), _ptr(sink),
+                                    _ptr(stream)), "laminar_hbm_gather")

@@ -79,13 +79,19 @@ class PagedDecodeAttention:
                                       self.workspace_bytes,
                                       _stream_handle(stream))
 
-    def outputs(self):
+    def outputs(self, fill: Optional[float] = float("nan")):
+        """New out [B, Hq, D] and lse [B, Hq] fp32 buffers, filled with
+        ``fill`` (NaN by default, so that a row the kernels leave unwritten
+        shows up instead of passing as a stale value; None leaves them
+        uninitialised)."""
         d = self.desc
-        out = torch.empty((d.batch, d.num_q_heads, d.head_dim),
-                          dtype=torch.float32, device=self.device)
-        lse = torch.empty((d.batch, d.num_q_heads), dtype=torch.float32,
-                          device=self.device)
-        return out, lse
+        shape_o = (d.batch, d.num_q_heads, d.head_dim)
+        shape_l = (d.batch, d.num_q_heads)
+        if fill is None:
+            return (torch.empty(shape_o, dtype=torch.float32, device=self.device),
+                    torch.empty(shape_l, dtype=torch.float32, device=self.device))
+        return (torch.full(shape_o, fill, dtype=torch.float32, device=self.device),
+                torch.full(shape_l, fill, dtype=torch.float32, device=self.device))
 
     def __call__(self, q, k_pages, v_pages, block_table, seq_lens, out=None,
                  lse=None, stream=None):

@@ -24,7 +24,9 @@
 //    several items (or whose shared prefix was decoded by a cascade item);
 //    one workgroup per record when records have few slots, one per
 //    (record, head) with the slots reduced in parallel otherwise.
-//  * hbm_read / hbm_copy: bandwidth calibration.
+//
+// The C-ABI entry points that validate a call and launch these kernels are
+// in attn_entry.hip; this file holds the kernels and their launchers only.
 
 #include <hip/hip_runtime.h>
 
@@ -33,6 +35,7 @@
 #include <cstring>
 #include <mutex>
 
+#include "attn_internal.h"
 #include "laminar_decode_attn.h"
 #include "plan_internal.h"
 
@@ -750,64 +753,11 @@ __global__ void __launch_bounds__(256) decode_merge_heads(const DecodeArgs a) {
   }
 }
 
-// Calibration kernels: each workgroup streams one contiguous chunk with
-// non-temporal 16-byte accesses, eight in flight per lane.
-constexpr int kCalibChunk16 = 4096;          // 64 KiB per workgroup
-constexpr int kReadSinkFloats = 1 << 16;     // workgroups per read pass
-
-__global__ void __launch_bounds__(256)
-hbm_read_kernel(const u32x4* __restrict__ src, size_t n16, float* sink) {
-  uint32_t acc = 0;
-  for (size_t blk = blockIdx.x; blk * kCalibChunk16 < n16; blk += gridDim.x) {
-    const size_t beg = blk * kCalibChunk16;
-    const size_t end = beg + kCalibChunk16 < n16 ? beg + kCalibChunk16 : n16;
-    size_t i = beg + threadIdx.x;
-    for (; i + 7 * 256 < end; i += 8 * 256) {
-      u32x4 v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * 256]);
-#pragma unroll
-      for (int u = 0; u < 8; ++u) acc ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
-    }
-    for (; i < end; i += 256) acc ^= src[i][0];
-  }
-  // Every lane's value feeds the workgroup sum, so no load is dead code.
-  float s = wave_sum(__uint_as_float(acc & 0x007FFFFFu));
-  __shared__ float red[4];
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) sink[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
-}
-
-__global__ void __launch_bounds__(256)
-hbm_copy_kernel(u32x4* __restrict__ dst, const u32x4* __restrict__ src,
-                size_t n16) {
-  for (size_t blk = blockIdx.x; blk * kCalibChunk16 < n16; blk += gridDim.x) {
-    const size_t beg = blk * kCalibChunk16;
-    const size_t end = beg + kCalibChunk16 < n16 ? beg + kCalibChunk16 : n16;
-    size_t i = beg + threadIdx.x;
-    for (; i + 7 * 256 < end; i += 8 * 256) {
-      u32x4 v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * 256]);
-#pragma unroll
-      for (int u = 0; u < 8; ++u) __builtin_nontemporal_store(v[u], &dst[i + u * 256]);
-    }
-    for (; i < end; i += 256) dst[i] = src[i];
-  }
-}
-
-unsigned calib_grid(size_t n16) {
-  const size_t chunks = (n16 + kCalibChunk16 - 1) / kCalibChunk16;
-  return unsigned(chunks < size_t(kReadSinkFloats) ? (chunks ? chunks : 1)
-                                                   : size_t(kReadSinkFloats));
-}
-
 template <int D, bool FP8, bool CASCADE>
-hipError_t launch_items(const laminar_plan* p, const DecodeArgs& a,
+hipError_t launch_items(const laminar_plan& p, const DecodeArgs& a,
                         hipStream_t stream) {
-  const dim3 grid(p->num_items);
-  switch (p->waves) {
+  const dim3 grid(p.num_items);
+  switch (p.waves) {
     case 1:
       hipLaunchKernelGGL((decode_items<D, FP8, 1, CASCADE>), grid, dim3(64), 0,
                          stream, a);
@@ -825,41 +775,40 @@ hipError_t launch_items(const laminar_plan* p, const DecodeArgs& a,
 }
 
 template <int D, bool FP8>
-hipError_t launch_partial(const laminar_plan* p, const DecodeArgs& a,
+hipError_t launch_partial(const laminar_plan& p, const DecodeArgs& a,
                           hipStream_t stream) {
-  return p->num_cascade_units > 0 ? launch_items<D, FP8, true>(p, a, stream)
-                                  : launch_items<D, FP8, false>(p, a, stream);
+  return p.num_cascade_units > 0 ? launch_items<D, FP8, true>(p, a, stream)
+                                 : launch_items<D, FP8, false>(p, a, stream);
 }
 
-DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
-                     const void* v_pages, const int32_t* block_table,
-                     const int32_t* seq_lens, float* out, float* lse) {
+DecodeArgs make_args(const laminar_plan& p,
+                     const laminar_detail::AttnCall& c) {
   DecodeArgs a;
-  const laminar_attn_desc& d = p->desc;
-  char* ws = static_cast<char*>(p->ws);
-  a.q = static_cast<const uint16_t*>(q);
+  const laminar_attn_desc& d = p.desc;
+  char* ws = static_cast<char*>(c.ws);
+  a.q = static_cast<const uint16_t*>(c.q);
   a.q_stride = d.input_row_stride ? d.input_row_stride
                                   : int64_t(d.num_q_heads) * d.head_dim;
-  a.k_pages = static_cast<const uint8_t*>(k_pages);
-  a.v_pages = static_cast<const uint8_t*>(v_pages);
+  a.k_pages = static_cast<const uint8_t*>(c.k_pages);
+  a.v_pages = static_cast<const uint8_t*>(c.v_pages);
   a.k_scale = d.k_scale;
   a.v_scale = d.v_scale;
-  a.block_table = block_table;
-  a.seq_lens = seq_lens;
-  a.out = out;
-  a.lse = lse;
-  a.items = reinterpret_cast<const int4*>(ws + p->off_items);
-  a.merges = reinterpret_cast<const int4*>(ws + p->off_merges);
-  a.tail_counter = reinterpret_cast<int*>(ws + p->off_tail);
-  a.num_main = p->num_main;
-  a.num_tail = p->num_items - p->num_main;
-  a.cunits = reinterpret_cast<const int4*>(ws + p->off_cunits);
-  a.cmembers = reinterpret_cast<const int2*>(ws + p->off_cmembers);
-  a.lse_part = reinterpret_cast<float*>(ws + p->off_lse);
-  a.o_part = reinterpret_cast<float*>(ws + p->off_o);
+  a.block_table = c.block_table;
+  a.seq_lens = c.seq_lens;
+  a.out = c.out;
+  a.lse = c.lse;
+  a.items = reinterpret_cast<const int4*>(ws + p.off_items);
+  a.merges = reinterpret_cast<const int4*>(ws + p.off_merges);
+  a.tail_counter = reinterpret_cast<int*>(ws + p.off_tail);
+  a.num_main = p.num_main;
+  a.num_tail = p.num_items - p.num_main;
+  a.cunits = reinterpret_cast<const int4*>(ws + p.off_cunits);
+  a.cmembers = reinterpret_cast<const int2*>(ws + p.off_cmembers);
+  a.lse_part = reinterpret_cast<float*>(ws + p.off_lse);
+  a.o_part = reinterpret_cast<float*>(ws + p.off_o);
   a.hq = d.num_q_heads;
   a.hkv = d.num_kv_heads;
-  a.group = p->group;
+  a.group = p.group;
   a.max_blocks = d.max_blocks_per_seq;
   a.num_pages = d.num_pages;
   a.scale_log2 = d.softmax_scale * kLog2e;
@@ -867,19 +816,17 @@ DecodeArgs make_args(const laminar_plan* p, const void* q, const void* k_pages,
   return a;
 }
 
-laminar_status check_bound(const laminar_plan* p) {
-  if (!p) return LAMINAR_ERR_INVALID_ARG;
-  if (p->ws_bytes > 0 && (!p->ws || p->ws_size < p->ws_bytes))
-    return LAMINAR_ERR_WORKSPACE;
-  return LAMINAR_OK;
-}
+}  // namespace
 
-laminar_status run_partial(const laminar_plan* p, const DecodeArgs& a,
-                           hipStream_t stream) {
-  if (p->num_items == 0) return LAMINAR_OK;
-  const bool fp8 = p->desc.kv_dtype == LAMINAR_KV_FP8_E4M3FN;
+namespace laminar_detail {
+
+laminar_status enqueue_partial(const laminar_plan& p, const AttnCall& c,
+                               hipStream_t stream) {
+  if (p.num_items == 0) return LAMINAR_OK;
+  const DecodeArgs a = make_args(p, c);
+  const bool fp8 = p.desc.kv_dtype == LAMINAR_KV_FP8_E4M3FN;
   hipError_t e;
-  if (p->desc.head_dim == 128)
+  if (p.desc.head_dim == 128)
     e = fp8 ? launch_partial<128, true>(p, a, stream)
             : launch_partial<128, false>(p, a, stream);
   else
@@ -888,14 +835,15 @@ laminar_status run_partial(const laminar_plan* p, const DecodeArgs& a,
   return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
 }
 
-laminar_status run_merge(const laminar_plan* p, const DecodeArgs& a,
-                         hipStream_t stream) {
-  if (p->num_merges == 0) return LAMINAR_OK;
+laminar_status enqueue_merge(const laminar_plan& p, const AttnCall& c,
+                             hipStream_t stream) {
+  if (p.num_merges == 0) return LAMINAR_OK;
+  const DecodeArgs a = make_args(p, c);
   // Few slots per record: a workgroup per record; many: a workgroup per
   // (record, head) reducing slots in parallel.
-  const bool rows = p->num_slots <= kRowsMergeMaxMeanSlots * p->num_merges;
-  const dim3 grid = rows ? dim3(p->num_merges) : dim3(p->num_merges, p->group);
-  if (p->desc.head_dim == 128) {
+  const bool rows = p.num_slots <= kRowsMergeMaxMeanSlots * p.num_merges;
+  const dim3 grid = rows ? dim3(p.num_merges) : dim3(p.num_merges, p.group);
+  if (p.desc.head_dim == 128) {
     if (rows)
       hipLaunchKernelGGL((decode_merge_rows<128>), grid, dim3(256), 0, stream, a);
     else
@@ -909,197 +857,4 @@ laminar_status run_merge(const laminar_plan* p, const DecodeArgs& a,
   return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
 }
 
-bool aligned(const void* ptr, uintptr_t bytes) {
-  return ptr && (reinterpret_cast<uintptr_t>(ptr) & (bytes - 1)) == 0;
-}
-
-// Pointers of a call: present, and aligned as the kernels access them (q
-// rows, K/V tiles and out rows move in 16-byte vectors; the block table,
-// lengths and lse in 4-byte words).
-bool inputs_ok(const laminar_plan* p, const void* q, const void* k_pages,
-               const void* v_pages, const int32_t* block_table,
-               const int32_t* seq_lens, const float* out, const float* lse) {
-  if (p->desc.batch == 0) return true;
-  return aligned(q, 16) && aligned(k_pages, 16) && aligned(v_pages, 16) &&
-         aligned(block_table, 4) && aligned(seq_lens, 4) &&
-         aligned(out, 16) && aligned(lse, 4);
-}
-
-bool outputs_ok(const laminar_plan* p, const float* out, const float* lse) {
-  return p->desc.batch == 0 || (aligned(out, 16) && aligned(lse, 4));
-}
-
-// Pinned staging for plan uploads. The tables are copied into one of a few
-// pinned, device-mapped host slots, and a small kernel on the caller's
-// stream copies them into the workspace. Compared with a DMA copy this keeps
-// the upload on the same hardware queue as the attention kernels (no
-// cross-engine hand-offs around it), blocks the host only when the oldest of
-// eight uploads has not yet run (the host is then eight steps ahead), and
-// lets the caller free the plan as soon as bind returns. One ring per
-// device, created on first use and kept for the life of the process; a slot
-// is reused only after the event recorded behind its last upload completed.
-// Copies n16 16-byte words from device-mapped pinned host memory.
-__global__ void __launch_bounds__(256)
-upload_kernel(u32x4* __restrict__ dst, const u32x4* __restrict__ src,
-              size_t n16) {
-  const size_t stride = size_t(gridDim.x) * blockDim.x;
-  for (size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n16;
-       i += stride)
-    dst[i] = src[i];
-}
-
-struct StagingRing {
-  static constexpr int kSlots = 8;
-  static constexpr size_t kSlotBytes = size_t(1) << 20;
-  char* host = nullptr;
-  char* dev_view = nullptr;    // device address of `host`
-  hipEvent_t done[kSlots] = {};
-  bool pending[kSlots] = {};
-  int next = 0;
-};
-
-constexpr int kMaxDevices = 64;
-std::mutex g_ring_mutex;
-StagingRing g_rings[kMaxDevices];
-
-laminar_status upload_tables(void* dst, const void* src, size_t bytes,
-                             hipStream_t stream) {
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess) return LAMINAR_ERR_HIP;
-  if (bytes > StagingRing::kSlotBytes || dev < 0 || dev >= kMaxDevices) {
-    // Too large for a slot: copy straight from the plan and wait for it, so
-    // the plan can still be freed when bind returns.
-    hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
-  }
-  std::lock_guard<std::mutex> lock(g_ring_mutex);
-  StagingRing& ring = g_rings[dev];
-  if (!ring.host) {
-    void* h = nullptr;
-    void* hd = nullptr;
-    if (hipHostMalloc(&h, StagingRing::kSlots * StagingRing::kSlotBytes,
-                      hipHostMallocMapped | hipHostMallocPortable) !=
-            hipSuccess ||
-        hipHostGetDevicePointer(&hd, h, 0) != hipSuccess)
-      return LAMINAR_ERR_HIP;
-    ring.dev_view = static_cast<char*>(hd);
-    for (int i = 0; i < StagingRing::kSlots; ++i)
-      if (hipEventCreateWithFlags(&ring.done[i], hipEventDisableTiming) !=
-          hipSuccess)
-        return LAMINAR_ERR_HIP;
-    ring.host = static_cast<char*>(h);
-  }
-  const int slot = ring.next;
-  ring.next = (slot + 1) % StagingRing::kSlots;
-  if (ring.pending[slot] && hipEventSynchronize(ring.done[slot]) != hipSuccess)
-    return LAMINAR_ERR_HIP;
-  char* stage = ring.host + size_t(slot) * StagingRing::kSlotBytes;
-  std::memcpy(stage, src, bytes);
-  const size_t n16 = (bytes + 15) / 16;    // tables are 256-byte multiples
-  const unsigned blocks = unsigned(n16 < 64 * 256 ? (n16 + 255) / 256 : 64);
-  hipLaunchKernelGGL(upload_kernel, dim3(blocks), dim3(256), 0, stream,
-                     static_cast<u32x4*>(dst),
-                     reinterpret_cast<const u32x4*>(
-                         ring.dev_view + size_t(slot) * StagingRing::kSlotBytes),
-                     n16);
-  if (hipGetLastError() != hipSuccess ||
-      hipEventRecord(ring.done[slot], stream) != hipSuccess)
-    return LAMINAR_ERR_HIP;
-  ring.pending[slot] = true;
-  return LAMINAR_OK;
-}
-
-}  // namespace
-
-extern "C" {
-
-laminar_status laminar_plan_bind_workspace(laminar_plan* plan, void* workspace,
-                                           size_t bytes, hipStream_t stream) {
-  if (!plan) return LAMINAR_ERR_INVALID_ARG;
-  if (plan->ws_bytes == 0) {
-    plan->ws = workspace;
-    plan->ws_size = bytes;
-    return LAMINAR_OK;
-  }
-  if (!workspace || bytes < plan->ws_bytes ||
-      (reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
-    return LAMINAR_ERR_WORKSPACE;
-  plan->ws = workspace;
-  plan->ws_size = bytes;
-  const size_t table_bytes = plan->tables.size() * sizeof(int32_t);
-  if (table_bytes == 0) return LAMINAR_OK;
-  return upload_tables(workspace, plan->tables.data(), table_bytes, stream);
-}
-
-laminar_status laminar_decode_attn_partial(const laminar_plan* plan,
-                                           const void* q, const void* k_pages,
-                                           const void* v_pages,
-                                           const int32_t* block_table,
-                                           const int32_t* seq_lens, float* out,
-                                           float* lse, hipStream_t stream) {
-  if (!plan) return LAMINAR_ERR_INVALID_ARG;
-  if (!inputs_ok(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse))
-    return LAMINAR_ERR_INVALID_ARG;
-  laminar_status st = check_bound(plan);
-  if (st != LAMINAR_OK) return st;
-  const DecodeArgs a = make_args(plan, q, k_pages, v_pages, block_table,
-                                 seq_lens, out, lse);
-  return run_partial(plan, a, stream);
-}
-
-laminar_status laminar_decode_attn_merge(const laminar_plan* plan, float* out,
-                                         float* lse, hipStream_t stream) {
-  if (!plan) return LAMINAR_ERR_INVALID_ARG;
-  if (!outputs_ok(plan, out, lse)) return LAMINAR_ERR_INVALID_ARG;
-  laminar_status st = check_bound(plan);
-  if (st != LAMINAR_OK) return st;
-  const DecodeArgs a = make_args(plan, nullptr, nullptr, nullptr, nullptr,
-                                 nullptr, out, lse);
-  return run_merge(plan, a, stream);
-}
-
-laminar_status laminar_decode_attn(const laminar_plan* plan, const void* q,
-                                   const void* k_pages, const void* v_pages,
-                                   const int32_t* block_table,
-                                   const int32_t* seq_lens, float* out,
-                                   float* lse, hipStream_t stream) {
-  if (!plan) return LAMINAR_ERR_INVALID_ARG;
-  if (!inputs_ok(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse))
-    return LAMINAR_ERR_INVALID_ARG;
-  laminar_status st = check_bound(plan);
-  if (st != LAMINAR_OK) return st;
-  const DecodeArgs a = make_args(plan, q, k_pages, v_pages, block_table,
-                                 seq_lens, out, lse);
-  st = run_partial(plan, a, stream);
-  if (st != LAMINAR_OK) return st;
-  return run_merge(plan, a, stream);
-}
-
-int32_t laminar_hbm_read_sink_floats(void) { return kReadSinkFloats; }
-
-laminar_status laminar_hbm_read(const void* src, size_t bytes, float* sink,
-                                hipStream_t stream) {
-  if (!src || !sink || (bytes & 15) ||
-      (reinterpret_cast<uintptr_t>(src) & 15))
-    return LAMINAR_ERR_INVALID_ARG;
-  hipLaunchKernelGGL(hbm_read_kernel, dim3(calib_grid(bytes / 16)), dim3(256),
-                     0, stream, static_cast<const u32x4*>(src), bytes / 16,
-                     sink);
-  return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
-}
-
-laminar_status laminar_hbm_copy(void* dst, const void* src, size_t bytes,
-                                hipStream_t stream) {
-  if (!src || !dst || (bytes & 15) ||
-      (reinterpret_cast<uintptr_t>(src) & 15) ||
-      (reinterpret_cast<uintptr_t>(dst) & 15))
-    return LAMINAR_ERR_INVALID_ARG;
-  if (bytes == 0) return LAMINAR_OK;
-  hipLaunchKernelGGL(hbm_copy_kernel, dim3(calib_grid(bytes / 16)), dim3(256),
-                     0, stream, static_cast<u32x4*>(dst),
-                     static_cast<const u32x4*>(src), bytes / 16);
-  return hipGetLastError() == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
-}
-
-}  // extern "C"
+}  // namespace laminar_detail

@@ -264,6 +264,20 @@ def test_call_errors_before_any_launch():
     assert lib.laminar_hbm_read(None, 16, None, None) == N.LAMINAR_ERR_INVALID_ARG
     assert lib.laminar_hbm_read(16, 17, 16, None) == N.LAMINAR_ERR_INVALID_ARG
     assert lib.laminar_hbm_copy(16, 16, 8, None) == N.LAMINAR_ERR_INVALID_ARG
+    gather = lib.laminar_hbm_gather
+    assert gather(None, 4096, 4096, 16, 1, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert gather(8, 4096, 4096, 16, 1, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert gather(16, 4096, 48, 16, 1, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert gather(16, 4096, 8, 16, 1, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert gather(16, 2048, 4096, 16, 1, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert gather(16, 4096, 4096, None, 1, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert gather(16, 4096, 4096, 18, 1, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert gather(16, 4096, 4096, 16, -1, 16, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert gather(16, 4096, 4096, None, 0, None, None) == N.LAMINAR_OK
+    assert lib.laminar_hbm_gather_sink_words(0, 4096) == 0
+    assert lib.laminar_hbm_gather_sink_words(1, 4096) == 1
+    assert lib.laminar_hbm_gather_sink_words(1 << 20, 4096) == \
+        N.laminar_hbm_read_sink_floats()
     assert lib.laminar_plan_num_items(None) == -1
     assert lib.laminar_plan_workspace_bytes(None) == 0
 

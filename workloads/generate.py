@@ -299,10 +299,11 @@ def host_arrays(wl: Workload, seqs: Optional[Sequence[int]] = None) -> dict:
     remap[used] = np.arange(used.shape[0])
     new_table = np.where(table >= 0, remap[np.maximum(table, 0)], -1)
     sel = torch.as_tensor(used, device=wl.k_pages.device)
+    pick = (lambda t: t) if seqs is None else (lambda t: t.index_select(0, sel))
     out = dict(
         q=_bits(wl.q[torch.as_tensor(idx, device=wl.q.device)]),
-        k_pages=_bits(wl.k_pages.index_select(0, sel)),
-        v_pages=_bits(wl.v_pages.index_select(0, sel)),
+        k_pages=_bits(pick(wl.k_pages)),
+        v_pages=_bits(pick(wl.v_pages)),
         block_table=new_table.astype(np.int32),
         seq_lens=lens.astype(np.int32),
         k_scale=None, v_scale=None,
@@ -310,6 +311,6 @@ def host_arrays(wl: Workload, seqs: Optional[Sequence[int]] = None) -> dict:
         num_kv_heads=wl.cfg.num_kv_heads, softmax_scale=wl.softmax_scale,
     )
     if wl.k_scale is not None:
-        out["k_scale"] = wl.k_scale.index_select(0, sel).cpu().numpy()
-        out["v_scale"] = wl.v_scale.index_select(0, sel).cpu().numpy()
+        out["k_scale"] = pick(wl.k_scale).cpu().numpy()
+        out["v_scale"] = pick(wl.v_scale).cpu().numpy()
     return out
