@@ -213,6 +213,32 @@ laminar_status laminar_decode_attn_partial(const laminar_plan* plan,
 laminar_status laminar_decode_attn_merge(const laminar_plan* plan, float* out,
                                          float* lse, hipStream_t stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * same computation as laminar_decode_attn, with the library's own static
+ * workspace of LAMINAR_STATIC_WORKSPACE_BYTES per GPU (a device array that
+ * the GPU holds from the library's load until the process ends) in place
+ * of a workspace bound to the plan. The plan need not be bound. Each call
+ * copies the plan's tables from its host memory into that workspace with
+ * hipMemcpyAsync on `stream` and launches the same kernels; it calls no
+ * allocation routine. Keep the plan alive until the stream has passed the
+ * call. Every call on one GPU shares that GPU's workspace, which keeps the
+ * last call's contents: calls that overlap on one GPU (other streams, other
+ * threads) race and give wrong results; order them on one stream.
+ * Errors, before any launch: INVALID_ARG (as laminar_decode_attn),
+ * WORKSPACE (the plan needs more than LAMINAR_STATIC_WORKSPACE_BYTES, see
+ * laminar_plan_workspace_bytes), HIP (the workspace's device address could
+ * not be found, or a copy or launch failed).
+ */
+#define LAMINAR_STATIC_WORKSPACE_BYTES (64u << 20)
+laminar_status laminar_decode_attn_static(const laminar_plan* plan,
+                                          const void* q, const void* k_pages,
+                                          const void* v_pages,
+                                          const int32_t* block_table,
+                                          const int32_t* seq_lens, float* out,
+                                          float* lse, hipStream_t stream);
+
 /* Plan introspection (host only). Items are listed in launch order
  * (longest first, one workgroup each). Each item is 4 int32:
  * (b * num_kv_heads + kvh, first page, end page, partial slot or -1 when the

@@ -85,6 +85,8 @@ _SIGNATURES = {
                                     + [c_void_p]),
     "laminar_decode_attn_merge": (c_int32, [c_void_p, c_void_p, c_void_p,
                                             c_void_p]),
+    "laminar_decode_attn_static": (c_int32, [c_void_p] + [c_void_p] * 7
+                                   + [c_void_p]),
     "laminar_plan_num_items": (c_int32, [c_void_p]),
     "laminar_plan_num_merges": (c_int32, [c_void_p]),
     "laminar_plan_pages_per_item": (c_int32, [c_void_p]),
@@ -247,6 +249,14 @@ def laminar_decode_attn_merge(plan, out, lse, stream):
     _check(lib().laminar_decode_attn_merge(plan, _ptr(out), _ptr(lse),
                                            _ptr(stream)),
            "laminar_decode_attn_merge")
+
+
+def laminar_decode_attn_static(plan, q, k_pages, v_pages, block_table,
+                               seq_lens, out, lse, stream):
+    _check(lib().laminar_decode_attn_static(
+        plan, _ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table),
+        _ptr(seq_lens), _ptr(out), _ptr(lse), _ptr(stream)),
+        "laminar_decode_attn_static")
 
 
 def laminar_plan_num_items(plan) -> int:

@@ -133,6 +133,31 @@ laminar_detail::AttnCall make_call(const laminar_plan* p, const void* q,
                                   out, lse, p->ws};
 }
 
+// The library's own workspace for laminar_decode_attn_static: one
+// LAMINAR_STATIC_WORKSPACE_BYTES array per GPU, held until the process
+// ends. `scratch` names a host-side stand-in in host code; kernels get the
+// device address that hipGetSymbolAddress returns for the current device.
+__device__ __align__(256) unsigned char scratch[LAMINAR_STATIC_WORKSPACE_BYTES];
+
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per
+// device; nullptr on failure.
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+      return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -195,6 +220,35 @@ laminar_status laminar_decode_attn(const laminar_plan* plan, const void* q,
   const laminar_detail::AttnCall c =
       make_call(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse);
   st = laminar_detail::enqueue_partial(*plan, c, stream);
+  if (st != LAMINAR_OK) return st;
+  return laminar_detail::enqueue_merge(*plan, c, stream);
+}
+
+laminar_status laminar_decode_attn_static(const laminar_plan* plan,
+                                          const void* q, const void* k_pages,
+                                          const void* v_pages,
+                                          const int32_t* block_table,
+                                          const int32_t* seq_lens, float* out,
+                                          float* lse, hipStream_t stream) {
+  if (!plan) return LAMINAR_ERR_INVALID_ARG;
+  if (!inputs_ok(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (plan->ws_bytes > LAMINAR_STATIC_WORKSPACE_BYTES)
+    return LAMINAR_ERR_WORKSPACE;
+  if (plan->num_items == 0) return LAMINAR_OK;
+  void* ws = scratch_on_current_device();
+  if (!ws) return LAMINAR_ERR_HIP;
+  // The plan's tables (work list, merge and cascade records, and the zero
+  // tail counter) go into the front of the workspace in stream order.
+  const size_t table_bytes = plan->tables.size() * sizeof(int32_t);
+  if (table_bytes > 0 &&
+      hipMemcpyAsync(ws, plan->tables.data(), table_bytes,
+                     hipMemcpyHostToDevice, stream) != hipSuccess)
+    return LAMINAR_ERR_HIP;
+  laminar_detail::AttnCall c =
+      make_call(plan, q, k_pages, v_pages, block_table, seq_lens, out, lse);
+  c.ws = ws;
+  laminar_status st = laminar_detail::enqueue_partial(*plan, c, stream);
   if (st != LAMINAR_OK) return st;
   return laminar_detail::enqueue_merge(*plan, c, stream);
 }
