@@ -145,14 +145,16 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, *,
             out[b, h0:h0 + g] = o
             lse[b, h0:h0 + g] = l
 
-    if workers <= 1:
-        for b in range(b_count):
-            one(b)
-    else:
-        # one BLAS thread per worker: a full BLAS pool in every worker
-        # oversubscribes the host and runs ~40x slower
-        with _blas_threads(1), ThreadPoolExecutor(max_workers=workers) as ex:
-            list(ex.map(one, range(b_count)))
+    # one BLAS thread per worker: a full BLAS pool in every worker
+    # oversubscribes the host and runs ~40x slower; the serial path uses one
+    # too, so the result does not depend on the number of workers
+    with _blas_threads(1):
+        if workers <= 1:
+            for b in range(b_count):
+                one(b)
+        else:
+            with ThreadPoolExecutor(max_workers=workers) as ex:
+                list(ex.map(one, range(b_count)))
     return out, lse
 
 

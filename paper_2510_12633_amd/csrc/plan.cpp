@@ -94,6 +94,31 @@ struct Chunk {
   Cut cut;
 };
 
+// XCD-aware launch order. The hardware deals workgroup k to XCD k % 8, and
+// each XCD has its own L2. The hkv items of one page range of one
+// trajectory (or cascade chunk), one per kv-head, form a group: they read
+// the same block-table entries and, for fp8 pools, the same lines of the
+// [page][kv-head] scale arrays, and their K and V tiles of a page are
+// adjacent in HBM. The list arrives longest first with each group's items
+// next to each other; every run of eight groups is laid out kv-head-major,
+// item (group x, kv-head h) at run start + 8 h + x, so that a group's items
+// sit on one XCD and run there side by side and the shared lines come from
+// its L2 instead of once per kv-head from HBM. A last run of fewer than
+// eight groups keeps the layout without that property.
+void xcd_order(Item* items, int64_t n, int32_t hkv) {
+  constexpr int64_t kXcds = 8;
+  if (hkv <= 1) return;
+  std::vector<Item> run(size_t(kXcds * hkv));
+  for (int64_t r = 0; r < n; r += kXcds * hkv) {
+    const int64_t len = std::min(n - r, kXcds * hkv);
+    const int64_t groups = len / hkv;          // n is a multiple of hkv
+    std::copy(items + r, items + r + len, run.begin());
+    for (int64_t x = 0; x < groups; ++x)
+      for (int64_t h = 0; h < hkv; ++h)
+        items[r + h * groups + x] = run[size_t(x * hkv + h)];
+  }
+}
+
 laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
                      const int32_t* group_of, int32_t num_groups,
                      const int32_t* group_pages, int32_t num_cus,
@@ -256,27 +281,37 @@ laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
   int32_t next_slot = 0, m = 0;
   for (int64_t u = 0; u < int64_t(B) * hkv; ++u) {
     const int32_t b = int32_t(u / hkv);
+    const int32_t ci = chunk_of[size_t(b)];
+    const int32_t n_all = int32_t(cuts[size_t(b)].n) +
+                          (ci >= 0 ? int32_t(chunks[size_t(ci)].cut.n) : 0);
+    if (ci >= 0 || n_all > 1) {
+      slot0[size_t(u)] = next_slot;
+      mrec[m++] = {int32_t(u), next_slot, n_all, 0};
+      next_slot += n_all;
+    }
+  }
+  // Items. The kv-heads of a unit are cut alike, so the hkv items of one
+  // page range (a group) have one size; they are placed next to each other
+  // (trajectory, piece, kv-head order), which xcd_order relies on.
+  for (int32_t b = 0; b < B; ++b) {
     const Cut& c = cuts[size_t(b)];
     const int32_t ci = chunk_of[size_t(b)];
     const uint32_t ncas = ci >= 0 ? chunks[size_t(ci)].cut.n : 0;
-    const int32_t n_all = int32_t(c.n + ncas);
-    const bool merged = ci >= 0 || n_all > 1;
-    if (merged) {
-      slot0[size_t(u)] = next_slot;
-      mrec[m++] = {int32_t(u), next_slot, n_all, 0};
-    }
     int32_t pos = int32_t(first[size_t(b)]);
     for (uint32_t i = 0; i < c.n; ++i) {
       const uint32_t sz = c.size(i);
-      items[start[longest - sz]++] = {
-          int32_t(u), pos, pos + int32_t(sz),
-          merged ? next_slot + int32_t(ncas + i) : -1};
+      for (int32_t h = 0; h < hkv; ++h) {
+        const int64_t u = int64_t(b) * hkv + h;
+        const int32_t s0 = slot0[size_t(u)];
+        items[start[longest - sz]++] = {int32_t(u), pos, pos + int32_t(sz),
+                                        s0 >= 0 ? s0 + int32_t(ncas + i) : -1};
+      }
       pos += int32_t(sz);
     }
-    if (merged) next_slot += n_all;
   }
   // Cascade units (chunk, kv-head): header (row, members, first member
-  // record, kv-head) and member records (trajectory, first slot).
+  // record, kv-head) and member records (trajectory, first slot); then
+  // their items, again a group of hkv items per piece.
   int32_t mo = 0;
   for (size_t ci = 0; ci < chunks.size(); ++ci) {
     const Chunk& c = chunks[ci];
@@ -288,15 +323,19 @@ laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
         cmem[2 * mo + 1] = slot0[size_t(b) * hkv + h];
         ++mo;
       }
-      int32_t pos = 0;
-      for (uint32_t i = 0; i < c.cut.n; ++i) {
-        const uint32_t sz = c.cut.size(i);
+    }
+    int32_t pos = 0;
+    for (uint32_t i = 0; i < c.cut.n; ++i) {
+      const uint32_t sz = c.cut.size(i);
+      for (int32_t h = 0; h < hkv; ++h) {
+        const int32_t cu = int32_t(ci) * hkv + h;
         items[start[longest - W * sz]++] = {-(cu + 1), pos, pos + int32_t(sz),
                                             int32_t(i)};
-        pos += int32_t(sz);
       }
+      pos += int32_t(sz);
     }
   }
+  xcd_order(items, total, hkv);
   // Dynamic tail. Workgroups are dealt to the eight XCDs round-robin by
   // index and the XCDs stream at rates up to ~10% apart, so a fixed
   // assignment ends when the slowest XCD ends. The smallest items (at most

@@ -24,7 +24,9 @@ def test_more_than_one_gpu_is_refused():
 def test_traffic_summary_needs_the_current_source(tmp_path, monkeypatch):
     src = tmp_path / "kernel.hip"
     src.write_text("// kernel v1\n")
-    monkeypatch.setattr(bench, "KERNEL_SOURCE", str(src))
+    plan = tmp_path / "plan.cpp"
+    plan.write_text("// plan v1\n")
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", (str(src), str(plan)))
     monkeypatch.setattr(bench, "PROFILE_DIR", str(tmp_path))
     digest = bench.source_digest()
     f = tmp_path / f"{bench.PARTIAL_KERNEL}_demo_traffic.txt"
@@ -33,16 +35,35 @@ def test_traffic_summary_needs_the_current_source(tmp_path, monkeypatch):
     assert bench.read_traffic("demo") == (1234.0, str(f))
     src.write_text("// kernel v2\n")                 # the kernel changed
     assert bench.read_traffic("demo") == (None, "stale")
+    src.write_text("// kernel v1\n")
+    assert bench.read_traffic("demo") == (1234.0, str(f))
+    plan.write_text("// plan v2\n")                  # the planner changed
+    assert bench.read_traffic("demo") == (None, "stale")
     assert bench.read_traffic("absent") == (None, None)
 
 
+WORKLOADS = ("tiny", "7b_pre_repack", "post_repack", "32b_fp8", "agentic_mix",
+             "32b_fp8_tp4", "agentic_mix_tp8")
+
+
 def test_committed_traffic_summaries_match_the_kernel_source():
-    """The committed counters were taken on the kernel source as it is, so
-    the bench line reports them (a stale summary would report null)."""
-    for w in ("7b_pre_repack", "post_repack", "32b_fp8", "agentic_mix"):
+    """The committed counters were taken on the kernel and planner sources
+    as they are, so the bench line reports them (a stale summary would
+    report null)."""
+    for w in WORKLOADS:
         value, where = bench.read_traffic(w)
         assert where not in (None, "stale"), w
         assert value > 0
+
+
+def test_committed_kernel_statistics_match_the_kernel_source():
+    """Each workload's rocprofv3 statistics list the attention kernels'
+    rows and were taken on the current kernel and planner sources."""
+    for w in WORKLOADS:
+        path = os.path.join(bench.PROFILE_DIR, f"decode_items_{w}_stats.md")
+        text = open(path).read()
+        assert f"kernel_source_sha256_16: {bench.source_digest()}" in text, w
+        assert "| decode_items<" in text, w
 
 
 def test_cpu_baseline_object_on_the_tiny_workload():

@@ -66,6 +66,22 @@ def test_status_strings():
     assert N.laminar_status_string(99) == "unknown status"
 
 
+def check_xcd_rounds(items, hkv):
+    """Items of one (trajectory or cascade chunk, first page) over the
+    kv-heads: in every full round of 8 x hkv items, the kv-heads of a group
+    sit at indices congruent mod 8 (workgroup k runs on XCD k % 8)."""
+    if hkv <= 1:
+        return
+    key = lambda it: ((int(it[0]) < 0), (-int(it[0]) - 1 if it[0] < 0
+                                         else int(it[0])) // hkv, int(it[1]))
+    full = len(items) // (8 * hkv) * 8 * hkv
+    pos = {}
+    for i, it in enumerate(items[:full]):
+        pos.setdefault(key(it), []).append(i)
+    for k, idx in pos.items():
+        assert len(idx) == hkv and len({i % 8 for i in idx}) == 1, (k, idx)
+
+
 def check_plan(lens, hkv, items, merges, ppi):
     """Coverage, size, ordering and slot invariants of a plan."""
     pages = -(-np.asarray(lens, np.int64) // 16)
@@ -84,7 +100,12 @@ def check_plan(lens, hkv, items, merges, ppi):
     assert len(covered) == int(pages.sum()) * hkv
     assert set(by_unit) == set(range(len(lens) * hkv))
     sizes = [int(p1 - p0) for _, p0, p1, _ in items]
-    assert sizes == sorted(sizes, reverse=True)         # longest first
+    # longest first for every kv-head; groups of a page range over the
+    # kv-heads laid out eight at a time, kv-head-major (one XCD per group)
+    for h in range(hkv):
+        sub = [sz for (u, _, _, _), sz in zip(items, sizes) if u % hkv == h]
+        assert sub == sorted(sub, reverse=True)
+    check_xcd_rounds(items, hkv)
     merged = {int(m[0]): (int(m[1]), int(m[2])) for m in merges}
     assert len(merged) == len(merges)
     all_slots = []
@@ -333,7 +354,11 @@ def check_cascade_plan(lens, hkv, g, group_of, group_pages, items, merges,
                 slot_of.setdefault(b * hkv + h, []).append((-1, int(s0 + slot)))
             cost.append(waves * int(p1 - p0))
     assert len(covered) == int(pages.sum()) * hkv
-    assert cost == sorted(cost, reverse=True)
+    for h in range(hkv):
+        sub = [c for it, c in zip(items, cost)
+               if (int(it[0]) if it[0] >= 0 else -int(it[0]) - 1) % hkv == h]
+        assert sub == sorted(sub, reverse=True)
+    check_xcd_rounds(items, hkv)
     merged = {int(m[0]): (int(m[1]), int(m[2])) for m in merges}
     all_slots = []
     for unit, lst in slot_of.items():
