@@ -68,6 +68,25 @@ laminar_status laminar_kv_append(const laminar_attn_desc* desc,
                                  void* v_pages, float* k_scale, float* v_scale,
                                  hipStream_t stream);
 
+/*
+ * Pack row-major KV pages into the tile order of laminar_decode_attn.h, for
+ * callers whose cache (or whose producer of K and V) keeps each (page,
+ * kv-head) tile as 16 token rows of head_dim contiguous elements, i.e. a
+ * pool [num_pages, num_kv_heads, 16, head_dim] (the paged KV cache whose
+ * capacity the paper's §5.2 budgets). src holds num_tiles such tiles
+ * (num_pages x num_kv_heads), dst receives them in the K order (which = 0)
+ * or the V order (which = 1) for elements of kv_dtype (bf16: 2 bytes, fp8
+ * e4m3fn: 1 byte; codes are moved, never converted, so fp8 scales are
+ * unchanged). Both are device pointers, 16-byte aligned, and must not
+ * overlap. Enqueued on `stream`; nothing is allocated or retained.
+ * Errors: INVALID_ARG (NULL or misaligned pointers when num_tiles > 0,
+ * overlapping buffers, num_tiles < 0, which or kv_dtype out of range),
+ * UNSUPPORTED (head_dim not 64 or 128), HIP (launch failure).
+ */
+laminar_status laminar_kv_pack(const void* src, void* dst, int64_t num_tiles,
+                               int32_t head_dim, int32_t kv_dtype,
+                               int32_t which, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -110,6 +110,8 @@ _SIGNATURES = {
                                      ctypes.c_int64, c_void_p, c_void_p]),
     "laminar_kv_append": (c_int32, [POINTER(LaminarAttnDesc)] + [c_void_p] * 8
                           + [c_void_p]),
+    "laminar_kv_pack": (c_int32, [c_void_p, c_void_p, ctypes.c_int64, c_int32,
+                                  c_int32, c_int32, c_void_p]),
     "laminar_repack_plan": (c_int32, [POINTER(LaminarRolloutState), c_int32,
                                       ctypes.c_int64, c_int32, POINTER(c_int32),
                                       POINTER(c_int32), POINTER(c_int32)]),
@@ -471,3 +473,10 @@ def laminar_hbm_gather(src, src_bytes: int, tile_bytes: int, idx, n_idx: int,
     _check(lib().laminar_hbm_gather(_ptr(src), int(src_bytes), int(tile_bytes),
                                     _ptr(idx), int(n_idx), _ptr(sink),
                                     _ptr(stream)), "laminar_hbm_gather")
+
+
+def laminar_kv_pack(src, dst, num_tiles: int, head_dim: int, kv_dtype: int,
+                    which: int, stream):
+    _check(lib().laminar_kv_pack(_ptr(src), _ptr(dst), int(num_tiles),
+                                 int(head_dim), int(kv_dtype), int(which),
+                                 _ptr(stream)), "laminar_kv_pack")

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 
 SOURCES = [os.path.join(CSRC, "decode_attn.hip"),
            os.path.join(CSRC, "attn_entry.hip"), os.path.join(CSRC, "calibrate.hip"),
-           os.path.join(CSRC, "kv_append.hip"), os.path.join(CSRC, "migrate.hip"),
+           os.path.join(CSRC, "kv_append.hip"), os.path.join(CSRC, "kv_pack.hip"), os.path.join(CSRC, "migrate.hip"),
            os.path.join(CSRC, "linear.hip"), os.path.join(CSRC, "decode_step.hip"),
            os.path.join(CSRC, "plan.cpp"), os.path.join(CSRC, "repack.cpp")]
 

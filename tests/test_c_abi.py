@@ -719,3 +719,21 @@ def test_attention_pointer_alignment_checked_before_any_launch():
         N.laminar_plan_create(desc(kv=N.LAMINAR_KV_FP8_E4M3FN, k_scale=4098,
                                    v_scale=4096), np.array([40, 9, 1, 1], np.int32), 256)
     assert e.value.status == N.LAMINAR_ERR_INVALID_ARG
+
+
+def test_kv_pack_errors_before_any_launch():
+    pack = N.lib().laminar_kv_pack
+    bf, f8 = N.LAMINAR_KV_BF16, N.LAMINAR_KV_FP8_E4M3FN
+    big = 1 << 40
+    assert pack(None, None, 0, 128, bf, 0, None) == N.LAMINAR_OK
+    assert pack(None, big, 1, 128, bf, 0, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert pack(big, None, 1, 128, bf, 1, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert pack(big + 8, 2 * big, 1, 128, bf, 0, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert pack(big, 2 * big + 4, 1, 128, f8, 0, None) == N.LAMINAR_ERR_INVALID_ARG
+    # overlapping buffers (one tile is 4 KiB in bf16 at head_dim 128)
+    assert pack(big, big + 4096 - 16, 1, 128, bf, 0, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert pack(big + 4096 - 16, big, 1, 128, bf, 0, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert pack(big, 2 * big, -1, 128, bf, 0, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert pack(big, 2 * big, 1, 128, bf, 2, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert pack(big, 2 * big, 1, 128, 7, 0, None) == N.LAMINAR_ERR_INVALID_ARG
+    assert pack(big, 2 * big, 1, 96, bf, 0, None) == N.LAMINAR_ERR_UNSUPPORTED
