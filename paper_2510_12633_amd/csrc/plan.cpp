@@ -71,17 +71,40 @@ laminar_status validate_groups(const laminar_attn_desc* d,
   return LAMINAR_OK;
 }
 
-// Near-equal page-aligned cut of `pages` into ceil(pages / cap) pieces, the
-// first pages % n of them one page longer (one empty piece for 0 pages).
+// Page-aligned cut of `pages` into n = ceil(pages / cap) pieces (one empty
+// piece for 0 pages). Plain: near-equal pieces, the first ones one page
+// longer. In halves (n >= 2): the first ceil(n / 2) pieces are twice as
+// long as the others, each half near-equal, so a unit's later pieces are
+// short ones that can join the dynamic tail.
 struct Cut {
-  uint32_t n, base, rem;
-  Cut() : n(1), base(0), rem(0) {}
-  Cut(uint32_t pages, uint32_t cap) {
+  uint32_t n, k;          // pieces; the first k are the long half
+  uint32_t lb, lr, sb, sr;  // long: size lb, first lr one longer; short alike
+  Cut() : n(1), k(1), lb(0), lr(0), sb(0), sr(0) {}
+  Cut(uint32_t pages, uint32_t cap, bool halves = false) {
     n = pages == 0 ? 1 : (pages - 1) / cap + 1;
-    base = pages / n;
-    rem = pages - base * n;
+    k = n;
+    lb = pages / n;
+    lr = pages - lb * n;
+    sb = sr = 0;
+    if (halves && n >= 2) {
+      const uint32_t kk = (n + 1) / 2;
+      // long pieces weigh 2, short ones 1: the long half holds
+      // pages * 2 kk / (2 kk + n - kk), rounded
+      const uint64_t w = uint64_t(kk) + n;
+      const uint32_t lng = uint32_t((uint64_t(pages) * 2 * kk + w / 2) / w);
+      const uint32_t sht = pages - lng;
+      if (sht / (n - kk) >= 2) {          // short pieces keep a page pair
+        k = kk;
+        lb = lng / k;
+        lr = lng - lb * k;
+        sb = sht / (n - k);
+        sr = sht - sb * (n - k);
+      }
+    }
   }
-  uint32_t size(uint32_t i) const { return base + (i < rem ? 1u : 0u); }
+  uint32_t size(uint32_t i) const {
+    return i < k ? lb + (i < lr ? 1u : 0u) : sb + (i - k < sr ? 1u : 0u);
+  }
 };
 
 // One group chunk that is decoded as a cascade: up to waves x (16 / g)
@@ -185,18 +208,40 @@ laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
   const int64_t resident = int64_t(num_cus) *
       std::max(1, laminar_detail::kResidentWavesPerCU / W);
   const int64_t step = 2 * int64_t(W);          // one page pair per wave
+  // Aim for num / den items per resident workgroup; every wave of an item
+  // gets at least one pair of pages.
+  auto chunk_for = [&](int64_t num, int64_t den) {
+    const int64_t target = resident * num / den;
+    const int64_t c = std::max<int64_t>(step, (work + target - 1) / target);
+    return (c + step - 1) / step * step;
+  };
   int64_t chunk;
+  bool halves = false;
   if (desc->pages_per_item > 0) {
     chunk = desc->pages_per_item;
   } else {
-    // Aim for kItemsPerSlot items per resident workgroup; every wave of an
-    // item gets at least one pair of pages.
-    const int64_t target = resident * laminar_detail::kItemsPerSlotNum /
-                           laminar_detail::kItemsPerSlotDen;
-    chunk = std::max<int64_t>(step, (work + target - 1) / target);
-    chunk = (chunk + step - 1) / step * step;
+    chunk = chunk_for(laminar_detail::kItemsPerSlotNum,
+                      laminar_detail::kItemsPerSlotDen);
+    // A batch that mixes units shorter than half a piece (whole items that
+    // fall to the dynamic tail) with units cut into several pieces aims
+    // for kMixedItemsPerSlot items per slot and cuts the long units in
+    // halves, so their short second halves join the tail too: measured
+    // 4% faster on the TP-4 share of the 32B workload, 0.6% on
+    // 7b_pre_repack and 0.2% on the 32B workload. A batch of long units
+    // only (post_repack) keeps equal pieces and no tail, which halves made
+    // 3-7% slower, and so do cascade plans, which have no dynamic tail
+    // (halves made the agentic mixes 0.5-1% slower).
+    bool has_short = false, has_long = false;
+    for (int32_t b = 0; b < B && chunks.empty(); ++b) {
+      const int64_t own = int64_t(pages[size_t(b)]) - first[size_t(b)];
+      has_short |= own > 0 && 2 * own < chunk;
+      has_long |= own > chunk;
+    }
+    if (has_short && has_long) {
+      halves = true;
+      chunk = chunk_for(laminar_detail::kMixedItemsPerSlot, 1);
+    }
   }
-  p->pages_per_item = int32_t(std::min<int64_t>(chunk, INT32_MAX));
   const uint32_t chunk32 = uint32_t(std::min<int64_t>(chunk, UINT32_MAX));
   // cascade pieces: the same wavefront-time, whole page pairs
   const uint32_t cchunk =
@@ -206,21 +251,28 @@ laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
   std::vector<Cut> cuts(static_cast<size_t>(B));
   int64_t total = 0, merges = 0, slots = 0, members = 0;
   uint32_t longest = 0;                          // longest item, wave-time
+  uint32_t max_piece = 0;                        // longest ordinary item
   for (int32_t b = 0; b < B; ++b) {
     const uint32_t own = pages[size_t(b)] - first[size_t(b)];
     const bool cas = chunk_of[size_t(b)] >= 0;
     // a cascade member with nothing of its own has no ordinary item
-    Cut c = (cas && own == 0) ? Cut() : Cut(own, chunk32);
+    Cut c = (cas && own == 0) ? Cut() : Cut(own, chunk32, halves);
     if (cas && own == 0) c.n = 0;
     cuts[size_t(b)] = c;
     total += int64_t(c.n) * hkv;
-    if (c.n) longest = std::max(longest, c.size(0));
+    if (c.n) {
+      longest = std::max(longest, c.size(0));
+      max_piece = std::max(max_piece, c.size(0));
+    }
     const int64_t n_all = c.n + (cas ? chunks[size_t(chunk_of[size_t(b)])].cut.n : 0);
     if (cas || n_all > 1) {
       merges += hkv;
       slots += n_all * hkv;
     }
   }
+  // the bound the pieces respect: the split size, or the long half's pieces
+  p->pages_per_item = int32_t(
+      std::min<int64_t>(std::max<int64_t>(chunk, max_piece), INT32_MAX));
   for (const Chunk& c : chunks) {
     total += int64_t(c.cut.n) * hkv;
     longest = std::max<uint32_t>(longest, uint32_t(W) * c.cut.size(0));
@@ -266,11 +318,8 @@ laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
   std::vector<int64_t> start(size_t(longest) + 2, 0);
   for (const Chunk& c : chunks)
     for (uint32_t i = 0; i < c.cut.n; ++i) start[longest - W * c.cut.size(i)] += hkv;
-  for (const Cut& c : cuts) {
-    if (c.n == 0) continue;
-    start[longest - c.base] += int64_t(c.n - c.rem) * hkv;
-    if (c.rem) start[longest - c.base - 1] += int64_t(c.rem) * hkv;
-  }
+  for (const Cut& c : cuts)
+    for (uint32_t i = 0; i < c.n; ++i) start[longest - c.size(i)] += hkv;
   int64_t acc = 0;
   for (auto& v : start) { const int64_t c = v; v = acc; acc += c; }
 

@@ -49,5 +49,9 @@ constexpr int kResidentWavesPerCU = 8;
 // the measured sweet spot on the 7B and post-repack workloads.
 constexpr int kItemsPerSlotNum = 3;
 constexpr int kItemsPerSlotDen = 2;
+// Items per resident slot for batches that mix short units (dynamic tail)
+// with long ones cut in halves: 2 measured at or near the best next to 1.5,
+// 2.5 and 3 on the 7B and 32B workloads and the 32B TP-4 share.
+constexpr int kMixedItemsPerSlot = 2;
 constexpr int kDefaultWaves = 4;
 }  // namespace laminar_detail

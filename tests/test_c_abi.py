@@ -110,8 +110,14 @@ def check_plan(lens, hkv, items, merges, ppi):
     assert len(merged) == len(merges)
     all_slots = []
     for unit, chunks in by_unit.items():
-        sz = [p1 - p0 for p0, p1, _ in chunks]
-        assert max(sz) - min(sz) <= 1                   # near-equal pieces
+        sz = [p1 - p0 for p0, p1, _ in sorted(chunks)]   # page order
+        if max(sz) - min(sz) > 1:
+            # halves: the first ceil(n/2) pieces twice as long as the rest,
+            # each half near-equal (batches mixing short and long units)
+            k = (len(sz) + 1) // 2
+            lng, sht = sz[:k], sz[k:]
+            assert max(lng) - min(lng) <= 1 and max(sht) - min(sht) <= 1, sz
+            assert 2 * min(sht) - 2 <= min(lng) and max(lng) <= 2 * max(sht) + 2, sz
         if len(chunks) == 1:
             assert chunks[0][2] == -1 and unit not in merged
         else:
