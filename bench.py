@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode-attn KV TB/s (fraction of HBM peak) + tokens/s at long-tail batch"
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+PARITY_TOL = 1e-3               # max-abs error of fp32 out and lse vs the oracle
 DEFAULT_WORKLOAD = "7b_pre_repack"
 PARTIAL_KERNEL = "decode_items"
 PROFILE_DIR = os.path.join(ROOT, "profiles")
@@ -671,10 +672,16 @@ def oracle_parity(wl, out, lse):
     fin = np.isfinite(rl)
     ok_shape = (np.isfinite(o).all() and np.isfinite(l[fin]).all()
                 and np.array_equal(np.isneginf(l), np.isneginf(rl)))
-    return {"max_abs_err_out": float(np.abs(o - ro).max()) if o.size else 0.0,
-            "max_abs_err_lse": float(np.abs(l[fin] - rl[fin]).max())
-            if fin.any() else 0.0,
+    eo = float(np.abs(o - ro).max()) if o.size else 0.0
+    el = float(np.abs(l[fin] - rl[fin]).max()) if fin.any() else 0.0
+    ok = bool(ok_shape) and eo <= PARITY_TOL and el <= PARITY_TOL
+    if not ok:
+        print(f"[bench] {wl.cfg.name}: parity FAILED (out {eo:.2e}, lse {el:.2e}, "
+              f"rows written and finite: {bool(ok_shape)})", file=sys.stderr,
+              flush=True)
+    return {"max_abs_err_out": eo, "max_abs_err_lse": el,
             "all_rows_written_and_finite": bool(ok_shape),
+            "within_tolerance": ok, "tolerance": PARITY_TOL,
             "trajectories_checked": int(wl.batch),
             "oracle_s": round(dt, 3), "oracle_threads": cores}
 
