@@ -836,6 +836,8 @@ def measure(torch, N, name, steps, warm, args, seed=None):
                                      if traffic else None),
         "work_items": n_items,
         "cascade_prefix": use_cascade,
+        "plan_host_us": round(sum(plan_ns) / len(plan_ns) / 1e3, 2)
+        if plan_ns else None,
     }
     if parity:
         entry.update(parity)
