@@ -8,7 +8,11 @@ before timing and stay resident in HBM.
 
 Default workload: 256 trajectories with lognormal(median 2048, sigma 1)
 lengths clipped to [16, 32768], 28 query / 4 KV heads, head_dim 128, bf16 KV
-(a 7B-class rollout step before repack). Prints ONE JSON line.
+(a 7B-class rollout step before repack). Prints ONE JSON line: the
+headline workload's figures, then `per_config`, one row per workload (all
+seven by default) with its step, kernel and merge times, fractions of HBM
+peak, committed HBM traffic ratio and its errors against the fp64 oracle
+over every trajectory.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME|N]
 """
@@ -688,11 +692,13 @@ def oracle_parity(wl, out, lse):
 
 def measure(torch, N, name, steps, warm, args, seed=None):
     """One workload: `steps` timed whole steps (host plan, table upload,
-    partial kernel, merge) after `warm` untimed ones, the two kernels timed
-    with HIP events on the launch stream; then the same with one plan
-    reused (one layer's call of a decode step whose plan all layers share);
-    then one more whole step into NaN-filled outputs, checked against the
-    oracle over every trajectory. Returns (entry, extras)."""
+    partial kernel, merge) after `warm` untimed ones; then the same with one
+    plan reused (one layer's call of a decode step whose plan all layers
+    share); then each kernel launched `steps` times back to back (its
+    average launch duration); every region bracketed by two HIP events on
+    the launch stream. Then one more whole step into NaN-filled outputs,
+    checked against the oracle over every trajectory. Returns (entry,
+    extras)."""
     import numpy as np
 
     from paper_2510_12633_amd.api import KV_DTYPES, num_cus
