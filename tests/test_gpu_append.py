@@ -167,19 +167,17 @@ def _sub_run_arrays(run, kp, vp, ks, vs, seqs):
 
 
 @pytest.mark.parametrize("config", ["32b_fp8", "7b_pre_repack"])
-def test_append_full_size_sampled(config):
+def test_append_full_size_every_trajectory(config):
     """Three decode steps on a full-size pool in one launch per step; the
-    oracle replays them for 24 sampled trajectories."""
+    oracle replays them for every trajectory, and every page any trajectory
+    references (K, V and fp8 scales) must match bit for bit."""
     _need_gpu()
     wl = make_workload(get_config(config), device="cuda")
     run = make_decode_run(wl, steps=3, seed=1, mix="stress")
     del wl
     kp, vp = run.k_pages, run.v_pages
     ks, vs = run.k_scale, run.v_scale
-    rng = np.random.default_rng(4)
-    order = np.argsort(run.lens0)
-    seqs = np.unique(np.concatenate([order[:8], order[-8:],
-                                     rng.choice(run.lens0.size, 8, replace=False)]))
+    seqs = np.arange(run.lens0.size)
     before, sub_table, used = _sub_run_arrays(run, kp, vp, ks, vs, seqs)
     for i in range(run.steps):
         gpu_append(run, i, kp, vp, ks, vs)
