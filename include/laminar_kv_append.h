@@ -48,7 +48,8 @@
  * trajectories must be copied before it is written. The append must be
  * ordered before the attention call that reads the token (same stream).
  * Errors: INVALID_ARG (NULL pointers when batch > 0, bad sizes, missing fp8
- * scales, misaligned k_new / v_new, an input_row_stride below
+ * scales, k_new / v_new / the pools not 16-byte aligned, block_table /
+ * seq_lens / the scales not 4-byte aligned, an input_row_stride below
  * num_kv_heads x head_dim or not a multiple of 8), UNSUPPORTED (page_size != 16, head_dim
  * not 64 or 128), HIP (launch failure).
  */

@@ -267,7 +267,13 @@ extern "C" laminar_status laminar_kv_append(
        reinterpret_cast<uintptr_t>(k_pages) |
        reinterpret_cast<uintptr_t>(v_pages)) & 15)
     return LAMINAR_ERR_INVALID_ARG;
-  if (fp8 && (!k_scale || !v_scale)) return LAMINAR_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(block_table) |
+       reinterpret_cast<uintptr_t>(seq_lens)) & 3)
+    return LAMINAR_ERR_INVALID_ARG;
+  if (fp8 && (!k_scale || !v_scale ||
+              ((reinterpret_cast<uintptr_t>(k_scale) |
+                reinterpret_cast<uintptr_t>(v_scale)) & 3)))
+    return LAMINAR_ERR_INVALID_ARG;
   if (d->input_row_stride != 0 &&
       (int64_t(d->input_row_stride) < int64_t(d->num_kv_heads) * d->head_dim ||
        d->input_row_stride % 8 != 0))

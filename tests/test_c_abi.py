@@ -474,9 +474,14 @@ def test_kv_append_errors_before_any_launch():
     assert call(desc(), lens=None) == INV
     assert call(desc(), vp=None) == INV
     assert call(desc(), k_new=24) == INV                # misaligned
+    assert call(desc(), kp=24) == INV
+    assert call(desc(), bt=18) == INV                   # 4-byte words
+    assert call(desc(), lens=17) == INV
     fp8 = desc(kv=N.LAMINAR_KV_FP8_E4M3FN)
     assert call(fp8, ks=None) == INV
     assert call(fp8, vs=None) == INV
+    assert call(fp8, ks=18) == INV
+    assert call(fp8, vs=17) == INV
 
 
 def test_linear_errors_before_any_launch():
