@@ -484,3 +484,45 @@ def test_extreme_score_ranges(name, cfg):
         if factor == 0.0:
             n = np.repeat(wl.seq_lens.astype(np.float64), cfg.num_q_heads)
             assert np.allclose(lse.reshape(-1), np.log(n), atol=1e-4, rtol=0)
+
+
+def _random_case(seed):
+    """A seeded random decode-attention problem: batch, head layout,
+    head_dim, dtype, ragged lengths with the page-boundary and empty cases,
+    forced split size, wavefronts per item and, for some, shared prefixes."""
+    rng = np.random.default_rng(1000 + seed)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    g = int(rng.integers(1, 17))
+    d = int(rng.choice([64, 128]))
+    kv = "fp8_e4m3fn" if rng.random() < 0.4 else "bf16"
+    b = int(rng.integers(1, 33))
+    special = [0, 1, 15, 16, 17, 31, 32, 33, 255, 256, 257]
+    lens = [int(rng.choice(special)) if rng.random() < 0.35
+            else int(rng.integers(1, 2500)) for _ in range(b)]
+    prefix = {}
+    if rng.random() < 0.35 and b >= 2:
+        prefix = dict(prefix_group=int(rng.integers(2, min(b, 9) + 1)),
+                      prefix_tokens=16 * int(rng.integers(1, 40)))
+    cfg = custom_config(lens, g * hkv, hkv, d, kv_dtype=kv, **prefix)
+    ppi = int(rng.choice([0, 0, 1, 2, 3, 8, 33]))
+    waves = int(rng.choice([0, 1, 2, 4]))
+    return cfg, ppi, waves, bool(prefix)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_shapes(seed):
+    """Seeded random problems (see _random_case) through the C ABI into
+    NaN-filled outputs, every trajectory and head against the oracle at the
+    bar; problems with shared prefixes also through the cascade plan."""
+    _need_gpu()
+    cfg, ppi, waves, has_prefix = _random_case(seed)
+    _say(f"random {seed}: B={cfg.batch} Hq={cfg.num_q_heads} Hkv={cfg.num_kv_heads} "
+         f"D={cfg.head_dim} {cfg.kv_dtype} ppi={ppi} waves={waves} "
+         f"prefix={has_prefix}")
+    wl = make_workload(cfg, seed=seed, device="cuda")
+    ref = decode_attention_from_host(host_arrays(wl), workers=_host_workers())
+    check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves), ref,
+          f"random {seed}")
+    if has_prefix:
+        check(run_gpu(wl, pages_per_item=ppi, waves_per_item=waves,
+                      cascade=True), ref, f"random {seed} cascade")
