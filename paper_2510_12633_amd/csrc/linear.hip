@@ -30,6 +30,13 @@
 // 1-4 us of the 13-31 us that the QKV, O and down projections of 7B-32B
 // models take at one row.
 //
+// When N / 128 groups of eight tiles leave the CUs unevenly loaded (the
+// gate and up projection: 296 groups on 256 CUs left 40 CUs with twice the
+// work), from 17 rows on a balanced split takes over: one workgroup of
+// eight wavefronts per CU streams whole groups, then an equal share of the
+// groups left over, cut along K; those pieces are added in a fixed order by
+// a second kernel.
+//
 // x can also be what the decode step has at hand rather than the operand
 // itself: the fp32 attention output, SwiGLU's gate and up, or the residual
 // stream with an RMS norm in front (at most 8 rows). The staging makes the
@@ -91,9 +98,12 @@ struct LinearArgs {
   float* y;              // [M, N] fp32 output, or NULL when yb is set
   uint16_t* yb;          // [M, N] bf16 output (rounded to nearest even)
   const uint16_t* res;   // [M, N] bf16 residual added before rounding, or NULL
-  float* part;           // [splits, M, N] when split
+  float* part;           // [splits, M, N] when split; balanced: [2 W, M, 128]
   int32_t m, n, k;
   int32_t n_tiles, splits, steps_per_split;
+  // balanced split: each of W workgroups streams full_rounds whole groups
+  // of eight tiles, then an equal share of the rem_groups left over
+  int32_t wgs, full_rounds, rem_groups;
 };
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -340,6 +350,268 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Balanced split (from 17 rows, when the group grid is uneven). A workgroup
+// is eight wavefronts on the eight tiles of a group (128 output features),
+// one workgroup per CU (W = 256: its LDS use admits no second one). Each
+// workgroup processes a stream of (group, step) units: first full_rounds
+// whole groups (w, w + W, ...), whose sums are final, then its share
+// [floor(w ru / W), floor((w + 1) ru / W)) of the ru = rem_groups x steps
+// units left over, in (group, step) order: at most two pieces, whose
+// partial sums go to slots 2 w and 2 w + 1 and are added by
+// linear_balance_reduce in workgroup order. So every CU streams the same
+// weight bytes, within one step.
+// x of a step is staged in LDS row-major: row r's 16 chunks of 16 bytes
+// (128 k) at slots r * 16 + (c ^ (r & 15)), so the 16 lanes of a
+// matrix-core step that read chunk c of rows 0..15 meet no bank conflict,
+// and one wavefront instruction moves 4 rows of x (4 x 256 contiguous
+// bytes; the layout of linear_kernel read 16 rows x 64 bytes per
+// instruction). bf16 x goes from memory into LDS directly (buffer load to
+// LDS); the fused kinds are made in registers and written in the same
+// layout, so every kind sums in the same order. x of a unit is loaded
+// right after the unit's weights, NB units ahead: the vector-memory counter
+// completes in order, so x loaded later than the weights in flight would
+// make each wait for x drain them.
+constexpr int kWideTiles = 8;
+constexpr int kBalancedWgs = 256;
+constexpr int kBalancedNB = 3;     // units in flight (x in LDS)
+constexpr int kBalancedRegNB = 2;  // units in flight (x made in registers)
+
+// s_waitcnt vmcnt(n); expcnt and lgkmcnt not waited for
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// First left-over unit of workgroup w: floor(w ru / W). The quotient's
+// fractional part is a multiple of 1 / W (W <= 256) and w ru < 2^35, so
+// the double division floors exactly.
+__host__ __device__ inline int64_t rem_start(int w, int64_t ru, int wgs) {
+  return int64_t(floor(double(w) * double(ru) / double(wgs)));
+}
+
+// Position in a workgroup's stream of units.
+struct UnitCursor {
+  int g, s;        // group and step
+  int round;       // full round, or full_rounds once in the left-over units
+  int piece;       // left-over piece (0 or 1) of this workgroup
+};
+
+template <int MT, int XK, int NB, bool DMA>
+__global__ void __launch_bounds__(512) linear_balanced_kernel(const LinearArgs a) {
+  static_assert(MT >= 2 && XK != kXRmsNorm, "17 rows or more, no fused norm");
+  static_assert(!DMA || XK == kXBf16, "only bf16 x is copied as it is");
+  constexpr int NBUF = DMA ? NB + 1 : 2;
+  constexpr int kBufSlots = MT * 256;
+  constexpr int XPW = MT / 2;      // x instructions per wavefront and unit
+  // more LDS than two workgroups could share: one workgroup per CU
+  constexpr int kMinSlots = (81 * 1024) / 16;
+  constexpr int kSlots = NBUF * kBufSlots > kMinSlots ? NBUF * kBufSlots : kMinSlots;
+  __shared__ u32x4 xs[kSlots];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wg = blockIdx.x;
+  const int W = a.wgs;
+  const int r16 = lane & 15, q = lane >> 4;
+  const int S = a.k / kStepK;
+  const int gf = a.full_rounds * W;
+  const int64_t ru = int64_t(a.rem_groups) * S;
+  const int u0 = int(rem_start(wg, ru, W));
+  const int u1 = int(rem_start(wg + 1, ru, W));
+  const int n_units = a.full_rounds * S + (u1 - u0);
+  constexpr int xe = kXBytes<XK>;
+  const XSource xsrc = x_source(a, xe);
+  const int w_lane = (q * 16 + r16) * 16;
+
+  // rows past M stay zero (their loads read zeros or nothing)
+  for (int i = tid; i < kSlots; i += 512) xs[i] = u32x4{0u, 0u, 0u, 0u};
+  lds_barrier();
+
+  auto start = [&](UnitCursor& c) {
+    c.round = 0;
+    c.piece = 0;
+    if (a.full_rounds > 0) {
+      c.g = wg;
+      c.s = 0;
+    } else {
+      c.g = gf + u0 / S;
+      c.s = u0 % S;
+    }
+  };
+  auto advance = [&](UnitCursor& c) {
+    if (++c.s < S) return;
+    c.s = 0;
+    if (c.round < a.full_rounds) {
+      if (++c.round < a.full_rounds) {
+        c.g += W;
+      } else {
+        c.g = gf + u0 / S;
+        c.s = u0 % S;
+      }
+    } else {
+      ++c.g;
+      ++c.piece;
+    }
+  };
+
+  u32x4 wb[NB][4];
+  XRaw<XK> xr[DMA ? 1 : NB][XPW];
+  UnitCursor lc;
+  start(lc);
+  int lv = 0;
+  // loads unit lv (its weights, then its x) into set i; units past the
+  // stream read zeros and are not computed
+  auto issue = [&](int i) {
+    const bool in = lv < n_units;
+    const int tile = lc.g * kWideTiles + wave;
+    const bool has = in && tile < a.n_tiles;
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.w) + size_t(has ? tile : 0) * 16 * a.k, 0,
+        has ? a.k * 32 : 0, kBufFlags);
+    const int wo = has ? lc.s * kStepK * 32 + w_lane : kOob;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      wb[i][j] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(wr, wo + 1024 * j, 0, /*nt*/ 2));
+#pragma unroll
+    for (int e = 0; e < XPW; ++e) {
+      const int d = wave * XPW + e;              // rows 4d .. 4d + 3
+      const int row = 4 * d + (lane >> 4);
+      const int c = (lane & 15) ^ (row & 15);
+      const bool inx = in && row < a.m;
+      const int kb = lc.s * kStepK + 8 * c;
+      const int off = inx ? (row * a.x_ld + kb) * xe : kOob;
+      if constexpr (DMA) {
+        u32x4* dst = xs + (lv % NBUF) * kBufSlots + d * 64;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            xsrc.x, (__attribute__((address_space(3))) void*)dst, 16, off, 0, 0, 0);
+      } else {
+        load_x<XK>(xr[i][e], xsrc, off, inx ? kb * 2 : kOob);
+      }
+    }
+    ++lv;
+    if (in) advance(lc);
+  };
+
+  f32x4 acc[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  UnitCursor cc;
+  start(cc);
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    asm volatile("" ::: "memory");
+    issue(i);
+  }
+  asm volatile("" ::: "memory");
+  for (int v0 = 0; v0 < n_units; v0 += NB) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int v = v0 + i;
+      const u32x4* buf;
+      if constexpr (DMA) {
+        // x of unit v went out (NB - 1) units of loads ago; stores issued
+        // since only make this wait longer
+        wait_vm<(NB - 1) * (4 + XPW)>();
+        buf = xs + (v % NBUF) * kBufSlots;
+      } else {
+        // the buffer written here was last read two units ago, before
+        // every wavefront passed the previous unit's barrier
+        u32x4* wbuf = xs + (v & 1) * kBufSlots;
+#pragma unroll
+        for (int e = 0; e < XPW; ++e)
+          wbuf[(wave * XPW + e) * 64 + lane] = x_operand<XK>(xr[i][e], 0.f);
+        buf = wbuf;
+      }
+      lds_barrier();
+      if (v < n_units) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+          for (int t = 0; t < MT; ++t) {
+            const int c = (4 * j + q) ^ r16;
+            const bf16x8 bv = __builtin_bit_cast(bf16x8, buf[(16 * t + r16) * 16 + c]);
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, wb[i][j]), bv, acc[t], 0, 0, 0);
+          }
+        }
+        if (cc.s == S - 1 || v == n_units - 1) {
+          // lane (q, r16) holds D[16 tile + 4q + r][m = 16t + r16]
+          const int tile = cc.g * kWideTiles + wave;
+          const bool whole = cc.round < a.full_rounds;
+#pragma unroll
+          for (int t = 0; t < MT; ++t) {
+            const int m = 16 * t + r16;
+            if (m < a.m) {
+              if (whole) {
+                if (tile < a.n_tiles)
+                  store4(a, size_t(m) * a.n + tile * 16 + 4 * q, acc[t]);
+              } else {
+                const size_t slot = size_t(2 * wg + cc.piece);
+                *reinterpret_cast<f32x4*>(
+                    a.part + (slot * a.m + m) * (kWideTiles * 16) + wave * 16 + 4 * q) =
+                    acc[t];
+              }
+            }
+            acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+        advance(cc);
+      }
+      asm volatile("" ::: "memory");
+      issue(i);
+      asm volatile("" ::: "memory");
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0);     // no load into LDS outlives the workgroup
+}
+
+// Adds the pieces of each left-over group in workgroup order (the order of
+// K), then the output epilogue; four outputs per thread. The pieces of a
+// group come from consecutive workgroups; eight loads go out before the
+// first add.
+__global__ void __launch_bounds__(256) linear_balance_reduce(const LinearArgs a) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int per_group = a.m * (kWideTiles * 4);
+  if (i >= int64_t(a.rem_groups) * per_group) return;
+  const int rg = int(i / per_group);
+  const int rem = int(i - int64_t(rg) * per_group);
+  const int m = rem / (kWideTiles * 4), c4 = rem % (kWideTiles * 4);
+  const int W = a.wgs, rgs = a.rem_groups;
+  const int S = a.k / kStepK;
+  const int n = (a.full_rounds * W + rg) * kWideTiles * 16 + 4 * c4;
+  if (n >= a.n) return;
+  const int64_t ru = int64_t(rgs) * S;
+  const int64_t u = int64_t(rg) * S, u_end = u + S;
+  const int w_lo = max(0, rg * W / rgs - 1);
+  const int w_hi = min(W - 1, ((rg + 1) * W + rgs - 1) / rgs);
+  f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+  int64_t s0 = rem_start(w_lo, ru, W);
+  for (int w = w_lo; w <= w_hi; w += 8) {
+    f32x4 v[8];
+    bool use[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int ww = w + j;
+      const int64_t s1 = rem_start(ww + 1, ru, W);
+      // workgroup ww has units [s0, s1); group rg is its second piece when
+      // its share began in the group before
+      use[j] = ww <= w_hi && s1 > s0 && s0 < u_end && s1 > u;
+      const size_t slot = size_t(2 * ww + (s0 < u ? 1 : 0));
+      v[j] = use[j] ? *reinterpret_cast<const f32x4*>(
+                          a.part + (slot * a.m + m) * (kWideTiles * 16) + 4 * c4)
+                    : f32x4{0.f, 0.f, 0.f, 0.f};
+      s0 = s1;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (use[j]) sum += v[j];
+  }
+  store4(a, size_t(m) * a.n + n, sum);
+}
+
 // One 16-row tile per workgroup, K split over its four wavefronts: wave w
 // takes steps w, w + 4, w + 8, ... The sums of the four are added in LDS in
 // wavefront order, so the result does not depend on timing. x has at most
@@ -498,6 +770,53 @@ SplitPlan split_plan(int32_t m, int32_t n, int32_t k) {
   return p;
 }
 
+struct BalancedPlan {
+  bool use;
+  int32_t wgs, full_rounds, rem_groups;
+};
+
+// The balanced split replaces the group grid from 17 rows on when that grid
+// has more than 256 workgroups and its last round leaves the CUs uneven by
+// more than 15% (rounds x 256 / workgroups; the pieces it cuts along K and
+// their reduction cost a few microseconds, about what 15% of the gate and
+// up projection is worth), and from 65 rows on whenever the grid has more
+// than 256 workgroups: there its staging of x (whole rows, in LDS without
+// registers, eight tiles per workgroup) also beat the group kernel on even
+// grids (the 7B LM head at 128 rows: 236-260 us against 279-288).
+BalancedPlan balanced_plan(int32_t m, int32_t n, int32_t k, const SplitPlan& sp) {
+  BalancedPlan b{false, 0, 0, 0};
+  const int32_t tiles = n / 16;
+  if (sp.wave_split || launch_tiles(m) < 2) return b;
+  const int32_t per_group = launch_tiles(m) >= 4 ? 8 : 4;
+  const int64_t grid = int64_t((tiles + per_group - 1) / per_group) * sp.splits;
+  if (grid <= kMaxGroups) return b;
+  const int64_t rounds = (grid + kMaxGroups - 1) / kMaxGroups;
+  if (launch_tiles(m) < 8 && rounds * kMaxGroups * 100 <= grid * 115) return b;
+  const int32_t groups = (tiles + kWideTiles - 1) / kWideTiles;
+  b.use = true;
+  b.wgs = kBalancedWgs;
+  b.full_rounds = groups / b.wgs;
+  b.rem_groups = groups - b.full_rounds * b.wgs;
+  return b;
+}
+
+// The most pieces any left-over group is cut into (1 when none is cut).
+int32_t balanced_pieces(const BalancedPlan& b, int32_t k) {
+  if (!b.rem_groups) return 1;
+  const int64_t ru = int64_t(b.rem_groups) * (k / kStepK);
+  int32_t most = 1;
+  for (int rg = 0; rg < b.rem_groups; ++rg) {
+    const int64_t u = int64_t(rg) * (k / kStepK), u_end = u + k / kStepK;
+    int32_t count = 0;
+    for (int w = 0; w < b.wgs; ++w) {
+      const int64_t s0 = rem_start(w, ru, b.wgs), s1 = rem_start(w + 1, ru, b.wgs);
+      if (s1 > s0 && s0 < u_end && s1 > u) ++count;
+    }
+    most = count > most ? count : most;
+  }
+  return most;
+}
+
 bool misaligned16(const void* p) {
   return reinterpret_cast<uintptr_t>(p) & 15;
 }
@@ -506,9 +825,37 @@ bool misaligned16(const void* p) {
 
 namespace {
 
+template <int MT, int XK>
+hipError_t launch_balanced(const LinearArgs& a, hipStream_t stream) {
+  const dim3 grid(a.wgs), block(512);
+  if constexpr (XK == kXBf16)
+    hipLaunchKernelGGL((linear_balanced_kernel<MT, XK, kBalancedNB, true>), grid,
+                       block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((linear_balanced_kernel<MT, XK, kBalancedRegNB, false>),
+                       grid, block, 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && a.rem_groups > 0) {
+    const int64_t total = int64_t(a.rem_groups) * a.m * kWideTiles * 4;
+    hipLaunchKernelGGL(linear_balance_reduce, dim3(unsigned((total + 255) / 256)),
+                       dim3(256), 0, stream, a);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
 template <int XK>
-hipError_t launch(const LinearArgs& a, const SplitPlan& plan, int m,
-                  hipStream_t stream) {
+hipError_t launch(const LinearArgs& a, const SplitPlan& plan, bool balanced,
+                  int m, hipStream_t stream) {
+  if constexpr (XK != kXRmsNorm) {
+    if (balanced) {
+      switch (launch_tiles(m)) {
+        case 2: return launch_balanced<2, XK>(a, stream);
+        case 4: return launch_balanced<4, XK>(a, stream);
+        default: return launch_balanced<8, XK>(a, stream);
+      }
+    }
+  }
   if (plan.wave_split) {
     hipLaunchKernelGGL((linear_wave_split_kernel<XK>), dim3(a.n_tiles),
                        dim3(256), 0, stream, a);
@@ -573,10 +920,14 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
   a.k = k;
   a.n_tiles = n / 16;
   const SplitPlan plan = split_plan(m, n, k);
-  a.splits = plan.splits;
+  const BalancedPlan bal = balanced_plan(m, n, k, plan);
+  a.splits = bal.use ? 1 : plan.splits;
   a.steps_per_split = plan.per;
+  a.wgs = bal.wgs;
+  a.full_rounds = bal.full_rounds;
+  a.rem_groups = bal.rem_groups;
   a.part = nullptr;
-  if (a.splits > 1) {
+  if (a.splits > 1 || (bal.use && bal.rem_groups > 0)) {
     const size_t need = laminar_linear_workspace_bytes(m, n, k);
     if (!workspace || workspace_bytes < need ||
         (reinterpret_cast<uintptr_t>(workspace) & 255))
@@ -585,13 +936,13 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
   }
   hipError_t e;
   if (x_kind == kXF32)
-    e = launch<kXF32>(a, plan, m, stream);
+    e = launch<kXF32>(a, plan, bal.use, m, stream);
   else if (x_kind == kXSiluMul)
-    e = launch<kXSiluMul>(a, plan, m, stream);
+    e = launch<kXSiluMul>(a, plan, bal.use, m, stream);
   else if (x_kind == kXRmsNorm)
-    e = launch<kXRmsNorm>(a, plan, m, stream);
+    e = launch<kXRmsNorm>(a, plan, bal.use, m, stream);
   else
-    e = launch<kXBf16>(a, plan, m, stream);
+    e = launch<kXBf16>(a, plan, bal.use, m, stream);
   return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
 }
 
@@ -613,12 +964,21 @@ laminar_status laminar_linear_pack(const void* w, void* w_packed, int32_t n,
 
 int32_t laminar_linear_splits(int32_t m, int32_t n, int32_t k) {
   if (!shape_ok(m, n, k)) return 0;
-  return split_plan(m, n, k).splits;
+  const SplitPlan p = split_plan(m, n, k);
+  const BalancedPlan b = balanced_plan(m, n, k, p);
+  return b.use ? balanced_pieces(b, k) : p.splits;
 }
 
 size_t laminar_linear_workspace_bytes(int32_t m, int32_t n, int32_t k) {
-  const int32_t s = laminar_linear_splits(m, n, k);
-  return s > 1 ? (size_t(s) * m * n * sizeof(float) + 255) & ~size_t(255) : 0;
+  if (!shape_ok(m, n, k)) return 0;
+  const SplitPlan p = split_plan(m, n, k);
+  const BalancedPlan b = balanced_plan(m, n, k, p);
+  size_t bytes = 0;
+  if (b.use)
+    bytes = b.rem_groups ? size_t(2) * b.wgs * m * kWideTiles * 16 * sizeof(float) : 0;
+  else if (p.splits > 1)
+    bytes = size_t(p.splits) * m * n * sizeof(float);
+  return (bytes + 255) & ~size_t(255);
 }
 
 laminar_status laminar_linear(const void* x, const void* w_packed, float* y,

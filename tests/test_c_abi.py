@@ -548,6 +548,21 @@ def test_linear_errors_before_any_launch():
     assert N.laminar_linear_splits(5, 3584, 3584) > 1
     assert N.laminar_linear_splits(1, 5120, 27648) > 1     # 216 steps
     assert N.laminar_linear_splits(0, 16, 128) == 0
+    # the balanced split (from 17 rows, uneven group grids): gate and up of
+    # 7B is 296 groups, one full round and 40 left over, cut into pieces of
+    # 4 or 5 steps of K (at most 7 per group) with two partial slots per
+    # workgroup
+    assert N.laminar_linear_splits(64, 37888, 3584) == 7
+    assert (N.laminar_linear_workspace_bytes(64, 37888, 3584)
+            == 2 * 256 * 64 * 128 * 4)
+    # an even grid keeps the group split up to 64 rows: the LM head (1188
+    # groups, 5 rounds); from 65 rows any grid past 256 workgroups is
+    # balanced (1188 = 4 full rounds and 164 left over)
+    assert N.laminar_linear_splits(64, 152064, 3584) == 1
+    assert N.laminar_linear_workspace_bytes(64, 152064, 3584) == 0
+    assert N.laminar_linear_splits(128, 152064, 3584) > 1
+    # one row tile keeps the group split
+    assert N.laminar_linear_workspace_bytes(16, 37888, 3584) == 0
 
 
 def test_planner_under_address_and_ub_sanitizers(tmp_path):
@@ -695,6 +710,12 @@ def test_linear_kernels_use_no_scratch():
             assert o >= (3 if "ILi3E" in n else 4), (n, o)
         elif "linear_kernelILi8E" not in n:
             assert o >= 2, (n, o)
+    # the balanced split: 32, 64 and 128 rows for bf16, fp32 and gate-and-up
+    # x, eight wavefronts (two per SIMD) in the one workgroup per CU
+    balanced = [(n, sc, o) for n, sc, o in zip(names, scratch, occ)
+                if "linear_balanced_kernel" in n]
+    assert len(balanced) == 9, balanced
+    assert all(sc == 0 and o >= 2 for _, sc, o in balanced), balanced
 
 
 def test_attention_pointer_alignment_checked_before_any_launch():

@@ -28,7 +28,12 @@ SHAPES = [(1, 16, 128), (7, 48, 256), (16, 4608, 3584), (17, 3584, 3584),
           # K split over the wavefronts of a workgroup (M <= 4): ragged
           # step counts per wavefront, 7B and 32B shapes
           (4, 48, 640), (1, 3584, 3584), (3, 3584, 18944), (2, 7168, 5120),
-          (4, 5120, 20480)]
+          (4, 5120, 20480),
+          # the balanced split: a full round and 40 groups left over (7B
+          # gate and up), 2 groups left over in 6 steps over 256 workgroups
+          # (most of them get none), one step of K, 128 rows
+          (64, 37888, 3584), (33, 33024, 384), (17, 37888, 128),
+          (128, 37888, 256)]
 
 
 @pytest.mark.parametrize("m,n,k", SHAPES)
@@ -102,7 +107,10 @@ def test_linear_errors():
 
 FUSED_SHAPES = [(1, 3584, 3584), (4, 3584, 3584), (3, 5120, 5120),
                 (2, 3584, 18944), (4, 48, 640), (5, 4608, 3584),
-                (17, 256, 1024), (64, 3584, 18944), (128, 208, 512)]
+                (17, 256, 1024), (64, 3584, 18944), (128, 208, 512),
+                # the balanced split (x made in registers against x copied
+                # into LDS as it is)
+                (64, 37888, 512), (40, 33024, 384)]
 
 
 @pytest.mark.parametrize("m,n,k", FUSED_SHAPES)
