@@ -505,9 +505,11 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
         the library GEMM, the skinny kernel, and for O and down also the
         skinny kernel with its input made on load. Each is timed over every
         layer's weights in turn (as in a step, so the 256 MB Infinity Cache
-        does not hold them), the best of three alternating passes, so that
-        one slow pass (a first call that tunes, a clock change) cannot
-        decide."""
+        does not hold them), captured in a HIP graph as the step is (timed
+        eagerly, the host's launches counted: the fused down projection,
+        one launch, won at batch 64 while its GPU time was 10 us longer
+        than SwiGLU and the bf16 call), the best of three alternating
+        passes, so that one slow pass (a clock change) cannot decide."""
         picks = {}
         for i, kind in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
             projs = ([lm_head] * 4 if kind == "lm_head" else
@@ -525,24 +527,33 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                 modes.append("skinny")
             if m <= (8 if normed else 128):
                 modes.append("fused")
+            graphs = {}
+            cap = torch.cuda.Stream()
             for mode in modes:
                 for p in projs:
                     p.mode = mode
-                projs[0](x, **kw)
+                # first calls (library tuning, code loading) stay outside
+                # the capture
+                for p in projs:
+                    p(x, **kw)
+                torch.cuda.synchronize()
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    for p in projs:
+                        p(x, **kw)
+                graphs[mode] = g
             torch.cuda.synchronize()
             times = {mode: float("inf") for mode in modes}
             for _ in range(3):
                 for mode in modes:
-                    for p in projs:
-                        p.mode = mode
                     e0 = torch.cuda.Event(enable_timing=True)
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record()
-                    for p in projs:
-                        p(x, **kw)
+                    graphs[mode].replay()
                     e1.record()
                     torch.cuda.synchronize()
                     times[mode] = min(times[mode], e0.elapsed_time(e1))
+            del graphs
             best = min(times, key=times.get)
             for p in projs:
                 p.mode = best

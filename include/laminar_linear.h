@@ -16,8 +16,9 @@
  * feature: the usual layout of a linear layer's weight), y [M, N] fp32,
  * all row-major and contiguous. Products of bf16 values are exact and are
  * accumulated in fp32 on the matrix cores; with several K splits (over
- * workgroups, or over the four wavefronts of one workgroup for M <= 4) the
- * partial sums are added in a fixed order, so results are deterministic.
+ * workgroups, over the four wavefronts of one workgroup for M <= 4, or the
+ * pieces of the balanced split) the partial sums are added in a fixed
+ * order, so results are deterministic.
  *
  * Packed weights. laminar_linear reads w in a packed layout made once per
  * weight by laminar_linear_pack: 16-row tiles, and within a tile 16-byte
@@ -34,8 +35,14 @@
  * to a general GEMM.
  * Workspace: laminar_linear_workspace_bytes(M, N, K) bytes of device
  * memory (0 when K is not split over workgroups), 256-byte aligned, owned
- * by the caller; calls that share a workspace must be ordered on one
- * stream.
+ * by the caller, zeroed once before its first use (hipMemset): it holds
+ * the partial sums of the K split and, up to 32 rows, one counter per
+ * group of output columns, with which the last workgroup of a group to
+ * finish adds the group's partial sums itself; every call leaves the
+ * counters at zero again, so no clearing is needed between calls (nor in a
+ * captured graph). Calls that share a workspace must be ordered on one
+ * stream. A call that fails part-way (a kernel fault) may leave counters
+ * set: zero the workspace again before reusing it.
  * Pointers: x, w, w_packed and y 16-byte aligned; the caller owns every
  * buffer.
  * Errors: INVALID_ARG (NULL pointers, misalignment, w_packed equal to w, a
@@ -58,12 +65,14 @@ laminar_status laminar_linear_pack(const void* w, void* w_packed, int32_t n,
                                    int32_t k, hipStream_t stream);
 
 /* Number of K ranges the call spreads over workgroups (1: none, also when
- * K is split only among the wavefronts of each workgroup). The same for
- * every kind of x. 0 outside the limits. */
+ * K is split only among the wavefronts of each workgroup); with the
+ * balanced split (from 17 rows, when N / 128 groups would leave the CUs
+ * unevenly loaded), the most pieces any left-over group is cut into. The
+ * same for every kind of x. 0 outside the limits. */
 int32_t laminar_linear_splits(int32_t m, int32_t n, int32_t k);
 
-/* Device workspace bytes for the K splits over workgroups (0 when there
- * are none). */
+/* Device workspace bytes for the K splits over workgroups, or for the
+ * pieces of the balanced split (0 when there are none). */
 size_t laminar_linear_workspace_bytes(int32_t m, int32_t n, int32_t k);
 
 /* y = x w^T with w given in the packed layout. */

@@ -202,7 +202,9 @@ class SkinnyLinear:
                               _stream_handle(stream))
         self.ws_bytes = max(N.laminar_linear_workspace_bytes(m, self.n, self.k)
                             for m in range(1, max_m + 1))
-        self.ws = (torch.empty(self.ws_bytes, dtype=torch.uint8,
+        # zeroed once: the K split's group counters start at zero and every
+        # call leaves them there
+        self.ws = (torch.zeros(self.ws_bytes, dtype=torch.uint8,
                                device=weight.device) if self.ws_bytes else None)
 
     def __call__(self, x, out=None, stream=None):

@@ -26,24 +26,44 @@ rmsnorm_kernel(const bf16x8* __restrict__ x, const bf16x8* __restrict__ w,
   __shared__ float part[4];
   const bf16x8* xr = x + size_t(blockIdx.x) * chunks;
   bf16x8* yr = y + size_t(blockIdx.x) * chunks;
+  // rows of up to 4 x 256 chunks (8192 values) stay in registers from the
+  // sum of squares to the scaling, and their weights are loaded with them:
+  // one trip to memory before the workgroup's reduction instead of two
+  constexpr int kHeld = 4;
+  bf16x8 xv[kHeld], wv[kHeld];
+#pragma unroll
+  for (int h = 0; h < kHeld; ++h) {
+    const int c = threadIdx.x + 256 * h;
+    if (c < chunks) {
+      xv[h] = xr[c];
+      if (w) wv[h] = w[c];
+    }
+  }
   float ss = 0.f;
-  for (int c = threadIdx.x; c < chunks; c += 256) ss = laminar::sumsq8(xr[c], ss);
+#pragma unroll
+  for (int h = 0; h < kHeld; ++h)
+    if (threadIdx.x + 256 * h < chunks) ss = laminar::sumsq8(xv[h], ss);
+  for (int c = threadIdx.x + 256 * kHeld; c < chunks; c += 256)
+    ss = laminar::sumsq8(xr[c], ss);
   ss = laminar::wave_sum(ss);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
   __syncthreads();
   const float r =
       laminar::rms_inverse(part[0], part[1], part[2], part[3], inv_n, eps);
-  for (int c = threadIdx.x; c < chunks; c += 256) {
-    const bf16x8 v = xr[c];
-    if (w) {
-      yr[c] = laminar::rms_scale8(v, w[c], r);
-    } else {
-      bf16x8 o;
+  auto scale = [&](const bf16x8& v, const bf16x8* wc) {
+    if (wc) return laminar::rms_scale8(v, *wc, r);
+    bf16x8 o;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = (__bf16)(float(v[e]) * r);
-      yr[c] = o;
-    }
+    for (int e = 0; e < 8; ++e) o[e] = (__bf16)(float(v[e]) * r);
+    return o;
+  };
+#pragma unroll
+  for (int h = 0; h < kHeld; ++h) {
+    const int c = threadIdx.x + 256 * h;
+    if (c < chunks) yr[c] = scale(xv[h], w ? &wv[h] : nullptr);
   }
+  for (int c = threadIdx.x + 256 * kHeld; c < chunks; c += 256)
+    yr[c] = scale(xr[c], w ? &w[c] : nullptr);
 }
 
 // Eight outputs per thread: y[m, i..i+7] from gate gu[m, i..] and up

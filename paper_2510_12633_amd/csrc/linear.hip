@@ -99,6 +99,7 @@ struct LinearArgs {
   uint16_t* yb;          // [M, N] bf16 output (rounded to nearest even)
   const uint16_t* res;   // [M, N] bf16 residual added before rounding, or NULL
   float* part;           // [splits, M, N] when split; balanced: [2 W, M, 128]
+  int* counters;         // per group: pieces written so far (split only)
   int32_t m, n, k;
   int32_t n_tiles, splits, steps_per_split;
   // balanced split: each of W workgroups streams full_rounds whole groups
@@ -225,6 +226,104 @@ __device__ __forceinline__ float row_rms_inverse(const LinearArgs& a,
   return row < a.m ? r : 0.f;
 }
 
+// Device-scope cache policy (SC1): a store with it is written through the
+// XCD's L2 to memory, and a load with it is served from memory, not from a
+// line a previous call left in the L2 -- the policy the compiler gives
+// agent-scope atomic loads and stores. The partial sums of a K split take
+// it both ways, so no L2 write-back or invalidation (a device-scope fence,
+// about 30 us per call here) is needed to hand them between workgroups.
+constexpr int kDevScope = 16;
+
+// The partial sums of a K split as a buffer (at most 256 ranges x 128
+// columns per group x 128 rows: far below 2 GiB).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t part_rsrc(const LinearArgs& a,
+                                                            int pieces) {
+  return __builtin_amdgcn_make_buffer_rsrc(
+      a.part, 0, int(size_t(pieces) * a.m * a.n * sizeof(float)), kBufFlags);
+}
+
+// f32x4 store of a partial sum at float index off of a.part, device scope
+__device__ __forceinline__ void store_part(__amdgpu_buffer_rsrc_t pr, size_t off,
+                                           f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), pr,
+                                         int(off * sizeof(float)), 0, kDevScope);
+}
+
+// Up to 32 rows, the last of a group's K ranges to finish adds them all (in
+// range order) and writes the group's outputs, so no second kernel runs: at
+// decode batch sizes each launch costs about 5 us, as much as the sum
+// itself. (From 33 rows one workgroup reading every range of its group,
+// 229 KB for 64 rows of QKV, took longer than linear_reduce, which spreads
+// the sum over the GPU.) Each
+// thread waits for its device-scope partial stores to complete before the
+// workgroup counts its range in, with one atomic on the group's counter;
+// the workgroup that completes the count reads every range with
+// device-scope loads, and leaves the counter at zero for the next call.
+// cols outputs per row from n0.
+__device__ __forceinline__ void finish_group(const LinearArgs& a, int group,
+                                             int pieces, int n0, int cols,
+                                             int threads) {
+  __shared__ int s_last;
+  __builtin_amdgcn_s_waitcnt(0);          // this thread's stores are done
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int done = __hip_atomic_fetch_add(a.counters + group, 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    s_last = done == pieces - 1;
+    if (done == pieces - 1)
+      __hip_atomic_store(a.counters + group, 0, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  const size_t total = size_t(a.m) * a.n;
+  const __amdgpu_buffer_rsrc_t pr = part_rsrc(a, pieces);
+  const int c4n = cols / 4;
+  for (int idx = threadIdx.x; idx < a.m * c4n; idx += threads) {
+    const int m = idx / c4n;
+    const int n = n0 + 4 * (idx - m * c4n);
+    if (n >= a.n) continue;
+    const size_t i = size_t(m) * a.n + n;
+    f32x4 v[8];
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < pieces; k0 += 8) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        v[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                   pr, k0 + j < pieces ? int(((k0 + j) * total + i) * sizeof(float)) : kOob,
+                   0, kDevScope));
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (k0 + j == 0) s = v[0];
+        else if (k0 + j < pieces) s += v[j];
+      }
+    }
+    store4(a, i, s);
+  }
+}
+
+// y[m, n] = sum over splits s (in order) of part[s, m, n], then the output
+// epilogue; four n per thread. Eight partial sums are loaded before the
+// first add.
+__global__ void __launch_bounds__(256) linear_reduce(const LinearArgs a) {
+  const size_t i = size_t(blockIdx.x) * 256 + threadIdx.x;    // float4 index
+  const size_t total = size_t(a.m) * a.n / 4;
+  if (i >= total) return;
+  const f32x4* p = reinterpret_cast<const f32x4*>(a.part);
+  f32x4 s = p[i];
+  for (int k0 = 1; k0 < a.splits; k0 += 8) {
+    f32x4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      v[j] = k0 + j < a.splits ? p[size_t(k0 + j) * total + i]
+                               : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (k0 + j < a.splits) s += v[j];
+  }
+  store4(a, 4 * i, s);
+}
+
 template <int MT, int XK>
 __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
   // x of one step, double-buffered: chunk (t, k/8 = c, row r) at
@@ -332,6 +431,8 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
   }
 
   // lane (group q, column r16) holds D[16 tile + 4q + r][m = 16t + r16]
+  constexpr bool kFinishInKernel = MT <= 2;
+  const __amdgpu_buffer_rsrc_t pr = part_rsrc(a, a.splits);
 #pragma unroll
   for (int tt = 0; tt < TW; ++tt) {
     const int tile = tile0 + tt;
@@ -341,13 +442,17 @@ __global__ void __launch_bounds__(256) linear_kernel(const LinearArgs a) {
       const int m = 16 * t + r16;
       if (m >= a.m) continue;
       const size_t off = size_t(m) * a.n + tile * 16 + 4 * q;
-      if (a.splits > 1)
+      if (a.splits == 1)
+        store4(a, off, acc[tt][t]);
+      else if (kFinishInKernel)
+        store_part(pr, size_t(split) * a.m * a.n + off, acc[tt][t]);
+      else
         *reinterpret_cast<f32x4*>(a.part + size_t(split) * a.m * a.n + off) =
             acc[tt][t];
-      else
-        store4(a, off, acc[tt][t]);
     }
   }
+  if (kFinishInKernel && a.splits > 1)
+    finish_group(a, blockIdx.x, a.splits, blockIdx.x * 64 * TW, 64 * TW, 256);
 }
 
 
@@ -570,8 +675,9 @@ __global__ void __launch_bounds__(512) linear_balanced_kernel(const LinearArgs a
 
 // Adds the pieces of each left-over group in workgroup order (the order of
 // K), then the output epilogue; four outputs per thread. The pieces of a
-// group come from consecutive workgroups; eight loads go out before the
-// first add.
+// group come from consecutive workgroups; sixteen candidates (a group's
+// pieces when W / rem_groups is at most 13) are loaded before the first
+// add.
 __global__ void __launch_bounds__(256) linear_balance_reduce(const LinearArgs a) {
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
   const int per_group = a.m * (kWideTiles * 4);
@@ -589,11 +695,11 @@ __global__ void __launch_bounds__(256) linear_balance_reduce(const LinearArgs a)
   const int w_hi = min(W - 1, ((rg + 1) * W + rgs - 1) / rgs);
   f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
   int64_t s0 = rem_start(w_lo, ru, W);
-  for (int w = w_lo; w <= w_hi; w += 8) {
-    f32x4 v[8];
-    bool use[8];
+  for (int w = w_lo; w <= w_hi; w += 16) {
+    f32x4 v[16];
+    bool use[16];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < 16; ++j) {
       const int ww = w + j;
       const int64_t s1 = rem_start(ww + 1, ru, W);
       // workgroup ww has units [s0, s1); group rg is its second piece when
@@ -606,7 +712,7 @@ __global__ void __launch_bounds__(256) linear_balance_reduce(const LinearArgs a)
       s0 = s1;
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < 16; ++j)
       if (use[j]) sum += v[j];
   }
   store4(a, size_t(m) * a.n + n, sum);
@@ -692,18 +798,6 @@ __global__ void __launch_bounds__(256) linear_wave_split_kernel(const LinearArgs
   acc += part[1][lane];
   acc += part[2][lane];
   if (r16 < a.m) store4(a, size_t(r16) * a.n + tile * 16 + 4 * q, acc);
-}
-
-// y[m, n] = sum over splits s (in order) of part[s, m, n], then the output
-// epilogue; four n per thread.
-__global__ void __launch_bounds__(256) linear_reduce(const LinearArgs a) {
-  const size_t i = size_t(blockIdx.x) * 256 + threadIdx.x;    // float4 index
-  const size_t total = size_t(a.m) * a.n / 4;
-  if (i >= total) return;
-  const f32x4* p = reinterpret_cast<const f32x4*>(a.part);
-  f32x4 s = p[i];
-  for (int k = 1; k < a.splits; ++k) s += p[size_t(k) * total + i];
-  store4(a, 4 * i, s);
 }
 
 // w [N, K] -> packed [N/16][K/8][16][8]: one 16-byte chunk per thread,
@@ -817,6 +911,18 @@ int32_t balanced_pieces(const BalancedPlan& b, int32_t k) {
   return most;
 }
 
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+// The group split's workspace: the partial sums, then one counter per group.
+size_t split_part_bytes(int32_t m, int32_t n, int32_t splits) {
+  return align256(size_t(splits) * m * n * sizeof(float));
+}
+
+int32_t split_groups(int32_t m, int32_t n) {
+  const int32_t per_group = launch_tiles(m) >= 4 ? 8 : 4;
+  return (n / 16 + per_group - 1) / per_group;
+}
+
 bool misaligned16(const void* p) {
   return reinterpret_cast<uintptr_t>(p) & 15;
 }
@@ -875,7 +981,8 @@ hipError_t launch(const LinearArgs& a, const SplitPlan& plan, bool balanced,
     }
   }
   hipError_t e = hipGetLastError();
-  if (e == hipSuccess && a.splits > 1) {
+  // from 33 rows the partial sums are added by a second kernel
+  if (e == hipSuccess && a.splits > 1 && launch_tiles(m) >= 4) {
     const size_t total = size_t(m) * a.n / 4;
     hipLaunchKernelGGL(linear_reduce, dim3(unsigned((total + 255) / 256)),
                        dim3(256), 0, stream, a);
@@ -927,12 +1034,16 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
   a.full_rounds = bal.full_rounds;
   a.rem_groups = bal.rem_groups;
   a.part = nullptr;
+  a.counters = nullptr;
   if (a.splits > 1 || (bal.use && bal.rem_groups > 0)) {
     const size_t need = laminar_linear_workspace_bytes(m, n, k);
     if (!workspace || workspace_bytes < need ||
         (reinterpret_cast<uintptr_t>(workspace) & 255))
       return LAMINAR_ERR_INVALID_ARG;
     a.part = static_cast<float*>(workspace);
+    if (a.splits > 1)
+      a.counters = reinterpret_cast<int*>(static_cast<char*>(workspace) +
+                                          split_part_bytes(m, n, a.splits));
   }
   hipError_t e;
   if (x_kind == kXF32)
@@ -977,8 +1088,9 @@ size_t laminar_linear_workspace_bytes(int32_t m, int32_t n, int32_t k) {
   if (b.use)
     bytes = b.rem_groups ? size_t(2) * b.wgs * m * kWideTiles * 16 * sizeof(float) : 0;
   else if (p.splits > 1)
-    bytes = size_t(p.splits) * m * n * sizeof(float);
-  return (bytes + 255) & ~size_t(255);
+    bytes = split_part_bytes(m, n, p.splits) +
+            align256(size_t(split_groups(m, n)) * sizeof(int32_t));
+  return align256(bytes);
 }
 
 laminar_status laminar_linear(const void* x, const void* w_packed, float* y,

@@ -181,3 +181,33 @@ def test_fused_norm_equals_rmsnorm_then_linear(m, n, k):
         assert torch.equal(bits_t(a), bits_t(b))
         assert torch.equal(bits_t(ra), bits_t(rb))
         assert torch.isfinite(a.float()).all()
+
+
+@pytest.mark.parametrize("m,n,k", [(16, 4608, 3584), (64, 3584, 18944),
+                                   (64, 37888, 512), (5, 3584, 3584)])
+def test_back_to_back_calls_share_the_workspace(m, n, k):
+    """Calls queued back to back on one stream reuse one workspace: the
+    partial sums of a K split and the per-group counters. Each of six calls
+    with different x (and the fused kinds in between) must equal its own
+    product: a partial sum left from the call before, or a counter not
+    returned to zero, would show up as a wrong output."""
+    from paper_2510_12633_amd.api import SkinnyLinear
+    _need_gpu()
+    print(f"[gpu-linear-reuse] m={m} n={n} k={k}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(5 * m + n + k)
+    w = (torch.randn((n, k), generator=g, device="cuda") / k ** 0.5).to(torch.bfloat16)
+    lin = SkinnyLinear(w)
+    xs = [torch.randn((m, k), generator=g, device="cuda").to(torch.bfloat16)
+          for _ in range(6)]
+    ys = [torch.full((m, n), float("nan"), device="cuda") for _ in xs]
+    refs = []
+    for i, (x, y) in enumerate(zip(xs, ys)):
+        lin(x, out=y)
+        if i % 2:
+            lin.bf16(x.float())                   # fp32 x, same workspace
+    torch.cuda.synchronize()
+    for x, y in zip(xs, ys):
+        ref = (x.float() @ w.float().t())
+        tol = 1e-5 * (x.float().abs() @ w.float().abs().t()) + 1e-6
+        assert bool(((y - ref).abs() <= tol).all()), (m, n, k)
+    assert torch.equal(ys[0], lin(xs[0]))
