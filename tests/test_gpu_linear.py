@@ -211,3 +211,42 @@ def test_back_to_back_calls_share_the_workspace(m, n, k):
         tol = 1e-5 * (x.float().abs() @ w.float().abs().t()) + 1e-6
         assert bool(((y - ref).abs() <= tol).all()), (m, n, k)
     assert torch.equal(ys[0], lin(xs[0]))
+
+
+@pytest.mark.parametrize("m,n,k", [(16, 4608, 3584), (32, 3584, 18944),
+                                   (64, 37888, 512), (64, 3584, 3584)])
+def test_graph_replays_equal_the_eager_call(m, n, k):
+    """The product captured in a HIP graph and replayed four times, with
+    eager calls on the same workspace between the replays: every replay
+    equals the eager result bit for bit (the K split's counters return to
+    zero in every call, so a replay starts from the state the capture saw;
+    nothing in the call is a memset)."""
+    from paper_2510_12633_amd.api import SkinnyLinear
+    _need_gpu()
+    print(f"[gpu-linear-graph] m={m} n={n} k={k}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(3 * m + n + k)
+    w = (torch.randn((n, k), generator=g, device="cuda") / k ** 0.5).to(torch.bfloat16)
+    lin = SkinnyLinear(w)
+    x = torch.randn((m, k), generator=g, device="cuda").to(torch.bfloat16)
+    x2 = torch.randn((m, k), generator=g, device="cuda").to(torch.bfloat16)
+    res = torch.randn((m, n), generator=g, device="cuda").to(torch.bfloat16)
+    eager = lin.bf16(x, residual=res)
+    torch.cuda.synchronize()
+    out = torch.empty_like(eager)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        lin.bf16(x, out=out, residual=res)            # warm on the side stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        lin.bf16(x, out=out, residual=res)
+    for i in range(4):
+        out.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(bits_t(out), bits_t(eager)), (m, n, k, i)
+        other = lin.bf16(x2, residual=res)           # eager, same workspace
+        torch.cuda.synchronize()
+        assert torch.isfinite(other.float()).all()
