@@ -230,14 +230,19 @@ laminar_status build(const laminar_attn_desc* desc, const int32_t* lens,
     // 7b_pre_repack and 0.2% on the 32B workload. A batch of long units
     // only (post_repack) keeps equal pieces and no tail, which halves made
     // 3-7% slower, and so do cascade plans, which have no dynamic tail
-    // (halves made the agentic mixes 0.5-1% slower).
+    // (halves made the agentic mixes 0.5-1% slower). Nor do batches with
+    // more than 4 kv-heads: the kv-heads of a page share its fp8 scale and
+    // block-table lines, which the XCD-grouped order keeps in one L2, and
+    // the dynamic tail hands its items to any XCD (the 32B workload, 8
+    // kv-heads: 1.017 x the algorithmic HBM bytes with halves, 1.010
+    // without, for 0.2% of time).
     bool has_short = false, has_long = false;
     for (int32_t b = 0; b < B && chunks.empty(); ++b) {
       const int64_t own = int64_t(pages[size_t(b)]) - first[size_t(b)];
       has_short |= own > 0 && 2 * own < chunk;
       has_long |= own > chunk;
     }
-    if (has_short && has_long) {
+    if (has_short && has_long && hkv <= 4) {
       halves = true;
       chunk = chunk_for(laminar_detail::kMixedItemsPerSlot, 1);
     }
