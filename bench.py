@@ -472,25 +472,45 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             del nk
             self.mode = "library"
 
-        def __call__(self, x, residual=None, swiglu=False, norm=None):
+        def __call__(self, x, residual=None, swiglu=False, norm=None,
+                     operand=None, next_norm=None, swiglu_out=False):
             """bf16(x w^T), plus residual when given (in place into it on
             the skinny path). fp32 x is rounded to bf16; with swiglu, x
             [M, 2K] is SwiGLU's gate and up; with norm (a [K] weight), the
-            operand is the RMS norm of x."""
-            if self.mode == "fused":
-                return self.skinny.bf16(x, out=residual, residual=residual,
-                                        swiglu=swiglu, norm_weight=norm)
+            operand is the RMS norm of x, unless `operand` hands it over
+            already made (by the producer's reduction). With next_norm (a
+            [N] weight) it returns (y, rmsnorm(y)) and with swiglu_out (y,
+            SwiGLU of y's halves); the skinny kernel makes the second in its
+            reduction launch where it has one, the other ways return None
+            for it."""
+            pair = next_norm is not None or swiglu_out
+            mode = self.mode
+            if operand is not None:
+                x, swiglu, norm = operand, False, None
+                mode = "skinny" if mode == "fused" else mode
+            if mode == "fused":           # the operand made on load
+                if next_norm is not None:
+                    return self.skinny.bf16_norm(x, next_norm, out=residual,
+                                                 residual=residual,
+                                                 swiglu=swiglu)
+                y = self.skinny.bf16(x, out=residual, residual=residual,
+                                     swiglu=swiglu, norm_weight=norm)
+                return (y, None) if pair else y
             if swiglu:
                 x = silu_mul(x)
             elif norm is not None:
                 x = rmsnorm(x, norm)
             elif x.dtype != bf:
                 x = x.to(bf)
-            if self.mode == "skinny":
+            if mode == "skinny":
+                if next_norm is not None:
+                    return self.skinny.bf16_norm(x, next_norm, out=residual,
+                                                 residual=residual)
+                if swiglu_out:
+                    return self.skinny.bf16_swiglu(x)
                 return self.skinny.bf16(x, out=residual, residual=residual)
-            if residual is None:
-                return x @ self.kn
-            return torch.addmm(residual, x, self.kn)
+            y = x @ self.kn if residual is None else torch.addmm(residual, x, self.kn)
+            return (y, None) if pair else y
 
     layers = [(Proj(h, (hq + 2 * hkv) * d), Proj(hq * d, h),
                Proj(h, 2 * inter), Proj(inter, h)) for _ in range(L)]
@@ -589,22 +609,45 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             out, lse = att.outputs()
             x0 = torch.randn((m, h), generator=gen, device="cuda", dtype=bf)
 
+            # Steps handed from a projection's reduction to the next
+            # projection: the RMS norm after O (for gate+up) and after down
+            # (for the next QKV or the LM head) unless the consumer makes it
+            # on load, and SwiGLU after gate+up unless down makes it on load.
+            wq0, wo0, wg0, wd0 = layers[0]
+            norm_after_o = wg0.mode != "fused"
+            norm_after_down = wq0.mode != "fused" and lm_head.mode != "fused"
+            swiglu_after_gu = wg0.mode == "skinny" and wd0.mode != "fused"
+
             def step():
                 cur = torch.cuda.current_stream()
                 x = x0.clone()                    # the residual stream
+                xn = None                         # its RMS norm, when made
 
                 for li, (wqkv, wo, wgu, wd) in enumerate(layers):
-                    qkv = wqkv(x, norm=norms[2 * li])
+                    qkv = wqkv(x, norm=norms[2 * li], operand=xn)
                     # q, k and v are read in place from the fused output
                     q = qkv[:, :hq * d].view(m, hq, d)
                     k_new = qkv[:, hq * d:(hq + hkv) * d].view(m, hkv, d)
                     v_new = qkv[:, (hq + hkv) * d:].view(m, hkv, d)
                     kv_append(k_new, v_new, table, lens, kp, vp, stream=cur)
                     att(q, kp, vp, table, lens, out, lse, stream=cur)
-                    x = wo(out.view(m, hq * d), residual=x)
-                    gu = wgu(x, norm=norms[2 * li + 1])
-                    x = wd(gu, residual=x, swiglu=True)
-                return lm_head(x, norm=norms[2 * L])
+                    if norm_after_o:
+                        x, xn = wo(out.view(m, hq * d), residual=x,
+                                   next_norm=norms[2 * li + 1])
+                    else:
+                        x, xn = wo(out.view(m, hq * d), residual=x), None
+                    if swiglu_after_gu:
+                        gu, act = wgu(x, norm=norms[2 * li + 1], operand=xn,
+                                      swiglu_out=True)
+                    else:
+                        gu, act = wgu(x, norm=norms[2 * li + 1], operand=xn), None
+                    nxt = norms[2 * li + 2]        # next QKV's, or the final
+                    if norm_after_down:
+                        x, xn = wd(gu, residual=x, swiglu=True, operand=act,
+                                   next_norm=nxt)
+                    else:
+                        x, xn = wd(gu, residual=x, swiglu=True, operand=act), None
+                return lm_head(x, norm=norms[2 * L], operand=xn)
 
             # The step is ~400 launches: capture it in a HIP graph so the
             # curve shows the GPU's time, not the host's launch rate.

@@ -117,6 +117,42 @@ laminar_status laminar_linear_bf16_ex(const void* x, int32_t x_kind,
                                       size_t workspace_bytes,
                                       hipStream_t stream);
 
+/* laminar_linear_bf16_ex followed by the RMS norm of each row of its
+ * output: y as laminar_linear_bf16_ex writes it, and y_norm [M, N] bf16
+ * equal bit for bit to laminar_rmsnorm(y, norm_weight, eps) (norm_weight
+ * [N] bf16 or NULL). In a decode step the O and down projections write
+ * the residual stream and the next RMS norm reads it: from 33 rows, where
+ * K is split and a second kernel adds the ranges, that kernel also makes
+ * the norm (one launch fewer); otherwise the norm is a laminar_rmsnorm
+ * launch of its own. y_norm and norm_weight are 16-byte aligned; y_norm
+ * must not overlap y. Errors as laminar_linear_bf16_ex, plus INVALID_ARG
+ * for a NULL or misaligned y_norm, a misaligned norm_weight, or eps
+ * negative or not finite. */
+laminar_status laminar_linear_bf16_norm(const void* x, int32_t x_kind,
+                                        const void* w_packed, void* y,
+                                        const void* residual,
+                                        const void* norm_weight, float eps,
+                                        void* y_norm, int32_t m, int32_t n,
+                                        int32_t k, void* workspace,
+                                        size_t workspace_bytes,
+                                        hipStream_t stream);
+
+/* laminar_linear_bf16_ex (no residual) followed by SwiGLU of its output's
+ * halves: y [M, N] bf16 as laminar_linear_bf16_ex writes it, and y_act
+ * [M, N / 2] bf16 equal bit for bit to laminar_silu_mul(y) (gate columns
+ * 0 .. N/2 - 1, up columns N/2 .. N - 1). For the gate and up projection:
+ * when the call takes the balanced split with groups left over, its
+ * reduction kernel also makes SwiGLU (one launch fewer); otherwise
+ * SwiGLU is a laminar_silu_mul launch of its own. y_act is 16-byte aligned
+ * and must not overlap y. Errors as laminar_linear_bf16_ex, plus
+ * INVALID_ARG for a NULL or misaligned y_act. */
+laminar_status laminar_linear_bf16_swiglu(const void* x, int32_t x_kind,
+                                          const void* w_packed, void* y,
+                                          void* y_act, int32_t m, int32_t n,
+                                          int32_t k, void* workspace,
+                                          size_t workspace_bytes,
+                                          hipStream_t stream);
+
 /* laminar_linear_bf16 on RMS-normalised rows, the norm done on load:
  * the operand is bf16((x[m, k] r_m) norm_weight[k]) with
  * r_m = 1 / sqrt(mean_k x[m, k]^2 + eps), the pre-norm of a decoder layer

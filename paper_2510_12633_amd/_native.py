@@ -136,6 +136,15 @@ _SIGNATURES = {
                                          c_void_p, c_void_p, c_int32, c_int32,
                                          c_int32, c_void_p, c_size_t,
                                          c_void_p]),
+    "laminar_linear_bf16_norm": (c_int32, [c_void_p, c_int32, c_void_p,
+                                           c_void_p, c_void_p, c_void_p,
+                                           ctypes.c_float, c_void_p, c_int32,
+                                           c_int32, c_int32, c_void_p,
+                                           c_size_t, c_void_p]),
+    "laminar_linear_bf16_swiglu": (c_int32, [c_void_p, c_int32, c_void_p,
+                                             c_void_p, c_void_p, c_int32,
+                                             c_int32, c_int32, c_void_p,
+                                             c_size_t, c_void_p]),
     "laminar_linear_bf16_rmsnorm": (c_int32, [c_void_p, c_void_p,
                                               ctypes.c_float, c_void_p,
                                               c_void_p, c_void_p, c_int32,
@@ -429,6 +438,25 @@ def laminar_linear_bf16_ex(x, x_kind: int, w_packed, y, residual, m: int,
                                         int(n), int(k), _ptr(workspace),
                                         int(workspace_bytes), _ptr(stream)),
            "laminar_linear_bf16_ex")
+
+
+def laminar_linear_bf16_norm(x, x_kind: int, w_packed, y, residual,
+                             norm_weight, eps: float, y_norm, m: int, n: int,
+                             k: int, workspace, workspace_bytes: int, stream):
+    _check(lib().laminar_linear_bf16_norm(
+        _ptr(x), int(x_kind), _ptr(w_packed), _ptr(y), _ptr(residual),
+        _ptr(norm_weight), float(eps), _ptr(y_norm), int(m), int(n), int(k),
+        _ptr(workspace), int(workspace_bytes), _ptr(stream)),
+        "laminar_linear_bf16_norm")
+
+
+def laminar_linear_bf16_swiglu(x, x_kind: int, w_packed, y, y_act, m: int,
+                               n: int, k: int, workspace, workspace_bytes: int,
+                               stream):
+    _check(lib().laminar_linear_bf16_swiglu(
+        _ptr(x), int(x_kind), _ptr(w_packed), _ptr(y), _ptr(y_act), int(m),
+        int(n), int(k), _ptr(workspace), int(workspace_bytes), _ptr(stream)),
+        "laminar_linear_bf16_swiglu")
 
 
 def laminar_linear_bf16_rmsnorm(x, norm_weight, eps: float, w_packed, y,

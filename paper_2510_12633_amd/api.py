@@ -258,6 +258,52 @@ class SkinnyLinear:
                                  _stream_handle(stream))
         return out
 
+    def _kind(self, x, swiglu):
+        if swiglu:
+            kind, want = N.LAMINAR_X_SILU_MUL, (torch.bfloat16, 2 * self.k)
+        elif x.dtype == torch.float32:
+            kind, want = N.LAMINAR_X_F32, (torch.float32, self.k)
+        else:
+            kind, want = N.LAMINAR_X_BF16, (torch.bfloat16, self.k)
+        if (x.dtype, x.shape[1]) != want or not x.is_contiguous():
+            raise ValueError(f"x must be contiguous {want[0]} [M, {want[1]}]")
+        return kind
+
+    def bf16_norm(self, x, norm_weight, eps: float = 1e-6, out=None,
+                  residual=None, out_norm=None, swiglu=False, stream=None):
+        """(y, rmsnorm(y, norm_weight, eps)) with y = bf16(x w^T + residual)
+        as bf16() computes it (x may be fp32 or, with swiglu, gate and up);
+        the norm equals laminar_rmsnorm on y bit for bit and, where K is
+        split (from 33 rows), comes from the same reduction launch."""
+        m = x.shape[0]
+        kind = self._kind(x, swiglu)
+        if out is None:
+            out = torch.empty((m, self.n), dtype=torch.bfloat16, device=x.device)
+        if out_norm is None:
+            out_norm = torch.empty((m, self.n), dtype=torch.bfloat16,
+                                   device=x.device)
+        N.laminar_linear_bf16_norm(x, kind, self.w_packed, out, residual,
+                                   norm_weight, eps, out_norm, m, self.n,
+                                   self.k, self.ws, self.ws_bytes,
+                                   _stream_handle(stream))
+        return out, out_norm
+
+    def bf16_swiglu(self, x, out=None, out_act=None, stream=None):
+        """(y, silu(y[:, :N/2]) * y[:, N/2:]) with y = bf16(x w^T); the
+        second equals laminar_silu_mul on y bit for bit and, with the
+        balanced split, comes from the same reduction launch."""
+        m = x.shape[0]
+        kind = self._kind(x, False)
+        if out is None:
+            out = torch.empty((m, self.n), dtype=torch.bfloat16, device=x.device)
+        if out_act is None:
+            out_act = torch.empty((m, self.n // 2), dtype=torch.bfloat16,
+                                  device=x.device)
+        N.laminar_linear_bf16_swiglu(x, kind, self.w_packed, out, out_act, m,
+                                     self.n, self.k, self.ws, self.ws_bytes,
+                                     _stream_handle(stream))
+        return out, out_act
+
 
 def rmsnorm(x, weight=None, eps: float = 1e-6, out=None, stream=None):
     """Row-wise RMS norm of bf16 x [M, N] (times weight [N]) -> bf16."""

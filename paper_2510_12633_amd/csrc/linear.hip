@@ -50,6 +50,7 @@
 #include <cstdint>
 
 #include "activation.h"
+#include "laminar_decode_step.h"
 #include "laminar_linear.h"
 
 namespace {
@@ -105,7 +106,16 @@ struct LinearArgs {
   // balanced split: each of W workgroups streams full_rounds whole groups
   // of eight tiles, then an equal share of the rem_groups left over
   int32_t wgs, full_rounds, rem_groups;
+  // A step after the product that its reduction kernel makes when the call
+  // has one: the RMS norm of each row of y (kPostNorm), or SwiGLU of y's
+  // halves (kPostSwiGlu), into post_out.
+  int32_t post_kind;
+  const uint16_t* post_norm_w;   // [N] norm weight, or NULL
+  float post_norm_inv_n, post_norm_eps;
+  uint16_t* post_out;            // [M, N] or [M, N / 2] bf16
 };
+
+constexpr int kPostNone = 0, kPostNorm = 1, kPostSwiGlu = 2;
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
@@ -718,6 +728,66 @@ __global__ void __launch_bounds__(256) linear_balance_reduce(const LinearArgs a)
   store4(a, size_t(m) * a.n + n, sum);
 }
 
+// Columns col .. col+7 of row m of a balanced call's bf16 output: read back
+// when their group was whole (its workgroup wrote them), else the group's
+// pieces added in workgroup order and rounded as linear_balance_reduce does
+// (and written to y, which the call also returns).
+__device__ __forceinline__ bf16x8 balanced_chunk8(const LinearArgs& a, int m, int col) {
+  const int W = a.wgs;
+  const int g = col / (kWideTiles * 16);
+  const int gf = a.full_rounds * W;
+  uint16_t* y8 = a.yb + size_t(m) * a.n + col;
+  if (g < gf) return *reinterpret_cast<const bf16x8*>(y8);
+  const int rg = g - gf, rgs = a.rem_groups;
+  const int S = a.k / kStepK;
+  const int64_t ru = int64_t(rgs) * S;
+  const int64_t u = int64_t(rg) * S, u_end = u + S;
+  const int w_lo = max(0, rg * W / rgs - 1);
+  const int w_hi = min(W - 1, ((rg + 1) * W + rgs - 1) / rgs);
+  const int c0 = col - g * kWideTiles * 16;
+  f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+  int64_t st0 = rem_start(w_lo, ru, W);
+  for (int w = w_lo; w <= w_hi; w += 8) {
+    f32x4 v[8][2];
+    bool use[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int ww = w + j;
+      const int64_t st1 = rem_start(ww + 1, ru, W);
+      use[j] = ww <= w_hi && st1 > st0 && st0 < u_end && st1 > u;
+      const size_t slot = size_t(2 * ww + (st0 < u ? 1 : 0));
+      const float* q = a.part + (slot * a.m + m) * (kWideTiles * 16) + c0;
+      v[j][0] = use[j] ? *reinterpret_cast<const f32x4*>(q) : f32x4{0.f, 0.f, 0.f, 0.f};
+      v[j][1] = use[j] ? *reinterpret_cast<const f32x4*>(q + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+      st0 = st1;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (use[j]) {
+        s0 += v[j][0];
+        s1 += v[j][1];
+      }
+  }
+  const bf16x8 o{(__bf16)s0[0], (__bf16)s0[1], (__bf16)s0[2], (__bf16)s0[3],
+                 (__bf16)s1[0], (__bf16)s1[1], (__bf16)s1[2], (__bf16)s1[3]};
+  *reinterpret_cast<bf16x8*>(y8) = o;
+  return o;
+}
+
+// The balanced split's reduction followed by SwiGLU of y's halves (gate
+// columns 0 .. N/2 - 1, up columns N/2 ..): post_out exactly as
+// laminar_silu_mul computes it from y, eight outputs per thread, in one
+// launch instead of two.
+__global__ void __launch_bounds__(256) linear_balance_reduce_swiglu(const LinearArgs a) {
+  const int inter = a.n / 2, c8 = inter / 8;
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= int64_t(a.m) * c8) return;
+  const int m = int(i / c8), j = int(i - int64_t(m) * c8) * 8;
+  const bf16x8 g = balanced_chunk8(a, m, j);
+  const bf16x8 u = balanced_chunk8(a, m, inter + j);
+  *reinterpret_cast<bf16x8*>(a.post_out + size_t(m) * inter + j) = laminar::silu_mul8(g, u);
+}
+
 // One 16-row tile per workgroup, K split over its four wavefronts: wave w
 // takes steps w, w + 4, w + 8, ... The sums of the four are added in LDS in
 // wavefront order, so the result does not depend on timing. x has at most
@@ -798,6 +868,90 @@ __global__ void __launch_bounds__(256) linear_wave_split_kernel(const LinearArgs
   acc += part[1][lane];
   acc += part[2][lane];
   if (r16 < a.m) store4(a, size_t(r16) * a.n + tile * 16 + 4 * q, acc);
+}
+
+// Columns 8c .. 8c+7 of row m as the group split's reduction writes them:
+// the ranges added in order (all loads in flight first), then store4's
+// epilogue (the residual, one rounding to bf16).
+__device__ __forceinline__ bf16x8 reduce_chunk8(const LinearArgs& a, int m, int c) {
+  const size_t total4 = size_t(a.m) * a.n / 4;
+  const f32x4* p = reinterpret_cast<const f32x4*>(a.part);
+  const size_t off = size_t(m) * a.n + 8 * c;
+  const size_t i = off / 4;
+  f32x4 s0 = p[i], s1 = p[i + 1];
+  for (int k0 = 1; k0 < a.splits; k0 += 8) {
+    f32x4 v[8][2];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool in = k0 + j < a.splits;
+      v[j][0] = in ? p[size_t(k0 + j) * total4 + i] : f32x4{0.f, 0.f, 0.f, 0.f};
+      v[j][1] = in ? p[size_t(k0 + j) * total4 + i + 1] : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (k0 + j < a.splits) {
+        s0 += v[j][0];
+        s1 += v[j][1];
+      }
+  }
+  if (a.res) {
+    const bf16x4 r0 = *reinterpret_cast<const bf16x4*>(a.res + off);
+    const bf16x4 r1 = *reinterpret_cast<const bf16x4*>(a.res + off + 4);
+    s0 += f32x4{float(r0[0]), float(r0[1]), float(r0[2]), float(r0[3])};
+    s1 += f32x4{float(r1[0]), float(r1[1]), float(r1[2]), float(r1[3])};
+  }
+  return bf16x8{(__bf16)s0[0], (__bf16)s0[1], (__bf16)s0[2], (__bf16)s0[3],
+                (__bf16)s1[0], (__bf16)s1[1], (__bf16)s1[2], (__bf16)s1[3]};
+}
+
+// The group split's reduction for whole rows followed by the RMS norm of
+// each row, one workgroup per row: y exactly as linear_reduce writes it and
+// post_out exactly as laminar_rmsnorm computes it from that y (thread t
+// chains the sums of squares of chunks t, t + 256, ... in one fma, then the
+// same butterfly and sums, the same scaling and rounding), in one launch
+// instead of two.
+__global__ void __launch_bounds__(256) linear_reduce_norm(const LinearArgs a) {
+  __shared__ float part[4];
+  const int m = blockIdx.x;
+  const int chunks = a.n / 8;
+  bf16x8* yr = reinterpret_cast<bf16x8*>(a.yb + size_t(m) * a.n);
+  bf16x8* zr = reinterpret_cast<bf16x8*>(a.post_out + size_t(m) * a.n);
+  const bf16x8* wr = reinterpret_cast<const bf16x8*>(a.post_norm_w);
+  constexpr int kHeld = 4;
+  bf16x8 yv[kHeld];
+  float ss = 0.f;
+#pragma unroll
+  for (int h = 0; h < kHeld; ++h) {
+    const int c = threadIdx.x + 256 * h;
+    if (c < chunks) {
+      yv[h] = reduce_chunk8(a, m, c);
+      yr[c] = yv[h];
+      ss = laminar::sumsq8(yv[h], ss);
+    }
+  }
+  for (int c = threadIdx.x + 256 * kHeld; c < chunks; c += 256) {
+    const bf16x8 v = reduce_chunk8(a, m, c);
+    yr[c] = v;
+    ss = laminar::sumsq8(v, ss);
+  }
+  ss = laminar::wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float r = laminar::rms_inverse(part[0], part[1], part[2], part[3],
+                                       a.post_norm_inv_n, a.post_norm_eps);
+  auto scale = [&](const bf16x8& v, int c) {
+    if (wr) return laminar::rms_scale8(v, wr[c], r);
+    bf16x8 o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (__bf16)(float(v[e]) * r);
+    return o;
+  };
+#pragma unroll
+  for (int h = 0; h < kHeld; ++h) {
+    const int c = threadIdx.x + 256 * h;
+    if (c < chunks) zr[c] = scale(yv[h], c);
+  }
+  for (int c = threadIdx.x + 256 * kHeld; c < chunks; c += 256) zr[c] = scale(yr[c], c);
 }
 
 // w [N, K] -> packed [N/16][K/8][16][8]: one 16-byte chunk per thread,
@@ -932,7 +1086,7 @@ bool misaligned16(const void* p) {
 namespace {
 
 template <int MT, int XK>
-hipError_t launch_balanced(const LinearArgs& a, hipStream_t stream) {
+hipError_t launch_balanced(const LinearArgs& a, hipStream_t stream, bool& post_done) {
   const dim3 grid(a.wgs), block(512);
   if constexpr (XK == kXBf16)
     hipLaunchKernelGGL((linear_balanced_kernel<MT, XK, kBalancedNB, true>), grid,
@@ -942,9 +1096,16 @@ hipError_t launch_balanced(const LinearArgs& a, hipStream_t stream) {
                        grid, block, 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e == hipSuccess && a.rem_groups > 0) {
-    const int64_t total = int64_t(a.rem_groups) * a.m * kWideTiles * 4;
-    hipLaunchKernelGGL(linear_balance_reduce, dim3(unsigned((total + 255) / 256)),
-                       dim3(256), 0, stream, a);
+    if (a.post_kind == kPostSwiGlu) {
+      const int64_t total = int64_t(a.m) * (a.n / 16);
+      hipLaunchKernelGGL(linear_balance_reduce_swiglu,
+                         dim3(unsigned((total + 255) / 256)), dim3(256), 0, stream, a);
+      post_done = true;
+    } else {
+      const int64_t total = int64_t(a.rem_groups) * a.m * kWideTiles * 4;
+      hipLaunchKernelGGL(linear_balance_reduce, dim3(unsigned((total + 255) / 256)),
+                         dim3(256), 0, stream, a);
+    }
     e = hipGetLastError();
   }
   return e;
@@ -952,13 +1113,13 @@ hipError_t launch_balanced(const LinearArgs& a, hipStream_t stream) {
 
 template <int XK>
 hipError_t launch(const LinearArgs& a, const SplitPlan& plan, bool balanced,
-                  int m, hipStream_t stream) {
+                  int m, hipStream_t stream, bool& post_done) {
   if constexpr (XK != kXRmsNorm) {
     if (balanced) {
       switch (launch_tiles(m)) {
-        case 2: return launch_balanced<2, XK>(a, stream);
-        case 4: return launch_balanced<4, XK>(a, stream);
-        default: return launch_balanced<8, XK>(a, stream);
+        case 2: return launch_balanced<2, XK>(a, stream, post_done);
+        case 4: return launch_balanced<4, XK>(a, stream, post_done);
+        default: return launch_balanced<8, XK>(a, stream, post_done);
       }
     }
   }
@@ -981,21 +1142,37 @@ hipError_t launch(const LinearArgs& a, const SplitPlan& plan, bool balanced,
     }
   }
   hipError_t e = hipGetLastError();
-  // from 33 rows the partial sums are added by a second kernel
+  // from 33 rows the partial sums are added by a second kernel, which also
+  // makes the next RMS norm when the call asks for it
   if (e == hipSuccess && a.splits > 1 && launch_tiles(m) >= 4) {
-    const size_t total = size_t(m) * a.n / 4;
-    hipLaunchKernelGGL(linear_reduce, dim3(unsigned((total + 255) / 256)),
-                       dim3(256), 0, stream, a);
+    if (a.post_kind == kPostNorm) {
+      hipLaunchKernelGGL(linear_reduce_norm, dim3(unsigned(m)), dim3(256), 0, stream, a);
+      post_done = true;
+    } else {
+      const size_t total = size_t(m) * a.n / 4;
+      hipLaunchKernelGGL(linear_reduce, dim3(unsigned((total + 255) / 256)),
+                         dim3(256), 0, stream, a);
+    }
     e = hipGetLastError();
   }
   return e;
 }
 
+// What follows the product in one call: nothing, the RMS norm of y, or
+// SwiGLU of y's halves.
+struct PostStep {
+  int32_t kind = kPostNone;
+  const void* norm_w = nullptr;   // RMS norm weight [N], or NULL
+  float eps = 0.f;
+  void* out = nullptr;            // [M, N] or [M, N / 2] bf16
+};
+
 laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
                            float* y, void* yb, const void* res, int32_t m,
                            int32_t n, int32_t k, void* workspace,
                            size_t workspace_bytes, hipStream_t stream,
-                           const void* norm_w = nullptr, float eps = 0.f) {
+                           const void* norm_w = nullptr, float eps = 0.f,
+                           const PostStep& post = PostStep()) {
   if (!x || !w_packed || (!y && !yb)) return LAMINAR_ERR_INVALID_ARG;
   if (x_kind != kXBf16 && x_kind != kXF32 && x_kind != kXSiluMul &&
       x_kind != kXRmsNorm)
@@ -1005,6 +1182,10 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
     return LAMINAR_ERR_INVALID_ARG;
   if (x_kind == kXRmsNorm &&
       (!norm_w || !(eps >= 0.f) || !std::isfinite(eps)))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (post.kind != kPostNone &&
+      (!yb || !post.out || misaligned16(post.out) || misaligned16(post.norm_w) ||
+       (post.kind == kPostNorm && (!(post.eps >= 0.f) || !std::isfinite(post.eps)))))
     return LAMINAR_ERR_INVALID_ARG;
   if (!shape_ok(m, n, k)) return LAMINAR_ERR_UNSUPPORTED;
   if (x_kind == kXRmsNorm && m > kNormMaxM) return LAMINAR_ERR_UNSUPPORTED;
@@ -1033,6 +1214,11 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
   a.wgs = bal.wgs;
   a.full_rounds = bal.full_rounds;
   a.rem_groups = bal.rem_groups;
+  a.post_kind = post.kind;
+  a.post_norm_w = static_cast<const uint16_t*>(post.norm_w);
+  a.post_norm_inv_n = 1.0f / float(n);
+  a.post_norm_eps = post.eps;
+  a.post_out = static_cast<uint16_t*>(post.out);
   a.part = nullptr;
   a.counters = nullptr;
   if (a.splits > 1 || (bal.use && bal.rem_groups > 0)) {
@@ -1046,15 +1232,22 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
                                           split_part_bytes(m, n, a.splits));
   }
   hipError_t e;
+  bool post_done = false;
   if (x_kind == kXF32)
-    e = launch<kXF32>(a, plan, bal.use, m, stream);
+    e = launch<kXF32>(a, plan, bal.use, m, stream, post_done);
   else if (x_kind == kXSiluMul)
-    e = launch<kXSiluMul>(a, plan, bal.use, m, stream);
+    e = launch<kXSiluMul>(a, plan, bal.use, m, stream, post_done);
   else if (x_kind == kXRmsNorm)
-    e = launch<kXRmsNorm>(a, plan, bal.use, m, stream);
+    e = launch<kXRmsNorm>(a, plan, bal.use, m, stream, post_done);
   else
-    e = launch<kXBf16>(a, plan, bal.use, m, stream);
-  return e == hipSuccess ? LAMINAR_OK : LAMINAR_ERR_HIP;
+    e = launch<kXBf16>(a, plan, bal.use, m, stream, post_done);
+  if (e != hipSuccess) return LAMINAR_ERR_HIP;
+  // without a reduction kernel to carry it, the step is its own launch
+  if (post.kind == kPostNorm && !post_done)
+    return laminar_rmsnorm(yb, post.norm_w, post.out, m, n, post.eps, stream);
+  if (post.kind == kPostSwiGlu && !post_done)
+    return laminar_silu_mul(yb, post.out, m, n / 2, stream);
+  return LAMINAR_OK;
 }
 
 }  // namespace
@@ -1121,6 +1314,38 @@ laminar_status laminar_linear_bf16_rmsnorm(const void* x,
   if (!y) return LAMINAR_ERR_INVALID_ARG;
   return linear_impl(x, kXRmsNorm, w_packed, nullptr, y, residual, m, n, k,
                      workspace, workspace_bytes, stream, norm_weight, eps);
+}
+
+laminar_status laminar_linear_bf16_norm(const void* x, int32_t x_kind,
+                                        const void* w_packed, void* y,
+                                        const void* residual,
+                                        const void* norm_weight, float eps,
+                                        void* y_norm, int32_t m, int32_t n,
+                                        int32_t k, void* workspace,
+                                        size_t workspace_bytes,
+                                        hipStream_t stream) {
+  if (!y || x_kind == kXRmsNorm) return LAMINAR_ERR_INVALID_ARG;
+  PostStep post;
+  post.kind = kPostNorm;
+  post.norm_w = norm_weight;
+  post.eps = eps;
+  post.out = y_norm;
+  return linear_impl(x, x_kind, w_packed, nullptr, y, residual, m, n, k,
+                     workspace, workspace_bytes, stream, nullptr, 0.f, post);
+}
+
+laminar_status laminar_linear_bf16_swiglu(const void* x, int32_t x_kind,
+                                          const void* w_packed, void* y,
+                                          void* y_act, int32_t m, int32_t n,
+                                          int32_t k, void* workspace,
+                                          size_t workspace_bytes,
+                                          hipStream_t stream) {
+  if (!y || x_kind == kXRmsNorm) return LAMINAR_ERR_INVALID_ARG;
+  PostStep post;
+  post.kind = kPostSwiGlu;
+  post.out = y_act;
+  return linear_impl(x, x_kind, w_packed, nullptr, y, nullptr, m, n, k,
+                     workspace, workspace_bytes, stream, nullptr, 0.f, post);
 }
 
 laminar_status laminar_linear_bf16_ex(const void* x, int32_t x_kind,

@@ -526,6 +526,32 @@ def test_linear_errors_before_any_launch():
               None) == INV
     assert nm(16, 16, f(1e-6), 16, None, None, 1, 16, 128, None, 0, None) == INV
     assert nm(16, 16, f(1e-6), 16, 16, None, 9, 16, 128, None, 0, None) == UNS
+    # the product with the next step: NULL or misaligned outputs, the norm's
+    # eps, the RMS-norm kind of x (it has its own call)
+    f = N.ctypes.c_float
+    nrm = lib.laminar_linear_bf16_norm
+    assert nrm(16, 0, 16, 16, None, 16, f(1e-6), None, 1, 16, 128, None, 0,
+               None) == INV
+    assert nrm(16, 0, 16, 16, None, 16, f(1e-6), 24, 1, 16, 128, None, 0,
+               None) == INV
+    assert nrm(16, 0, 16, 16, None, 40, f(1e-6), 32, 1, 16, 128, None, 0,
+               None) == INV
+    assert nrm(16, 0, 16, 16, None, 16, f(-1.0), 32, 1, 16, 128, None, 0,
+               None) == INV
+    assert nrm(16, 0, 16, 16, None, 16, f(float("nan")), 32, 1, 16, 128, None,
+               0, None) == INV
+    assert nrm(16, 3, 16, 16, None, 16, f(1e-6), 32, 1, 16, 128, None, 0,
+               None) == INV
+    assert nrm(16, 0, 16, None, None, 16, f(1e-6), 32, 1, 16, 128, None, 0,
+               None) == INV
+    assert nrm(16, 0, 16, 16, None, 16, f(1e-6), 32, 129, 16, 128, None, 0,
+               None) == UNS
+    sw = lib.laminar_linear_bf16_swiglu
+    assert sw(16, 0, 16, 16, None, 1, 32, 128, None, 0, None) == INV
+    assert sw(16, 0, 16, 16, 24, 1, 32, 128, None, 0, None) == INV
+    assert sw(16, 3, 16, 16, 32, 1, 32, 128, None, 0, None) == INV
+    assert sw(16, 0, 16, None, 32, 1, 32, 128, None, 0, None) == INV
+    assert sw(16, 0, 16, 16, 32, 1, 24, 128, None, 0, None) == UNS
     # packing: NULL, in place, misaligned, shapes
     assert lib.laminar_linear_pack(None, 16, 16, 128, None) == INV
     assert lib.laminar_linear_pack(16, 16, 16, 128, None) == INV

@@ -250,3 +250,48 @@ def test_graph_replays_equal_the_eager_call(m, n, k):
         other = lin.bf16(x2, residual=res)           # eager, same workspace
         torch.cuda.synchronize()
         assert torch.isfinite(other.float()).all()
+
+
+POST_SHAPES = [(64, 3584, 3584), (40, 3584, 18944), (128, 4608, 3584),
+               (16, 3584, 3584), (4, 3584, 3584), (3, 48, 640),
+               (64, 37888, 512), (33, 33024, 384), (64, 32768, 256),
+               (16, 37888, 512)]
+
+
+@pytest.mark.parametrize("m,n,k", POST_SHAPES)
+def test_norm_and_swiglu_outputs_equal_the_separate_launches(m, n, k):
+    """laminar_linear_bf16_norm and _swiglu against the product followed by
+    laminar_rmsnorm / laminar_silu_mul, bit for bit, on every path: the K
+    split whose second kernel carries the step (33 rows and more), the K
+    split finished inside the kernel, no split, the split over wavefronts,
+    and the balanced split with and without groups left over; x in bf16,
+    fp32 and gate-and-up form, the residual in place, with and without a
+    norm weight."""
+    from paper_2510_12633_amd.api import SkinnyLinear, rmsnorm, silu_mul
+    _need_gpu()
+    print(f"[gpu-linear-post] m={m} n={n} k={k}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(13 * m + n + k)
+    w = (torch.randn((n, k), generator=g, device="cuda") / k ** 0.5).to(torch.bfloat16)
+    lin = SkinnyLinear(w)
+    x = (torch.randn((m, k), generator=g, device="cuda") * 2).to(torch.bfloat16)
+    x32 = torch.randn((m, k), generator=g, device="cuda") * 2
+    gu = (torch.randn((m, 2 * k), generator=g, device="cuda") * 3).to(torch.bfloat16)
+    res = torch.randn((m, n), generator=g, device="cuda").to(torch.bfloat16)
+    nw = (1 + 0.2 * torch.randn((n,), generator=g, device="cuda")).to(torch.bfloat16)
+    for xin, sw in ((x, False), (x32, False), (gu, True)):
+        for weight, eps in ((nw, 1e-6), (None, 0.0)):
+            ra, rb = res.clone(), res.clone()
+            ya, za = lin.bf16_norm(xin, weight, eps, out=ra, residual=ra, swiglu=sw)
+            yb = lin.bf16(xin, out=rb, residual=rb, swiglu=sw)
+            zb = rmsnorm(yb, weight, eps=eps)
+            torch.cuda.synchronize()
+            assert torch.equal(bits_t(ya), bits_t(yb)), (m, n, k, sw)
+            assert torch.equal(bits_t(za), bits_t(zb)), (m, n, k, sw)
+            assert torch.isfinite(za.float()).all()
+    ya, act_a = lin.bf16_swiglu(x)
+    yb = lin.bf16(x)
+    act_b = silu_mul(yb)
+    torch.cuda.synchronize()
+    assert torch.equal(bits_t(ya), bits_t(yb)), (m, n, k)
+    assert torch.equal(bits_t(act_a), bits_t(act_b)), (m, n, k)
+    assert torch.isfinite(act_a.float()).all()
