@@ -35,12 +35,14 @@
  * to a general GEMM.
  * Workspace: laminar_linear_workspace_bytes(M, N, K) bytes of device
  * memory (0 when K is not split over workgroups), 256-byte aligned, owned
- * by the caller, zeroed once before its first use (hipMemset): it holds
- * the partial sums of the K split and, up to 32 rows, one counter per
- * group of output columns, with which the last workgroup of a group to
- * finish adds the group's partial sums itself; every call leaves the
- * counters at zero again, so no clearing is needed between calls (nor in a
- * captured graph). Calls that share a workspace must be ordered on one
+ * by the caller, zeroed once before its first use (hipMemset): it starts
+ * with 256 counters (one per group of output columns, with which, up to 32
+ * rows, the last workgroup of a group to finish adds the group's partial
+ * sums itself) and holds the partial sums of the K split after them. Every
+ * call leaves the counters at zero again, so no clearing is needed between
+ * calls (nor in a captured graph), and the counters sit at the same place
+ * for every shape: one workspace of the largest size serves calls of any
+ * M, N and K. Calls that share a workspace must be ordered on one
  * stream. A call that fails part-way (a kernel fault) may leave counters
  * set: zero the workspace again before reusing it.
  * Pointers: x, w, w_packed and y 16-byte aligned; the caller owns every

@@ -1067,14 +1067,15 @@ int32_t balanced_pieces(const BalancedPlan& b, int32_t k) {
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
-// The group split's workspace: the partial sums, then one counter per group.
+// A workspace starts with one counter per group of a split that the last
+// range of each group finishes (at most 256 groups), at the same place
+// whatever the call's shape, so that calls of different M (or of different
+// weights) can share one workspace: no call's partial sums cover another
+// call's counters. The partial sums, or the balanced split's pieces, follow.
+constexpr size_t kDataOffset = kMaxGroups * sizeof(int32_t);
+
 size_t split_part_bytes(int32_t m, int32_t n, int32_t splits) {
   return align256(size_t(splits) * m * n * sizeof(float));
-}
-
-int32_t split_groups(int32_t m, int32_t n) {
-  const int32_t per_group = launch_tiles(m) >= 4 ? 8 : 4;
-  return (n / 16 + per_group - 1) / per_group;
 }
 
 bool misaligned16(const void* p) {
@@ -1226,10 +1227,8 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
     if (!workspace || workspace_bytes < need ||
         (reinterpret_cast<uintptr_t>(workspace) & 255))
       return LAMINAR_ERR_INVALID_ARG;
-    a.part = static_cast<float*>(workspace);
-    if (a.splits > 1)
-      a.counters = reinterpret_cast<int*>(static_cast<char*>(workspace) +
-                                          split_part_bytes(m, n, a.splits));
+    a.counters = static_cast<int*>(workspace);
+    a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + kDataOffset);
   }
   hipError_t e;
   bool post_done = false;
@@ -1277,13 +1276,11 @@ size_t laminar_linear_workspace_bytes(int32_t m, int32_t n, int32_t k) {
   if (!shape_ok(m, n, k)) return 0;
   const SplitPlan p = split_plan(m, n, k);
   const BalancedPlan b = balanced_plan(m, n, k, p);
-  size_t bytes = 0;
   if (b.use)
-    bytes = b.rem_groups ? size_t(2) * b.wgs * m * kWideTiles * 16 * sizeof(float) : 0;
-  else if (p.splits > 1)
-    bytes = split_part_bytes(m, n, p.splits) +
-            align256(size_t(split_groups(m, n)) * sizeof(int32_t));
-  return align256(bytes);
+    return b.rem_groups ? kDataOffset + align256(size_t(2) * b.wgs * m * kWideTiles *
+                                                 16 * sizeof(float))
+                        : 0;
+  return p.splits > 1 ? kDataOffset + split_part_bytes(m, n, p.splits) : 0;
 }
 
 laminar_status laminar_linear(const void* x, const void* w_packed, float* y,

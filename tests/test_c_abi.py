@@ -577,10 +577,17 @@ def test_linear_errors_before_any_launch():
     # the balanced split (from 17 rows, uneven group grids): gate and up of
     # 7B is 296 groups, one full round and 40 left over, cut into pieces of
     # 4 or 5 steps of K (at most 7 per group) with two partial slots per
-    # workgroup
+    # workgroup, after the 256 group counters every shape keeps at the start
+    # of the workspace (so calls of any M can share one)
+    ctrl = 256 * 4
     assert N.laminar_linear_splits(64, 37888, 3584) == 7
     assert (N.laminar_linear_workspace_bytes(64, 37888, 3584)
-            == 2 * 256 * 64 * 128 * 4)
+            == ctrl + 2 * 256 * 64 * 128 * 4)
+    # the group split: the counters, then its ranges of partial sums: QKV
+    # of 7B at 64 rows is 36 groups of 8 tiles in 7 ranges
+    assert N.laminar_linear_splits(64, 4608, 3584) == 7
+    assert (N.laminar_linear_workspace_bytes(64, 4608, 3584)
+            == ctrl + 7 * 64 * 4608 * 4)
     # an even grid keeps the group split up to 64 rows: the LM head (1188
     # groups, 5 rounds); from 65 rows any grid past 256 workgroups is
     # balanced (1188 = 4 full rounds and 164 left over)

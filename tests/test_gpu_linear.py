@@ -213,6 +213,44 @@ def test_back_to_back_calls_share_the_workspace(m, n, k):
     assert torch.equal(ys[0], lin(xs[0]))
 
 
+@pytest.mark.parametrize("n,k", [(4608, 3584), (3584, 18944), (37888, 512)])
+def test_calls_of_every_batch_size_share_the_workspace(n, k):
+    """One weight called at batch sizes in turn, as a decode step's
+    projection is when the batch changes: every path of the split (inside
+    the workgroup, finished by a group's last range, added by a second
+    kernel, balanced) on one workspace, sized for the largest. Each call
+    must equal its own product: a call whose partial sums covered the
+    group counters of another batch size would leave that size's later
+    calls with no last range, their outputs unwritten (NaN here). The next
+    norm and SwiGLU ride along on some calls."""
+    from paper_2510_12633_amd.api import SkinnyLinear, rmsnorm, silu_mul
+    _need_gpu()
+    print(f"[gpu-linear-mixed-m] n={n} k={k}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(n + 3 * k)
+    w = (torch.randn((n, k), generator=g, device="cuda") / k ** 0.5).to(torch.bfloat16)
+    lin = SkinnyLinear(w)
+    nw = (1 + 0.2 * torch.randn((n,), generator=g, device="cuda")).to(torch.bfloat16)
+    for i, m in enumerate((16, 64, 8, 32, 128, 3, 16, 40, 64, 8, 17, 128, 32)):
+        x = torch.randn((m, k), generator=g, device="cuda").to(torch.bfloat16)
+        y = torch.full((m, n), float("nan"), device="cuda")
+        lin(x, out=y)
+        ref = x.float() @ w.float().t()
+        tol = 1e-5 * (x.float().abs() @ w.float().abs().t()) + 1e-6
+        torch.cuda.synchronize()
+        assert bool(((y - ref).abs() <= tol).all()), (m, n, k, i)
+        if i % 3 == 1:
+            ya, za = lin.bf16_norm(x, nw, 1e-6)
+            zb = rmsnorm(lin.bf16(x), nw, eps=1e-6)
+            torch.cuda.synchronize()
+            assert torch.equal(bits_t(ya), bits_t(y.to(torch.bfloat16))), (m, i)
+            assert torch.equal(bits_t(za), bits_t(zb)), (m, n, k, i)
+        elif i % 3 == 2:
+            ya, act = lin.bf16_swiglu(x)
+            torch.cuda.synchronize()
+            assert torch.equal(bits_t(ya), bits_t(y.to(torch.bfloat16))), (m, i)
+            assert torch.equal(bits_t(act), bits_t(silu_mul(ya))), (m, n, k, i)
+
+
 @pytest.mark.parametrize("m,n,k", [(16, 4608, 3584), (32, 3584, 18944),
                                    (64, 37888, 512), (64, 3584, 3584)])
 def test_graph_replays_equal_the_eager_call(m, n, k):
