@@ -499,11 +499,13 @@ template <int N> __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// First left-over unit of workgroup w: floor(w ru / W). The quotient's
-// fractional part is a multiple of 1 / W (W <= 256) and w ru < 2^35, so
-// the double division floors exactly.
+// First left-over unit of workgroup w: floor(w ru / W), W = 256 (a shift:
+// the reductions evaluate it for every candidate piece of every output, and
+// a division there cost more than the sums).
+static_assert(kBalancedWgs == 256, "rem_start divides by 256 with a shift");
 __host__ __device__ inline int64_t rem_start(int w, int64_t ru, int wgs) {
-  return int64_t(floor(double(w) * double(ru) / double(wgs)));
+  (void)wgs;
+  return (int64_t(w) * ru) >> 8;
 }
 
 // Position in a workgroup's stream of units.
@@ -905,53 +907,55 @@ __device__ __forceinline__ bf16x8 reduce_chunk8(const LinearArgs& a, int m, int 
 }
 
 // The group split's reduction for whole rows followed by the RMS norm of
-// each row, one workgroup per row: y exactly as linear_reduce writes it and
-// post_out exactly as laminar_rmsnorm computes it from that y (thread t
-// chains the sums of squares of chunks t, t + 256, ... in one fma, then the
-// same butterfly and sums, the same scaling and rounding), in one launch
-// instead of two.
-__global__ void __launch_bounds__(256) linear_reduce_norm(const LinearArgs a) {
+// each row, one workgroup of 1024 threads per row: y exactly as
+// linear_reduce writes it and post_out exactly as laminar_rmsnorm computes
+// it from that y, in one launch instead of two. Thread t adds the ranges of
+// chunk t (all loads of a row in one round: with 256 threads the row's
+// 100-130 KB of partial sums took two); the row's chunks go through LDS so
+// that threads 0-255 chain the sums of squares of chunks t, t + 256, ... in
+// one fma each, then the same butterfly and sums, the same scaling and
+// rounding as laminar_rmsnorm.
+constexpr int kNormThreads = 1024;
+constexpr int kNormMaxChunks = 2048;        // N up to 16384: 32 KB of LDS
+
+__global__ void __launch_bounds__(kNormThreads) linear_reduce_norm(const LinearArgs a) {
+  extern __shared__ bf16x8 yl[];            // the row's chunks of y
   __shared__ float part[4];
   const int m = blockIdx.x;
   const int chunks = a.n / 8;
+  const int t = threadIdx.x;
   bf16x8* yr = reinterpret_cast<bf16x8*>(a.yb + size_t(m) * a.n);
   bf16x8* zr = reinterpret_cast<bf16x8*>(a.post_out + size_t(m) * a.n);
   const bf16x8* wr = reinterpret_cast<const bf16x8*>(a.post_norm_w);
-  constexpr int kHeld = 4;
-  bf16x8 yv[kHeld];
-  float ss = 0.f;
-#pragma unroll
-  for (int h = 0; h < kHeld; ++h) {
-    const int c = threadIdx.x + 256 * h;
-    if (c < chunks) {
-      yv[h] = reduce_chunk8(a, m, c);
-      yr[c] = yv[h];
-      ss = laminar::sumsq8(yv[h], ss);
-    }
-  }
-  for (int c = threadIdx.x + 256 * kHeld; c < chunks; c += 256) {
+  // the norm weight of the first chunk does not depend on the sums
+  bf16x8 w0{};
+  if (wr && t < chunks) w0 = wr[t];
+  for (int c = t; c < chunks; c += kNormThreads) {
     const bf16x8 v = reduce_chunk8(a, m, c);
     yr[c] = v;
-    ss = laminar::sumsq8(v, ss);
+    yl[c] = v;
   }
-  ss = laminar::wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  if (t < 256) {
+    float ss = 0.f;
+    for (int c = t; c < chunks; c += 256) ss = laminar::sumsq8(yl[c], ss);
+    ss = laminar::wave_sum(ss);
+    if ((t & 63) == 0) part[t >> 6] = ss;
+  }
   __syncthreads();
   const float r = laminar::rms_inverse(part[0], part[1], part[2], part[3],
                                        a.post_norm_inv_n, a.post_norm_eps);
-  auto scale = [&](const bf16x8& v, int c) {
-    if (wr) return laminar::rms_scale8(v, wr[c], r);
-    bf16x8 o;
+  for (int c = t; c < chunks; c += kNormThreads) {
+    const bf16x8 v = yl[c];
+    if (wr) {
+      zr[c] = laminar::rms_scale8(v, c == t ? w0 : wr[c], r);
+    } else {
+      bf16x8 o;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = (__bf16)(float(v[e]) * r);
-    return o;
-  };
-#pragma unroll
-  for (int h = 0; h < kHeld; ++h) {
-    const int c = threadIdx.x + 256 * h;
-    if (c < chunks) zr[c] = scale(yv[h], c);
+      for (int e = 0; e < 8; ++e) o[e] = (__bf16)(float(v[e]) * r);
+      zr[c] = o;
+    }
   }
-  for (int c = threadIdx.x + 256 * kHeld; c < chunks; c += 256) zr[c] = scale(yr[c], c);
 }
 
 // w [N, K] -> packed [N/16][K/8][16][8]: one 16-byte chunk per thread,
@@ -1146,8 +1150,9 @@ hipError_t launch(const LinearArgs& a, const SplitPlan& plan, bool balanced,
   // from 33 rows the partial sums are added by a second kernel, which also
   // makes the next RMS norm when the call asks for it
   if (e == hipSuccess && a.splits > 1 && launch_tiles(m) >= 4) {
-    if (a.post_kind == kPostNorm) {
-      hipLaunchKernelGGL(linear_reduce_norm, dim3(unsigned(m)), dim3(256), 0, stream, a);
+    if (a.post_kind == kPostNorm && a.n / 8 <= kNormMaxChunks) {
+      hipLaunchKernelGGL(linear_reduce_norm, dim3(unsigned(m)), dim3(kNormThreads),
+                         size_t(a.n / 8) * sizeof(bf16x8), stream, a);
       post_done = true;
     } else {
       const size_t total = size_t(m) * a.n / 4;
