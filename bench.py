@@ -433,7 +433,8 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
     serves all layers (the bytes read per layer are those of a real step).
     Rotary embedding and biases are left out."""
     import numpy as np
-    from paper_2510_12633_amd.api import PagedDecodeAttention, kv_append
+    from paper_2510_12633_amd.api import (PagedDecodeAttention, kv_append,
+                                          kv_append_desc)
     model_name, (L, h, hq, hkv, d, inter, vocab) = CURVE_MODELS[model]
     shape = N.LaminarModelShape(layers=L, hidden=h, q_heads=hq, kv_heads=hkv,
                                 head_dim=d, intermediate=inter, vocab=vocab,
@@ -473,7 +474,8 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             self.mode = "library"
 
         def __call__(self, x, residual=None, swiglu=False, norm=None,
-                     operand=None, next_norm=None, swiglu_out=False):
+                     operand=None, next_norm=None, swiglu_out=False,
+                     append=None):
             """bf16(x w^T), plus residual when given (in place into it on
             the skinny path). fp32 x is rounded to bf16; with swiglu, x
             [M, 2K] is SwiGLU's gate and up; with norm (a [K] weight), the
@@ -482,9 +484,12 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             [N] weight) it returns (y, rmsnorm(y)) and with swiglu_out (y,
             SwiGLU of y's halves); the skinny kernel makes the second in its
             reduction launch where it has one, the other ways return None
-            for it."""
+            for it. With append (the arguments of
+            SkinnyLinear.bf16_kv_append after x) the skinny path also makes
+            the step's KV append and sets self.appended."""
             pair = next_norm is not None or swiglu_out
             mode = self.mode
+            self.appended = False
             if operand is not None:
                 x, swiglu, norm = operand, False, None
                 mode = "skinny" if mode == "fused" else mode
@@ -503,6 +508,9 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
             elif x.dtype != bf:
                 x = x.to(bf)
             if mode == "skinny":
+                if append is not None:
+                    self.appended = True
+                    return self.skinny.bf16_kv_append(x, *append)
                 if next_norm is not None:
                     return self.skinny.bf16_norm(x, next_norm, out=residual,
                                                  residual=residual)
@@ -608,6 +616,10 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                 q_row_stride=(hq + 2 * hkv) * d)
             out, lse = att.outputs()
             x0 = torch.randn((m, h), generator=gen, device="cuda", dtype=bf)
+            # QKV's skinny call makes the KV append too (its K-split
+            # reduction stores K and V from 33 rows on)
+            app_args = (kv_append_desc(m, hkv, d, m * pages, pages),
+                        hq * d, (hq + hkv) * d, table, lens, kp, vp)
 
             # Steps handed from a projection's reduction to the next
             # projection: the RMS norm after O (for gate+up) and after down
@@ -624,12 +636,14 @@ def latency_curve(torch, N, batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 384,
                 xn = None                         # its RMS norm, when made
 
                 for li, (wqkv, wo, wgu, wd) in enumerate(layers):
-                    qkv = wqkv(x, norm=norms[2 * li], operand=xn)
+                    qkv = wqkv(x, norm=norms[2 * li], operand=xn,
+                               append=app_args)
                     # q, k and v are read in place from the fused output
                     q = qkv[:, :hq * d].view(m, hq, d)
-                    k_new = qkv[:, hq * d:(hq + hkv) * d].view(m, hkv, d)
-                    v_new = qkv[:, (hq + hkv) * d:].view(m, hkv, d)
-                    kv_append(k_new, v_new, table, lens, kp, vp, stream=cur)
+                    if not wqkv.appended:
+                        k_new = qkv[:, hq * d:(hq + hkv) * d].view(m, hkv, d)
+                        v_new = qkv[:, (hq + hkv) * d:].view(m, hkv, d)
+                        kv_append(k_new, v_new, table, lens, kp, vp, stream=cur)
                     att(q, kp, vp, table, lens, out, lse, stream=cur)
                     if norm_after_o:
                         x, xn = wo(out.view(m, hq * d), residual=x,

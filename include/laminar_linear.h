@@ -155,6 +155,28 @@ laminar_status laminar_linear_bf16_swiglu(const void* x, int32_t x_kind,
                                           size_t workspace_bytes,
                                           hipStream_t stream);
 
+/* laminar_linear_bf16_ex (no residual) followed by the decode step's KV
+ * append: y [M, N] bf16 as laminar_linear_bf16_ex writes it, then exactly
+ * laminar_kv_append(kv_desc, y + k_col, y + v_col, block_table, seq_lens,
+ * k_pages, v_pages, k_scale, v_scale) with kv_desc's input_row_stride
+ * taken as N (its own value is ignored): row m is trajectory m's new token,
+ * columns [k_col, k_col + num_kv_heads head_dim) its K and [v_col, ...) its
+ * V. For the fused QKV projection in front of attention (the paged KV cache
+ * of the paper's §5.2): from 33 rows, where K is split and a second kernel
+ * adds the ranges, that kernel also stores K and V into bf16 pools (one
+ * launch fewer); fp8 pools, and calls without that kernel, run the append
+ * as its own launch. The pools and tables are laid out and checked as
+ * laminar_kv_append's; kv_desc (host) must have batch = M. Pools, tables
+ * and y must not overlap. Errors as laminar_linear_bf16_ex and
+ * laminar_kv_append, plus INVALID_ARG for a NULL kv_desc, batch != M, or
+ * k_col / v_col negative, not a multiple of 8, past N or overlapping. */
+laminar_status laminar_linear_bf16_kv_append(
+    const void* x, int32_t x_kind, const void* w_packed, void* y, int32_t m,
+    int32_t n, int32_t k, void* workspace, size_t workspace_bytes,
+    const laminar_attn_desc* kv_desc, int32_t k_col, int32_t v_col,
+    const int32_t* block_table, const int32_t* seq_lens, void* k_pages,
+    void* v_pages, float* k_scale, float* v_scale, hipStream_t stream);
+
 /* laminar_linear_bf16 on RMS-normalised rows, the norm done on load:
  * the operand is bf16((x[m, k] r_m) norm_weight[k]) with
  * r_m = 1 / sqrt(mean_k x[m, k]^2 + eps), the pre-norm of a decoder layer

@@ -132,6 +132,12 @@ _SIGNATURES = {
     "laminar_linear_bf16": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p,
                                       c_int32, c_int32, c_int32, c_void_p,
                                       c_size_t, c_void_p]),
+    "laminar_linear_bf16_kv_append": (c_int32, [c_void_p, c_int32, c_void_p,
+                                                c_void_p, c_int32, c_int32,
+                                                c_int32, c_void_p, c_size_t,
+                                                POINTER(LaminarAttnDesc),
+                                                c_int32, c_int32]
+                                      + [c_void_p] * 7),
     "laminar_linear_bf16_ex": (c_int32, [c_void_p, c_int32, c_void_p,
                                          c_void_p, c_void_p, c_int32, c_int32,
                                          c_int32, c_void_p, c_size_t,
@@ -448,6 +454,19 @@ def laminar_linear_bf16_norm(x, x_kind: int, w_packed, y, residual,
         _ptr(norm_weight), float(eps), _ptr(y_norm), int(m), int(n), int(k),
         _ptr(workspace), int(workspace_bytes), _ptr(stream)),
         "laminar_linear_bf16_norm")
+
+
+def laminar_linear_bf16_kv_append(x, x_kind: int, w_packed, y, m: int, n: int,
+                                  k: int, workspace, workspace_bytes: int,
+                                  kv_desc: LaminarAttnDesc, k_col: int,
+                                  v_col: int, block_table, seq_lens, k_pages,
+                                  v_pages, k_scale, v_scale, stream):
+    _check(lib().laminar_linear_bf16_kv_append(
+        _ptr(x), int(x_kind), _ptr(w_packed), _ptr(y), int(m), int(n), int(k),
+        _ptr(workspace), int(workspace_bytes), ctypes.byref(kv_desc),
+        int(k_col), int(v_col), _ptr(block_table), _ptr(seq_lens),
+        _ptr(k_pages), _ptr(v_pages), _ptr(k_scale), _ptr(v_scale),
+        _ptr(stream)), "laminar_linear_bf16_kv_append")
 
 
 def laminar_linear_bf16_swiglu(x, x_kind: int, w_packed, y, y_act, m: int,

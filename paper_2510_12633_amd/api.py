@@ -167,14 +167,24 @@ def kv_append(k_new, v_new, block_table, seq_lens, k_pages, v_pages,
         raise ValueError("k_new and v_new need contiguous [heads, dim] rows "
                          "and one row stride")
     row = k_new.stride(0)
-    desc = N.LaminarAttnDesc(
-        batch=b, num_q_heads=hkv, num_kv_heads=hkv, head_dim=d, page_size=16,
-        num_pages=k_pages.shape[0], max_blocks_per_seq=block_table.shape[1],
-        kv_dtype=KV_DTYPES[kv_dtype], softmax_scale=1.0, k_scale=None,
-        v_scale=None, pages_per_item=0, waves_per_item=0,
-        input_row_stride=0 if row == hkv * d else row)
+    desc = kv_append_desc(b, hkv, d, k_pages.shape[0], block_table.shape[1],
+                          kv_dtype, input_row_stride=0 if row == hkv * d else row)
     N.laminar_kv_append(desc, k_new, v_new, block_table, seq_lens, k_pages,
                         v_pages, k_scale, v_scale, _stream_handle(stream))
+
+
+def kv_append_desc(batch: int, num_kv_heads: int, head_dim: int,
+                   num_pages: int, max_blocks: int, kv_dtype: str = "bf16",
+                   input_row_stride: int = 0):
+    """The description laminar_kv_append (and the projection that makes the
+    append, SkinnyLinear.bf16_kv_append) reads: pools of num_pages pages of
+    16 tokens, a block table of max_blocks entries per trajectory."""
+    return N.LaminarAttnDesc(
+        batch=batch, num_q_heads=num_kv_heads, num_kv_heads=num_kv_heads,
+        head_dim=head_dim, page_size=16, num_pages=num_pages,
+        max_blocks_per_seq=max_blocks, kv_dtype=KV_DTYPES[kv_dtype],
+        softmax_scale=1.0, k_scale=None, v_scale=None, pages_per_item=0,
+        waves_per_item=0, input_row_stride=input_row_stride)
 
 
 def migrate(src_pools, dst_pools, pairs, stream=None):
@@ -303,6 +313,24 @@ class SkinnyLinear:
                                      self.n, self.k, self.ws, self.ws_bytes,
                                      _stream_handle(stream))
         return out, out_act
+
+    def bf16_kv_append(self, x, kv_desc, k_col: int, v_col: int, block_table,
+                       seq_lens, k_pages, v_pages, k_scale=None, v_scale=None,
+                       out=None, swiglu=False, stream=None):
+        """y = bf16(x w^T) as bf16() computes it, then the decode step's KV
+        append of row m's new token (columns [k_col, k_col + Hkv D) and
+        [v_col, ...) of y) into the pools, exactly laminar_kv_append on y;
+        from 33 rows on bf16 pools the split's reduction launch stores them.
+        kv_desc is a LaminarAttnDesc with batch = M."""
+        m = x.shape[0]
+        kind = self._kind(x, swiglu)
+        if out is None:
+            out = torch.empty((m, self.n), dtype=torch.bfloat16, device=x.device)
+        N.laminar_linear_bf16_kv_append(
+            x, kind, self.w_packed, out, m, self.n, self.k, self.ws,
+            self.ws_bytes, kv_desc, k_col, v_col, block_table, seq_lens,
+            k_pages, v_pages, k_scale, v_scale, _stream_handle(stream))
+        return out
 
 
 def rmsnorm(x, weight=None, eps: float = 1e-6, out=None, stream=None):

@@ -18,6 +18,7 @@
 #include <cstdint>
 
 #include "laminar_kv_append.h"
+#include "kv_append_internal.h"
 
 namespace {
 
@@ -246,10 +247,14 @@ hipError_t launch(bool fp8, int units, const AppendArgs& a, hipStream_t st) {
 
 }  // namespace
 
-extern "C" laminar_status laminar_kv_append(
-    const laminar_attn_desc* d, const void* k_new, const void* v_new,
-    const int32_t* block_table, const int32_t* seq_lens, void* k_pages,
-    void* v_pages, float* k_scale, float* v_scale, hipStream_t stream) {
+namespace laminar_detail {
+
+laminar_status kv_append_check(const laminar_attn_desc* d, const void* k_new,
+                               const void* v_new, const int32_t* block_table,
+                               const int32_t* seq_lens, const void* k_pages,
+                               const void* v_pages, const float* k_scale,
+                               const float* v_scale, bool* empty) {
+  *empty = false;
   if (!d || d->batch < 0 || d->num_kv_heads <= 0 || d->num_pages <= 0 ||
       d->max_blocks_per_seq < 0 || d->head_dim <= 0)
     return LAMINAR_ERR_INVALID_ARG;
@@ -260,7 +265,10 @@ extern "C" laminar_status laminar_kv_append(
     return LAMINAR_ERR_UNSUPPORTED;
   const int64_t units = int64_t(d->batch) * d->num_kv_heads;
   if (units > INT32_MAX) return LAMINAR_ERR_INVALID_ARG;
-  if (units == 0) return LAMINAR_OK;
+  if (units == 0) {
+    *empty = true;
+    return LAMINAR_OK;
+  }
   if (!k_new || !v_new || !block_table || !seq_lens || !k_pages || !v_pages)
     return LAMINAR_ERR_INVALID_ARG;
   if ((reinterpret_cast<uintptr_t>(k_new) | reinterpret_cast<uintptr_t>(v_new) |
@@ -278,6 +286,22 @@ extern "C" laminar_status laminar_kv_append(
       (int64_t(d->input_row_stride) < int64_t(d->num_kv_heads) * d->head_dim ||
        d->input_row_stride % 8 != 0))
     return LAMINAR_ERR_INVALID_ARG;
+  return LAMINAR_OK;
+}
+
+}  // namespace laminar_detail
+
+extern "C" laminar_status laminar_kv_append(
+    const laminar_attn_desc* d, const void* k_new, const void* v_new,
+    const int32_t* block_table, const int32_t* seq_lens, void* k_pages,
+    void* v_pages, float* k_scale, float* v_scale, hipStream_t stream) {
+  bool empty = false;
+  const laminar_status st = laminar_detail::kv_append_check(
+      d, k_new, v_new, block_table, seq_lens, k_pages, v_pages, k_scale,
+      v_scale, &empty);
+  if (st != LAMINAR_OK || empty) return st;
+  const bool fp8 = d->kv_dtype == LAMINAR_KV_FP8_E4M3FN;
+  const int64_t units = int64_t(d->batch) * d->num_kv_heads;
   AppendArgs a;
   a.row_stride = d->input_row_stride
                      ? d->input_row_stride

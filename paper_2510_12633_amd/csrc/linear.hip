@@ -51,6 +51,7 @@
 
 #include "activation.h"
 #include "laminar_decode_step.h"
+#include "kv_append_internal.h"
 #include "laminar_linear.h"
 
 namespace {
@@ -113,9 +114,16 @@ struct LinearArgs {
   const uint16_t* post_norm_w;   // [N] norm weight, or NULL
   float post_norm_inv_n, post_norm_eps;
   uint16_t* post_out;            // [M, N] or [M, N / 2] bf16
+  // kPostAppend: the KV append of row m's new token (columns [k_col,
+  // k_col + hkv D) and [v_col, ...) of y) into bf16 pools, as
+  // laminar_kv_append stores it
+  const int32_t* ap_lens;        // [M] lengths after the append
+  const int32_t* ap_table;       // [M, max_blocks] block table
+  uint16_t *ap_k, *ap_v;         // the K and V pools
+  int32_t ap_k_col, ap_v_col, ap_hkv, ap_d, ap_max_blocks, ap_num_pages;
 };
 
-constexpr int kPostNone = 0, kPostNorm = 1, kPostSwiGlu = 2;
+constexpr int kPostNone = 0, kPostNorm = 1, kPostSwiGlu = 2, kPostAppend = 3;
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
@@ -332,6 +340,68 @@ __global__ void __launch_bounds__(256) linear_reduce(const LinearArgs a) {
       if (k0 + j < a.splits) s += v[j];
   }
   store4(a, 4 * i, s);
+}
+
+// linear_reduce followed by the KV append of each row's new token: y as
+// linear_reduce writes it, and where the four outputs are K or V of a
+// kv-head, the same bf16 values stored at the token's slot of its page as
+// laminar_kv_append stores them (K element (t, d) of a tile at
+// ((d / 8) 16 + t) 8 + d % 8, V element at ((t / 4) D + d) 4 + t % 4). The
+// token's length and block-table entry are loaded with the partial sums;
+// nothing goes to the pools for a length below 1, a block past the table or
+// a table entry outside the pool.
+__global__ void __launch_bounds__(256) linear_reduce_append(const LinearArgs a) {
+  const size_t i = size_t(blockIdx.x) * 256 + threadIdx.x;    // float4 index
+  const size_t total = size_t(a.m) * a.n / 4;
+  if (i >= total) return;
+  const int m = int(4 * i / size_t(a.n));
+  const int n = int(4 * i - size_t(m) * a.n);
+  const int hd = a.ap_hkv * a.ap_d;
+  const bool is_k = n >= a.ap_k_col && n < a.ap_k_col + hd;
+  const bool is_v = n >= a.ap_v_col && n < a.ap_v_col + hd;
+  int page = -1, slot = 0;
+  if (is_k || is_v) {
+    const int len = a.ap_lens[m];
+    const int t = len - 1;
+    if (len >= 1 && (t >> 4) < a.ap_max_blocks) {
+      const int e = a.ap_table[size_t(m) * a.ap_max_blocks + (t >> 4)];
+      if (e >= 0 && e < a.ap_num_pages) {
+        page = e;
+        slot = t & 15;
+      }
+    }
+  }
+  const f32x4* p = reinterpret_cast<const f32x4*>(a.part);
+  f32x4 s = p[i];
+  for (int k0 = 1; k0 < a.splits; k0 += 8) {
+    f32x4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      v[j] = k0 + j < a.splits ? p[size_t(k0 + j) * total + i]
+                               : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (k0 + j < a.splits) s += v[j];
+  }
+  store4(a, 4 * i, s);
+  if (page < 0) return;
+  // the values store4 wrote (one rounding; these calls have no residual)
+  const bf16x4 o{(__bf16)s[0], (__bf16)s[1], (__bf16)s[2], (__bf16)s[3]};
+  const int c = n - (is_k ? a.ap_k_col : a.ap_v_col);
+  const int kvh = c / a.ap_d, d = c - kvh * a.ap_d;
+  uint16_t* tile = (is_k ? a.ap_k : a.ap_v) +
+                   (size_t(page) * a.ap_hkv + kvh) * 16 * a.ap_d;
+  if (is_k) {
+    *reinterpret_cast<bf16x4*>(tile + ((d >> 3) * 16 + slot) * 8 + (d & 7)) = o;
+  } else {
+    // the bits of the four values (a bit cast of one element of the bf16
+    // vector read element 0 every time: cast the whole vector)
+    typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+    const u16x4 ob = __builtin_bit_cast(u16x4, o);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      tile[((slot >> 2) * a.ap_d + d + e) * 4 + (slot & 3)] = ob[e];
+  }
 }
 
 template <int MT, int XK>
@@ -1154,6 +1224,11 @@ hipError_t launch(const LinearArgs& a, const SplitPlan& plan, bool balanced,
       hipLaunchKernelGGL(linear_reduce_norm, dim3(unsigned(m)), dim3(kNormThreads),
                          size_t(a.n / 8) * sizeof(bf16x8), stream, a);
       post_done = true;
+    } else if (a.post_kind == kPostAppend) {
+      const size_t total = size_t(m) * a.n / 4;
+      hipLaunchKernelGGL(linear_reduce_append, dim3(unsigned((total + 255) / 256)),
+                         dim3(256), 0, stream, a);
+      post_done = true;
     } else {
       const size_t total = size_t(m) * a.n / 4;
       hipLaunchKernelGGL(linear_reduce, dim3(unsigned((total + 255) / 256)),
@@ -1171,6 +1246,14 @@ struct PostStep {
   const void* norm_w = nullptr;   // RMS norm weight [N], or NULL
   float eps = 0.f;
   void* out = nullptr;            // [M, N] or [M, N / 2] bf16
+  // kPostAppend: the append's description (input_row_stride N) and
+  // arguments, checked by the caller
+  const laminar_attn_desc* kv = nullptr;
+  int32_t k_col = 0, v_col = 0;
+  const int32_t* block_table = nullptr;
+  const int32_t* seq_lens = nullptr;
+  void *k_pages = nullptr, *v_pages = nullptr;
+  float *k_scale = nullptr, *v_scale = nullptr;
 };
 
 laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
@@ -1189,9 +1272,11 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
   if (x_kind == kXRmsNorm &&
       (!norm_w || !(eps >= 0.f) || !std::isfinite(eps)))
     return LAMINAR_ERR_INVALID_ARG;
-  if (post.kind != kPostNone &&
+  if (post.kind != kPostNone && post.kind != kPostAppend &&
       (!yb || !post.out || misaligned16(post.out) || misaligned16(post.norm_w) ||
        (post.kind == kPostNorm && (!(post.eps >= 0.f) || !std::isfinite(post.eps)))))
+    return LAMINAR_ERR_INVALID_ARG;
+  if (post.kind == kPostAppend && (!yb || !post.kv || res))
     return LAMINAR_ERR_INVALID_ARG;
   if (!shape_ok(m, n, k)) return LAMINAR_ERR_UNSUPPORTED;
   if (x_kind == kXRmsNorm && m > kNormMaxM) return LAMINAR_ERR_UNSUPPORTED;
@@ -1220,7 +1305,23 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
   a.wgs = bal.wgs;
   a.full_rounds = bal.full_rounds;
   a.rem_groups = bal.rem_groups;
-  a.post_kind = post.kind;
+  // the reduction stores bf16 K and V; fp8 pools take the append's own
+  // launch (its per-page scales)
+  const bool append_in_reduction =
+      post.kind == kPostAppend && post.kv->kv_dtype == LAMINAR_KV_BF16 &&
+      post.kv->batch > 0;
+  a.post_kind = post.kind == kPostAppend && !append_in_reduction ? kPostNone
+                                                                : post.kind;
+  a.ap_lens = post.seq_lens;
+  a.ap_table = post.block_table;
+  a.ap_k = static_cast<uint16_t*>(post.k_pages);
+  a.ap_v = static_cast<uint16_t*>(post.v_pages);
+  a.ap_k_col = post.k_col;
+  a.ap_v_col = post.v_col;
+  a.ap_hkv = post.kv ? post.kv->num_kv_heads : 0;
+  a.ap_d = post.kv ? post.kv->head_dim : 0;
+  a.ap_max_blocks = post.kv ? post.kv->max_blocks_per_seq : 0;
+  a.ap_num_pages = post.kv ? post.kv->num_pages : 0;
   a.post_norm_w = static_cast<const uint16_t*>(post.norm_w);
   a.post_norm_inv_n = 1.0f / float(n);
   a.post_norm_eps = post.eps;
@@ -1251,6 +1352,12 @@ laminar_status linear_impl(const void* x, int32_t x_kind, const void* w_packed,
     return laminar_rmsnorm(yb, post.norm_w, post.out, m, n, post.eps, stream);
   if (post.kind == kPostSwiGlu && !post_done)
     return laminar_silu_mul(yb, post.out, m, n / 2, stream);
+  if (post.kind == kPostAppend && !post_done) {
+    uint16_t* y16 = static_cast<uint16_t*>(yb);
+    return laminar_kv_append(post.kv, y16 + post.k_col, y16 + post.v_col,
+                             post.block_table, post.seq_lens, post.k_pages,
+                             post.v_pages, post.k_scale, post.v_scale, stream);
+  }
   return LAMINAR_OK;
 }
 
@@ -1346,6 +1453,43 @@ laminar_status laminar_linear_bf16_swiglu(const void* x, int32_t x_kind,
   PostStep post;
   post.kind = kPostSwiGlu;
   post.out = y_act;
+  return linear_impl(x, x_kind, w_packed, nullptr, y, nullptr, m, n, k,
+                     workspace, workspace_bytes, stream, nullptr, 0.f, post);
+}
+
+laminar_status laminar_linear_bf16_kv_append(
+    const void* x, int32_t x_kind, const void* w_packed, void* y, int32_t m,
+    int32_t n, int32_t k, void* workspace, size_t workspace_bytes,
+    const laminar_attn_desc* kv_desc, int32_t k_col, int32_t v_col,
+    const int32_t* block_table, const int32_t* seq_lens, void* k_pages,
+    void* v_pages, float* k_scale, float* v_scale, hipStream_t stream) {
+  if (!y || !kv_desc || x_kind == kXRmsNorm) return LAMINAR_ERR_INVALID_ARG;
+  if (kv_desc->batch != m) return LAMINAR_ERR_INVALID_ARG;
+  // the K and V columns: whole kv-heads inside y's rows, 16-byte aligned,
+  // not overlapping
+  const int64_t hd = int64_t(kv_desc->num_kv_heads) * kv_desc->head_dim;
+  if (k_col < 0 || v_col < 0 || k_col % 8 || v_col % 8 || k_col + hd > n ||
+      v_col + hd > n || (k_col < v_col + hd && v_col < k_col + hd))
+    return LAMINAR_ERR_INVALID_ARG;
+  laminar_attn_desc d = *kv_desc;
+  d.input_row_stride = n;
+  uint16_t* y16 = static_cast<uint16_t*>(y);
+  bool empty = false;
+  const laminar_status st = laminar_detail::kv_append_check(
+      &d, y16 + k_col, y16 + v_col, block_table, seq_lens, k_pages, v_pages,
+      k_scale, v_scale, &empty);
+  if (st != LAMINAR_OK) return st;
+  PostStep post;
+  post.kind = kPostAppend;
+  post.kv = &d;
+  post.k_col = k_col;
+  post.v_col = v_col;
+  post.block_table = block_table;
+  post.seq_lens = seq_lens;
+  post.k_pages = k_pages;
+  post.v_pages = v_pages;
+  post.k_scale = k_scale;
+  post.v_scale = v_scale;
   return linear_impl(x, x_kind, w_packed, nullptr, y, nullptr, m, n, k,
                      workspace, workspace_bytes, stream, nullptr, 0.f, post);
 }

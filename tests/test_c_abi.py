@@ -802,3 +802,38 @@ def test_kv_pack_errors_before_any_launch():
     assert pack(big, 2 * big, 1, 128, bf, 2, None) == N.LAMINAR_ERR_INVALID_ARG
     assert pack(big, 2 * big, 1, 128, 7, 0, None) == N.LAMINAR_ERR_INVALID_ARG
     assert pack(big, 2 * big, 1, 96, bf, 0, None) == N.LAMINAR_ERR_UNSUPPORTED
+
+
+def test_linear_kv_append_errors_before_any_launch():
+    """laminar_linear_bf16_kv_append refuses, before any launch, what
+    laminar_kv_append refuses and a description or K / V columns that do
+    not fit the product: NULL kv_desc, batch != M, columns not a multiple of
+    8, past N or overlapping."""
+    from paper_2510_12633_amd.api import kv_append_desc
+    lib = N.lib()
+    INV = N.LAMINAR_ERR_INVALID_ARG
+    m, n, k = 64, 4608, 3584
+    ws = N.laminar_linear_workspace_bytes(m, n, k)
+    good = dict(x=4096, kind=0, w=4096, y=4096, m=m, n=n, k=k, ws=4096,
+                wsb=ws, desc=kv_append_desc(m, 4, 128, 1024, 8), kc=3584,
+                vc=4096, table=4096, lens=4096, kp=4096, vp=4096)
+
+    def call(**over):
+        a = dict(good, **over)
+        d = a["desc"]
+        return lib.laminar_linear_bf16_kv_append(
+            a["x"], a["kind"], a["w"], a["y"], a["m"], a["n"], a["k"], a["ws"],
+            a["wsb"], ctypes.byref(d) if d is not None else None, a["kc"],
+            a["vc"], a["table"], a["lens"], a["kp"], a["vp"], None, None, None)
+
+    assert call(desc=None) == INV
+    assert call(desc=kv_append_desc(m - 1, 4, 128, 1024, 8)) == INV
+    assert call(kc=3588) == INV                 # not a multiple of 8
+    assert call(vc=4608 - 256) == INV           # V past N
+    assert call(kc=3584, vc=3584 + 256) == INV  # overlapping
+    assert call(kc=-8) == INV
+    assert call(table=4098) == INV              # as laminar_kv_append
+    assert call(kp=4104) == INV
+    assert call(lens=None) == INV
+    assert call(desc=kv_append_desc(m, 4, 96, 1024, 8)) == N.LAMINAR_ERR_UNSUPPORTED
+    assert call(desc=kv_append_desc(m, 4, 128, 1024, 8, "fp8_e4m3fn")) == INV

@@ -333,3 +333,79 @@ def test_norm_and_swiglu_outputs_equal_the_separate_launches(m, n, k):
     assert torch.equal(bits_t(ya), bits_t(yb)), (m, n, k)
     assert torch.equal(bits_t(act_a), bits_t(act_b)), (m, n, k)
     assert torch.isfinite(act_a.float()).all()
+
+
+APPEND_SHAPES = [
+    # (M, Hq, Hkv, D, K, pool dtype): QKV of 7B at 64 rows and of 32B at 40
+    # (the split's reduction stores K and V), at 16 rows (the split finished
+    # in the kernel) and 3 rows (the split over wavefronts), where the append
+    # is its own launch, and an fp8 pool (its own launch at any size)
+    (64, 28, 4, 128, 3584, "bf16"), (40, 40, 8, 128, 5120, "bf16"),
+    (16, 28, 4, 128, 3584, "bf16"), (3, 28, 4, 128, 3584, "bf16"),
+    (48, 8, 2, 64, 1024, "bf16"), (64, 28, 4, 128, 3584, "fp8_e4m3fn")]
+
+
+@pytest.mark.parametrize("m,hq,hkv,d,k,kv_dtype", APPEND_SHAPES)
+def test_qkv_with_kv_append_equals_the_separate_launches(m, hq, hkv, d, k,
+                                                         kv_dtype):
+    """laminar_linear_bf16_kv_append against laminar_linear_bf16_ex followed
+    by laminar_kv_append on y's K and V columns: y, both pools and the fp8
+    scales bit for bit, with a trajectory of length 0, one whose block lies
+    past the table and one whose table entry is -1 (nothing stored for any
+    of them), on fresh pools of random codes."""
+    from paper_2510_12633_amd.api import SkinnyLinear, kv_append, kv_append_desc
+    _need_gpu()
+    print(f"[gpu-linear-append] m={m} hq={hq} hkv={hkv} d={d} k={k} {kv_dtype}",
+          flush=True)
+    n = (hq + 2 * hkv) * d
+    g = torch.Generator(device="cuda").manual_seed(m + n + k)
+    w = (torch.randn((n, k), generator=g, device="cuda") / k ** 0.5).to(torch.bfloat16)
+    lin = SkinnyLinear(w)
+    x = torch.randn((m, k), generator=g, device="cuda").to(torch.bfloat16)
+    blocks = 6
+    pages = m * blocks
+    table = torch.randperm(pages, generator=g, device="cuda").to(torch.int32)
+    table = table.view(m, blocks).contiguous()
+    lens = torch.randint(1, blocks * 16 + 1, (m,), generator=g, device="cuda",
+                         dtype=torch.int32)
+    lens[0] = 0
+    lens[1] = blocks * 16 + 5                   # block past the table
+    t2 = int(lens[2].item()) - 1
+    table[2, t2 // 16] = -1                     # no page
+    fp8 = kv_dtype != "bf16"
+    if fp8:
+        kp = torch.randint(0, 0x78, (pages, hkv, 16 * d), generator=g,
+                           device="cuda", dtype=torch.uint8)
+        ks = (0.5 + torch.rand((pages, hkv), generator=g, device="cuda"))
+    else:
+        kp = torch.randn((pages, hkv, 16 * d), generator=g,
+                         device="cuda").to(torch.bfloat16)
+        ks = None
+    vp = kp.flip(0).contiguous()
+    vs = None if ks is None else ks.flip(0).contiguous()
+    kp2, vp2 = kp.clone(), vp.clone()
+    ks2 = None if ks is None else ks.clone()
+    vs2 = None if vs is None else vs.clone()
+    desc = kv_append_desc(m, hkv, d, pages, blocks, kv_dtype)
+    ya = lin.bf16_kv_append(x, desc, hq * d, (hq + hkv) * d, table, lens, kp,
+                            vp, ks, vs)
+    yb = lin.bf16(x)
+    kv_append(yb[:, hq * d:(hq + hkv) * d].view(m, hkv, d),
+              yb[:, (hq + hkv) * d:].view(m, hkv, d), table, lens, kp2, vp2,
+              ks2, vs2, kv_dtype=kv_dtype)
+    torch.cuda.synchronize()
+    assert torch.equal(bits_t(ya), bits_t(yb)), (m, n, k)
+    assert torch.equal(kp.view(torch.uint8), kp2.view(torch.uint8)), "K pool"
+    assert torch.equal(vp.view(torch.uint8), vp2.view(torch.uint8)), "V pool"
+    if fp8:
+        assert torch.equal(ks.view(torch.int32), ks2.view(torch.int32))
+        assert torch.equal(vs.view(torch.int32), vs2.view(torch.int32))
+    # the append did happen: the last trajectory's token is in its page
+    # (trajectories 0-2 store nothing)
+    t = int(lens[-1].item()) - 1
+    page = int(table[-1, t // 16].item())
+    if not fp8 and m > 3:
+        # V element (t, dim) of a tile at ((t / 4) D + dim) 4 + t % 4
+        vt = vp[page, 0]
+        got = vt[((t % 16) // 4) * d * 4 + (t % 4)::4][:d]
+        assert torch.equal(bits_t(got), bits_t(ya[-1, (hq + hkv) * d:(hq + hkv + 1) * d]))
