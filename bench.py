@@ -244,6 +244,39 @@ def calibrate(torch, N, nbytes=4 << 30, iters=10):
     return res
 
 
+def graph_launch_floor(torch, chain=100, reps=20):
+    """What one kernel costs in a captured graph when it does almost
+    nothing: a chain of `chain` in-place adds on 4 KiB and on 1 MiB,
+    captured once and replayed `reps` times; microseconds per kernel."""
+    side = torch.cuda.Stream()
+    res = {}
+    for label, nbytes in (("4KiB", 4096), ("1MiB", 1 << 20)):
+        x = torch.zeros(nbytes // 4, device="cuda")
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(3):
+                x.add_(1.0)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for _ in range(chain):
+                x.add_(1.0)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        res[label] = round(1e3 * e0.elapsed_time(e1) / (reps * chain), 2)
+        del g, x
+    return res
+
+
 def measure_append(torch, wl, steps=24):
     """Time the KV append (one launch per decode step) on this workload's
     pools, copied and grown by ``steps`` tokens per trajectory. Returns None
@@ -1038,6 +1071,9 @@ def main(argv=None):
         result["frac_of_calibrated_read"] = round(value * 1e3 / cal["read"], 4)
         result["frac_of_calibrated_gather"] = round(
             roofline["achieved"] / cal["gather_4KiB"], 4)
+        # the fixed cost of a kernel in a captured graph (the decode-step
+        # curve's floor per launch)
+        result["graph_launch_floor_us"] = graph_launch_floor(torch)
     if not args.no_per_config:
         rows = []
         for name in ALL_WORKLOADS:
