@@ -180,3 +180,86 @@ def test_fused_decode_step_equals_unfused(m):
         assert torch.equal(ta.view(torch.int16), tb.view(torch.int16))
     assert torch.isfinite(a[0].float()).all()
     att.close()
+
+
+@pytest.mark.parametrize("m", [40, 64])
+def test_reduction_fused_decode_step_equals_unfused(m):
+    """The same two-layer step from 33 rows on, where K is split and a
+    second kernel adds the ranges: once with every norm, SwiGLU and the KV
+    append as its own launch, once with each made by the preceding
+    projection's reduction (laminar_linear_bf16_kv_append for QKV,
+    laminar_linear_bf16_norm for O and down, laminar_linear_bf16_swiglu for
+    gate+up on the balanced split: 258 groups of 128 columns). Logits, the
+    residual stream and the KV pages agree bit for bit."""
+    from paper_2510_12633_amd import _native as N
+    from paper_2510_12633_amd.api import (PagedDecodeAttention, SkinnyLinear,
+                                          kv_append, kv_append_desc, rmsnorm,
+                                          silu_mul)
+    _need_gpu()
+    print(f"[gpu-decode-step] reduction-fused vs unfused m={m}", flush=True)
+    L, h, hq, hkv, d, inter, vocab = 2, 512, 8, 2, 64, 16512, 2048
+    g = torch.Generator(device="cuda").manual_seed(77 + m)
+    bf = torch.bfloat16
+
+    def lin(k, n):
+        return SkinnyLinear(rand_bf16(g, (n, k), k ** -0.5))
+
+    layers = [(lin(h, (hq + 2 * hkv) * d), lin(hq * d, h), lin(h, 2 * inter),
+               lin(inter, h)) for _ in range(L)]
+    head = lin(h, vocab)
+    # the reductions this step relies on do run at this size
+    assert N.laminar_linear_splits(m, (hq + 2 * hkv) * d, h) > 1
+    assert N.laminar_linear_splits(m, h, hq * d) > 1
+    assert N.laminar_linear_splits(m, h, inter) > 1
+    assert N.laminar_linear_workspace_bytes(m, 2 * inter, h) > 0     # balanced
+    norms = (1 + 0.1 * torch.randn((2 * L + 1, h), generator=g,
+                                   device="cuda")).to(bf)
+    ctx = 40
+    pages = -(-(ctx + 1) // 16)
+    kp0 = rand_bf16(g, (m * pages, hkv, 16 * d))
+    vp0 = rand_bf16(g, (m * pages, hkv, 16 * d))
+    table = torch.randperm(m * pages, generator=g, device="cuda").to(torch.int32)
+    table = table.view(m, pages).contiguous()
+    lens_host = np.full(m, ctx + 1, np.int32)
+    lens = torch.as_tensor(lens_host, device="cuda")
+    att = PagedDecodeAttention(
+        batch=m, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+        num_pages=m * pages, max_blocks_per_seq=pages, seq_lens_host=lens_host,
+        softmax_scale=d ** -0.5, q_row_stride=(hq + 2 * hkv) * d)
+    out, lse = att.outputs()
+    x0 = rand_bf16(g, (m, h))
+    desc = kv_append_desc(m, hkv, d, m * pages, pages)
+
+    def step(fused):
+        kp, vp = kp0.clone(), vp0.clone()
+        x = x0.clone()
+        xn = rmsnorm(x, norms[0])
+        for li, (wqkv, wo, wgu, wd) in enumerate(layers):
+            if fused:
+                qkv = wqkv.bf16_kv_append(xn, desc, hq * d, (hq + hkv) * d,
+                                          table, lens, kp, vp)
+            else:
+                qkv = wqkv.bf16(xn)
+                kv_append(qkv[:, hq * d:(hq + hkv) * d].view(m, hkv, d),
+                          qkv[:, (hq + hkv) * d:].view(m, hkv, d), table,
+                          lens, kp, vp)
+            att(qkv[:, :hq * d].view(m, hq, d), kp, vp, table, lens, out, lse)
+            a = out.view(m, hq * d)
+            if fused:
+                x, xn = wo.bf16_norm(a, norms[2 * li + 1], out=x, residual=x)
+                _, act = wgu.bf16_swiglu(xn)
+                x, xn = wd.bf16_norm(act, norms[2 * li + 2], out=x, residual=x)
+            else:
+                wo.bf16(a, out=x, residual=x)
+                act = silu_mul(wgu.bf16(rmsnorm(x, norms[2 * li + 1])))
+                wd.bf16(act, out=x, residual=x)
+                xn = rmsnorm(x, norms[2 * li + 2])
+        logits = head.bf16(xn)
+        torch.cuda.synchronize()
+        return logits, x, kp, vp
+
+    a, b = step(False), step(True)
+    for name, ta, tb in zip(("logits", "x", "k pages", "v pages"), a, b):
+        assert torch.equal(ta.view(torch.int16), tb.view(torch.int16)), name
+    assert torch.isfinite(a[0].float()).all()
+    att.close()
